@@ -1,0 +1,267 @@
+// Gradient-dropping oracle: TEST INFRASTRUCTURE ONLY.
+//
+// A plain, single-threaded, deliberately slow CPU statement of what the
+// compressor computes.  Only the test suite, the smoke check and the
+// benchmark's CPU-baseline leg may load it.  It shares no code, header or
+// constant with the HIP library and includes none of its files.
+//
+// Source: Aji & Heafield, "Sparse Communication for Distributed Gradient
+// Descent" (EMNLP 2017).
+//   * Section 4, Algorithm 1 (GradDrop): add the residual to the gradient,
+//     pick the threshold below which R% of |gradient| lies, keep the entries
+//     above it, leave the rest as the new residual, return the kept entries
+//     as a sparse (offset, value) list.
+//   * Section 4, last paragraph: the threshold is chosen either once over all
+//     parameters (global) or once per parameter matrix (local).
+//   * Section 4, paragraph on pulls: parameter pulls are sent as deltas from
+//     the last pulled copy, compressed the same way.
+//   * Section 5.4: 1-bit quantisation applied after dropping, with centres
+//     taken as averages of the values being quantised.
+//   * Section 3: a server owns a shard of the parameters and applies the
+//     pushed (sparse) gradients to it.
+//
+// Readings where the paper is silent (each also listed in the design notes):
+//   R1  k = floor(n * keep_ppm / 1e6) with keep_ppm = llround((1 - R) * 1e6).
+//   R2  exactly k entries are kept: the k largest keys, key = |acc| taken as
+//       the IEEE bit pattern with the sign cleared (so -0 ties +0, Inf is above
+//       every finite value and NaN above Inf).  Equal keys are taken in
+//       ascending flat index.  With distinct keys this is Algorithm 1 with the
+//       threshold set to the (k+1)-th largest magnitude.
+//   R3  the residual of a kept entry is exactly +0.0f; a dropped entry keeps
+//       acc's bits (the same as acc - dropped for finite values).
+//   R4  binary32 round-to-nearest-even, no fused multiply-add, denormals kept.
+//   R5  sign-mean quantisation is per tensor even under a global threshold:
+//       positives (acc not < 0, so zeros count as positive) and negatives are
+//       averaged separately as (sum in double, ascending index) / count,
+//       rounded to float; an empty group has centre 0.  The quantisation error
+//       acc - centre goes back into the residual.
+//   R6  server apply: s[i] = sum of the pushed values at i in client order
+//       (float adds starting from +0.0f), then p[i] = p[i] - lr * s[i].
+//   R7  pull delta: acc = (p_new - p_last) + residual, two float roundings.
+//
+// Build: g++ -O2 -ffp-contract=off -fPIC -shared (no fast-math).
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <functional>
+#include <vector>
+
+namespace {
+
+inline uint32_t key_of(float x) {
+    uint32_t b;
+    std::memcpy(&b, &x, sizeof b);
+#ifdef GDO_MUTANT_SIGNED_KEY
+    return b;  // mutant: compares raw bits, ignoring |.|
+#else
+    return b & 0x7FFFFFFFu;
+#endif
+}
+
+}  // namespace
+
+extern "C" {
+
+// R1: the keep fraction in parts per million.
+uint64_t gdo_keep_ppm(double drop_ratio) {
+    return (uint64_t)std::llround((1.0 - drop_ratio) * 1e6);
+}
+
+// R1: number of entries kept out of n.
+uint64_t gdo_keep_count(uint64_t n, double drop_ratio) {
+    uint64_t ppm = gdo_keep_ppm(drop_ratio);
+#ifdef GDO_MUTANT_CEIL_K
+    return (n * ppm + 999999u) / 1000000u;  // mutant: rounds k up
+#else
+    return n * ppm / 1000000u;
+#endif
+}
+
+// Algorithm 1 over the tensors described by offsets[0..T] (offsets[T] = N).
+// grad, base (nullable), residual: length N.  residual is read and rewritten.
+// Outputs (caller-allocated, capacity entries): idx, val; sign_bits
+// (ceil(capacity/32) words) and means (2*T) when quant != 0; tensor_counts (T).
+// Returns 0 on success, 1 on bad arguments, 3 when capacity is too small.
+int gdo_compress(const float* grad, const float* base, float* residual, const uint64_t* offsets,
+                 uint32_t T, double drop_ratio, int per_tensor, int quant, uint32_t* idx, float* val,
+                 uint32_t* sign_bits, float* means, uint32_t* tensor_counts, uint64_t capacity,
+                 uint64_t* out_k) {
+    if (!grad || !residual || !offsets || T == 0 || !idx || !val || !tensor_counts) return 1;
+    if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return 1;
+    if (quant && (!sign_bits || !means)) return 1;
+    const uint64_t N = offsets[T];
+    if (offsets[0] != 0 || N > 0xFFFFFFFFull) return 1;
+    for (uint32_t t = 0; t < T; ++t)
+        if (offsets[t + 1] < offsets[t]) return 1;
+
+    // Segments over which one threshold is chosen (Section 4: global or local).
+    std::vector<std::pair<uint64_t, uint64_t>> seg;
+    if (per_tensor) {
+        for (uint32_t t = 0; t < T; ++t) seg.push_back({offsets[t], offsets[t + 1]});
+    } else {
+        seg.push_back({0, N});
+    }
+    uint64_t k_total = 0;
+    for (auto& s : seg) {
+#ifdef GDO_MUTANT_GLOBAL_K_PER_TENSOR
+        k_total += std::min<uint64_t>(s.second - s.first, gdo_keep_count(N, drop_ratio) / seg.size());
+#else
+        k_total += gdo_keep_count(s.second - s.first, drop_ratio);
+#endif
+    }
+    if (out_k) *out_k = k_total;
+    if (capacity < k_total) return 3;
+
+    // Algorithm 1, first line: add the carried residual (pulls: delta first, R7).
+    std::vector<float> acc(N);
+    for (uint64_t i = 0; i < N; ++i) {
+        float g = grad[i];
+#ifdef GDO_MUTANT_DELTA_REVERSED
+        if (base) g = base[i] - g;
+#else
+        if (base) g = g - base[i];
+#endif
+#ifdef GDO_MUTANT_NO_RESIDUAL
+        acc[i] = g;
+#else
+        acc[i] = g + residual[i];
+#endif
+    }
+
+    // Algorithm 1, threshold selection and the keep mask (R2).
+    std::vector<uint8_t> keep(N, 0);
+    for (auto& s : seg) {
+        const uint64_t n = s.second - s.first;
+#ifdef GDO_MUTANT_GLOBAL_K_PER_TENSOR
+        const uint64_t k = std::min<uint64_t>(n, gdo_keep_count(N, drop_ratio) / seg.size());
+#else
+        const uint64_t k = gdo_keep_count(n, drop_ratio);
+#endif
+        if (k == 0) continue;
+        std::vector<uint32_t> keys(n);
+        for (uint64_t i = 0; i < n; ++i) keys[i] = key_of(acc[s.first + i]);
+        std::nth_element(keys.begin(), keys.begin() + (k - 1), keys.end(), std::greater<uint32_t>());
+        const uint32_t thr = keys[k - 1];  // the k-th largest key
+        uint64_t above = 0;
+        for (uint64_t i = s.first; i < s.second; ++i) above += key_of(acc[i]) > thr;
+        uint64_t ties_left = k - above;  // entries equal to thr still to take
+#ifdef GDO_MUTANT_STRICT_ONLY
+        ties_left = 0;  // mutant: Algorithm 1's strict ">" without the exact-k rule
+#endif
+#ifdef GDO_MUTANT_TIES_HIGH_INDEX
+        for (uint64_t i = s.second; i-- > s.first;) {
+#else
+        for (uint64_t i = s.first; i < s.second; ++i) {
+#endif
+            const uint32_t kk = key_of(acc[i]);
+            if (kk > thr) {
+                keep[i] = 1;
+            } else if (kk == thr && ties_left > 0) {
+                keep[i] = 1;
+                --ties_left;
+            }
+        }
+    }
+
+    // Algorithm 1, sparse(dropped): ascending flat indices and values.
+    uint64_t j = 0;
+    for (uint32_t t = 0; t < T; ++t) tensor_counts[t] = 0;
+    for (uint32_t t = 0; t < T; ++t) {
+        for (uint64_t i = offsets[t]; i < offsets[t + 1]; ++i) {
+            if (!keep[i]) continue;
+            idx[j] = (uint32_t)i;
+            val[j] = acc[i];
+            ++j;
+            ++tensor_counts[t];
+        }
+    }
+
+    // Algorithm 1, residual update (R3).
+    for (uint64_t i = 0; i < N; ++i) {
+#ifdef GDO_MUTANT_KEPT_RESIDUAL_KEEPS_ACC
+        residual[i] = acc[i];
+#else
+        residual[i] = keep[i] ? 0.0f : acc[i];
+#endif
+    }
+
+    // Section 5.4, sign-mean 1-bit quantisation with error feedback (R5).
+    if (quant) {
+        const uint64_t words = (k_total + 31) / 32;
+        for (uint64_t w = 0; w < words; ++w) sign_bits[w] = 0;
+        uint64_t first = 0;  // first output slot of tensor t
+        for (uint32_t t = 0; t < T; ++t) {
+            const uint64_t last = first + tensor_counts[t];
+            double pos_sum = 0.0, neg_sum = 0.0;
+            uint64_t pos_n = 0, neg_n = 0;
+            for (uint64_t q = first; q < last; ++q) {
+                if (val[q] < 0.0f) {
+                    neg_sum += (double)val[q];
+                    ++neg_n;
+                } else {
+                    pos_sum += (double)val[q];
+                    ++pos_n;
+                }
+            }
+            const float pos_c = pos_n ? (float)(pos_sum / (double)pos_n) : 0.0f;
+            const float neg_c = neg_n ? (float)(neg_sum / (double)neg_n) : 0.0f;
+#ifdef GDO_MUTANT_SWAP_CENTRES
+            means[2 * t + 0] = neg_c;
+            means[2 * t + 1] = pos_c;
+#else
+            means[2 * t + 0] = pos_c;
+            means[2 * t + 1] = neg_c;
+#endif
+            for (uint64_t q = first; q < last; ++q) {
+                const bool neg = val[q] < 0.0f;
+#ifdef GDO_MUTANT_BITS_MSB_FIRST
+                if (neg) sign_bits[q >> 5] |= 1u << (31 - (q & 31));
+#else
+                if (neg) sign_bits[q >> 5] |= 1u << (q & 31);
+#endif
+                const float sent = neg ? means[2 * t + 1] : means[2 * t + 0];
+                residual[idx[q]] = val[q] - sent;
+            }
+            first = last;
+        }
+    }
+    return 0;
+}
+
+// Section 3: a server applies sparse pushes to its parameter shard (R6).
+// idx[c] (ascending, unique within a client) and val[c] hold nnz[c] entries.
+// Returns 0 on success, 1 on bad arguments (including an index >= n).
+int gdo_apply_sparse(float* params, uint64_t n, uint32_t C, const uint32_t* const* idx,
+                     const float* const* val, const uint64_t* nnz, float lr) {
+    if (!params || (C && (!idx || !val || !nnz))) return 1;
+    for (uint32_t c = 0; c < C; ++c)
+        for (uint64_t j = 0; j < nnz[c]; ++j)
+            if (idx[c][j] >= n) return 1;
+    std::vector<float> s(n, 0.0f);
+    std::vector<uint8_t> touched(n, 0);
+#ifdef GDO_MUTANT_APPLY_REVERSE_CLIENTS
+    for (uint32_t c = C; c-- > 0;) {
+#else
+    for (uint32_t c = 0; c < C; ++c) {
+#endif
+        for (uint64_t j = 0; j < nnz[c]; ++j) {
+            const uint32_t i = idx[c][j];
+            s[i] = s[i] + val[c][j];
+            touched[i] = 1;
+        }
+    }
+    for (uint64_t i = 0; i < n; ++i) {
+        if (!touched[i]) continue;
+        const float step = lr * s[i];
+#ifdef GDO_MUTANT_APPLY_ADD
+        params[i] = params[i] + step;
+#else
+        params[i] = params[i] - step;
+#endif
+    }
+    return 0;
+}
+
+}  // extern "C"

@@ -1,0 +1,379 @@
+"""Pins for the CPU oracle: checks that do not re-use the oracle's own code.
+
+Each ``pin_*`` function takes a loaded oracle library and raises
+``AssertionError`` when the oracle disagrees with something the paper or the
+mathematics fixes:
+
+* hand-worked examples of Algorithm 1 (``golden/hand_examples.json``),
+* brute force by full sort on tiny inputs (exhaustive) and on random inputs
+  with heavy ties,
+* the closed form of k and the kept-count stated for the 784-512-512-10 MLP,
+* invariants that hold for any input,
+* exact rational arithmetic (``fractions.Fraction``) for the quantisation
+  centres and the server apply.
+
+The same functions run against deliberately broken builds of the oracle in
+``test_oracle_mutants.py``: every planted mistake must trip at least one pin.
+"""
+from __future__ import annotations
+
+import itertools
+import json
+import math
+import os
+from fractions import Fraction
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "hand_examples.json")
+
+
+def f32(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float32)
+
+
+def bits(a) -> np.ndarray:
+    return f32(a).view(np.uint32)
+
+
+def keys(a) -> np.ndarray:
+    return bits(a) & np.uint32(0x7FFFFFFF)
+
+
+# ---------------------------------------------------------------------------
+# brute force: full sort by (|acc| descending, index ascending)
+# ---------------------------------------------------------------------------
+
+def brute_keep(acc: np.ndarray, offsets: Sequence[int], keep_ppm: int, per_tensor: bool) -> np.ndarray:
+    """Keep mask from a full sort; magnitudes compared as Python floats (finite inputs)."""
+    keep = np.zeros(acc.size, dtype=bool)
+    segs = [(offsets[t], offsets[t + 1]) for t in range(len(offsets) - 1)] if per_tensor else [(0, acc.size)]
+    for a, b in segs:
+        n = b - a
+        k = n * keep_ppm // 1_000_000
+        order = sorted(range(a, b), key=lambda i: (-abs(float(acc[i])), i))
+        keep[order[:k]] = True
+    return keep
+
+
+def check_against_brute(lib, grad, residual, offsets, keep_ppm, per_tensor):
+    drop = 1.0 - keep_ppm / 1e6
+    acc = f32(grad) + f32(residual)
+    out = oracle.compress(grad, residual, offsets, drop, per_tensor=per_tensor, lib=lib)
+    keep = brute_keep(acc, offsets, keep_ppm, per_tensor)
+    want_idx = np.nonzero(keep)[0].astype(np.uint32)
+    assert np.array_equal(out.idx, want_idx), (out.idx, want_idx)
+    assert np.array_equal(bits(out.val), bits(acc[want_idx]))
+    want_res = np.where(keep, np.float32(0.0), acc).astype(np.float32)
+    assert np.array_equal(bits(out.residual), bits(want_res))
+    T = len(offsets) - 1
+    want_counts = [int(keep[offsets[t]:offsets[t + 1]].sum()) for t in range(T)]
+    assert list(out.tensor_counts) == want_counts
+
+
+# ---------------------------------------------------------------------------
+# invariants (hold for every input)
+# ---------------------------------------------------------------------------
+
+def check_invariants(acc: np.ndarray, offsets, keep_ppm: int, per_tensor: bool, idx, val, residual, counts):
+    """Properties any correct exact-k gradient drop must satisfy (finite or not)."""
+    N = acc.size
+    segs = [(offsets[t], offsets[t + 1]) for t in range(len(offsets) - 1)] if per_tensor else [(0, N)]
+    idx = np.asarray(idx, dtype=np.int64)
+    assert np.all(np.diff(idx) > 0), "indices must be strictly ascending"
+    kept = np.zeros(N, dtype=bool)
+    kept[idx] = True
+    kk = keys(acc)
+    k_total = 0
+    for a, b in segs:
+        n = b - a
+        k = n * keep_ppm // 1_000_000
+        k_total += k
+        seg_kept = kept[a:b]
+        assert int(seg_kept.sum()) == k, "kept count must equal k"
+        if 0 < k < n:
+            kmin = kk[a:b][seg_kept].min()
+            kmax = kk[a:b][~seg_kept].max()
+            assert kmin >= kmax, "a dropped |value| exceeds a kept one"
+            if kmin == kmax:  # ties at the threshold: kept ones come first
+                tie = np.nonzero(kk[a:b] == kmin)[0]
+                tk = seg_kept[tie]
+                assert np.all(tk[:int(tk.sum())]) and not np.any(tk[int(tk.sum()):]), "ties not by lower index"
+    assert idx.size == k_total
+    assert int(np.asarray(counts, dtype=np.int64).sum()) == k_total
+    # sent + residual == acc, bit for bit
+    assert np.array_equal(bits(val), bits(acc[idx]))
+    assert np.all(bits(residual)[kept] == 0), "kept residual must be +0.0"
+    assert np.array_equal(bits(residual)[~kept], bits(acc)[~kept])
+
+
+# ---------------------------------------------------------------------------
+# exact rational helpers
+# ---------------------------------------------------------------------------
+
+def ulp32(x: np.float32) -> Fraction:
+    x = np.float32(abs(x))
+    up = np.nextafter(x, np.float32(np.inf))
+    return Fraction(float(up)) - Fraction(float(x))
+
+
+def within_half_ulp(got: np.float32, exact: Fraction) -> bool:
+    g = Fraction(float(np.float32(got)))
+    return abs(g - exact) <= ulp32(np.float32(got)) / 2 * Fraction(1000001, 1000000)
+
+
+# ---------------------------------------------------------------------------
+# pins
+# ---------------------------------------------------------------------------
+
+def pin_keep_count(lib):
+    # the 784-512-512-10 MLP gradient (669,706 entries) keeps 6,697 at a 99% drop
+    assert oracle.keep_count(669_706, 0.99, lib) == 6_697
+    # closed form floor(n * (1 - R)) in exact arithmetic for decimal drop ratios
+    for n in (0, 1, 7, 8, 99, 100, 101, 12345, 37_000_000, 42_500_000):
+        for r in ("0", "0.5", "0.9", "0.99", "0.999", "0.625", "1"):
+            want = math.floor(n * (1 - Fraction(r)))
+            assert oracle.keep_count(n, float(r), lib) == want, (n, r)
+    # R = 1/3 is quantised to 666,667 parts per million of kept entries
+    assert oracle.keep_count(6, 1 / 3, lib) == 4
+    assert oracle.keep_count(3_000_000, 1 / 3, lib) == 2_000_001
+
+
+def pin_golden_compress(lib):
+    with open(GOLDEN) as f:
+        gold = json.load(f)
+    for case in gold["compress"]:
+        res = None
+        for st in case["steps"]:
+            r_in = res if st["residual_in"] == "previous" else f32(st["residual_in"])
+            out = oracle.compress(f32(st["grad"]), r_in, case["offsets"], case["drop"],
+                                  per_tensor=case.get("per_tensor", False), quant=case.get("quant", False), lib=lib)
+            assert out.idx.tolist() == st["idx"], (case["name"], out.idx)
+            assert np.array_equal(bits(out.val), bits(st["val"])), case["name"]
+            assert np.array_equal(bits(out.residual), bits(st["residual_out"])), (case["name"], out.residual)
+            assert out.tensor_counts.tolist() == st["tensor_counts"], case["name"]
+            if "sign_bits" in st:
+                assert out.sign_bits.tolist() == st["sign_bits"], case["name"]
+                assert np.array_equal(bits(out.means), bits(st["means"])), case["name"]
+            res = out.residual
+
+
+def pin_golden_apply(lib):
+    with open(GOLDEN) as f:
+        gold = json.load(f)
+    for case in gold["apply"]:
+        p0 = f32(case["params"])
+        idx = [np.array(pi, np.uint32) for pi, _ in case["pushes"]]
+        val = [f32(pv) for _, pv in case["pushes"]]
+        p1 = oracle.apply_sparse(p0, idx, val, case["lr"], lib=lib)
+        assert np.array_equal(bits(p1), bits(case["params_out"])), (case["name"], p1)
+        if "pull" in case:
+            pl = case["pull"]
+            out = oracle.compress(p1, np.zeros_like(p1), [0, p1.size], pl["drop"], base=p0, lib=lib)
+            assert out.idx.tolist() == pl["idx"]
+            assert np.array_equal(bits(out.val), bits(pl["val"]))
+            assert np.array_equal(bits(out.residual), bits(pl["residual_out"]))
+
+
+def pin_brute_exhaustive(lib):
+    """Every vector of length <= 4 over {0, -0, +-1, +-2} and every k."""
+    alphabet = [0.0, -0.0, 1.0, -1.0, 2.0, -2.0]
+    for n in range(1, 5):
+        for vec in itertools.product(alphabet, repeat=n):
+            g = f32(vec)
+            z = np.zeros(n, np.float32)
+            for k in range(n + 1):
+                # smallest ppm giving exactly k of n
+                ppm = -(-k * 1_000_000 // n)
+                check_against_brute(lib, g, z, [0, n], ppm, False)
+
+
+def pin_brute_random_ties(lib):
+    rng = np.random.default_rng(12345)
+    for trial in range(60):
+        T = int(rng.integers(1, 6))
+        sizes = rng.integers(0, 400, size=T)
+        if trial % 7 == 0:
+            sizes[rng.integers(0, T)] = 0
+        offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64).tolist()
+        N = offsets[-1]
+        if N == 0:
+            continue
+        levels = f32([0.0, 0.25, 0.5, 1.0, 1.5, 3.0, 1e-3, 2.0 ** -130])
+        g = levels[rng.integers(0, levels.size, N)] * np.where(rng.random(N) < 0.5, -1, 1).astype(np.float32)
+        r = (levels[rng.integers(0, levels.size, N)] * np.where(rng.random(N) < 0.5, -1, 1)).astype(np.float32)
+        r[rng.random(N) < 0.5] = 0.0
+        ppm = int(rng.choice([0, 1_000, 10_000, 100_000, 333_334, 500_000, 900_000, 1_000_000]))
+        per = bool(trial % 2)
+        check_against_brute(lib, g, r, offsets, ppm, per)
+        out = oracle.compress(g, r, offsets, 1 - ppm / 1e6, per_tensor=per, lib=lib)
+        check_invariants(g + r, offsets, ppm, per, out.idx, out.val, out.residual, out.tensor_counts)
+
+
+def pin_invariants_large(lib):
+    """Gaussian and heavy-tailed draws at a 99% drop, several tensors, both modes."""
+    rng = np.random.default_rng(7)
+    offsets = [0, 50_000, 50_017, 120_000, 120_000, 200_003]
+    N = offsets[-1]
+    g = (rng.standard_t(3, N) * 1e-3).astype(np.float32)
+    r = (rng.normal(0, 1e-3, N)).astype(np.float32)
+    for per in (False, True):
+        out = oracle.compress(g, r, offsets, 0.99, per_tensor=per, lib=lib)
+        check_invariants(g + r, offsets, 10_000, per, out.idx, out.val, out.residual, out.tensor_counts)
+
+
+def pin_special_cases(lib):
+    rng = np.random.default_rng(3)
+    g = rng.normal(0, 1, 1000).astype(np.float32)
+    r = rng.normal(0, 1, 1000).astype(np.float32)
+    acc = g + r
+    # R = 0 keeps everything, residual all +0
+    out = oracle.compress(g, r, [0, 1000], 0.0, lib=lib)
+    assert out.idx.tolist() == list(range(1000)) and np.all(bits(out.residual) == 0)
+    # R = 1 keeps nothing, residual is acc
+    out = oracle.compress(g, r, [0, 1000], 1.0, lib=lib)
+    assert out.idx.size == 0 and np.array_equal(bits(out.residual), bits(acc))
+    # one tensor: per-tensor equals global
+    a = oracle.compress(g, r, [0, 1000], 0.9, per_tensor=False, lib=lib)
+    b = oracle.compress(g, r, [0, 1000], 0.9, per_tensor=True, lib=lib)
+    assert np.array_equal(a.idx, b.idx) and np.array_equal(bits(a.residual), bits(b.residual))
+    # all zeros: the lowest indices are kept
+    z = np.zeros(100, np.float32)
+    out = oracle.compress(z, z, [0, 100], 0.9, lib=lib)
+    assert out.idx.tolist() == list(range(10))
+    # equal magnitudes with random signs: indices 0..k-1
+    s = np.where(rng.random(100) < 0.5, -0.75, 0.75).astype(np.float32)
+    out = oracle.compress(s, z, [0, 100], 0.95, lib=lib)
+    assert out.idx.tolist() == list(range(5))
+    # Inf above finite, NaN above Inf; +-Inf tie by index
+    v = f32([1.0, np.inf, np.nan, -np.inf, 2.0])
+    out = oracle.compress(v, np.zeros(5, np.float32), [0, 5], 0.6, lib=lib)
+    assert out.idx.tolist() == [1, 2]
+    out = oracle.compress(v, np.zeros(5, np.float32), [0, 5], 0.4, lib=lib)
+    assert out.idx.tolist() == [1, 2, 3]
+    # signed zeros: -0 + -0 = -0 keeps its sign bit; -0 + +0 = +0
+    gz = f32([-0.0, 0.0, -0.0])
+    rz = f32([-0.0, -0.0, 0.0])
+    out = oracle.compress(gz, rz, [0, 3], 0.6666, lib=lib)  # keep_ppm 333400 -> k = 1
+    assert out.idx.tolist() == [0] and bits(out.val).tolist() == [0x80000000]
+    assert bits(out.residual).tolist() == [0, 0, 0]
+    # denormals survive the add and the copy
+    d = f32([2.0 ** -149, -(2.0 ** -148), 2.0 ** -140, 0.0])
+    out = oracle.compress(d, d, [0, 4], 0.5, lib=lib)
+    assert out.idx.tolist() == [1, 2]
+    assert np.array_equal(bits(out.val), bits(f32([-(2.0 ** -147), 2.0 ** -139])))
+    assert np.array_equal(bits(out.residual), bits(f32([2.0 ** -148, 0, 0, 0])))
+
+
+def pin_quant_exact(lib):
+    """Sign-mean centres and residuals against exact rational arithmetic."""
+    rng = np.random.default_rng(11)
+    offsets = [0, 700, 701, 1500, 1500, 2600]
+    N = offsets[-1]
+    for trial in range(6):
+        g = (rng.standard_t(3, N) * 10.0 ** rng.uniform(-4, 0)).astype(np.float32)
+        r = rng.normal(0, 1e-3, N).astype(np.float32)
+        per = bool(trial % 2)
+        out = oracle.compress(g, r, offsets, 0.9, per_tensor=per, quant=True, lib=lib)
+        acc = g + r
+        k = out.idx.size
+        first = 0
+        for t in range(len(offsets) - 1):
+            last = first + int(out.tensor_counts[t])
+            v = out.val[first:last]
+            assert np.array_equal(bits(v), bits(acc[out.idx[first:last]]))
+            pos = [Fraction(float(x)) for x in v if not (x < 0)]
+            neg = [Fraction(float(x)) for x in v if x < 0]
+            mp, mn = out.means[2 * t], out.means[2 * t + 1]
+            assert mp >= 0 >= mn
+            if pos:
+                assert within_half_ulp(mp, sum(pos) / len(pos)), (t, mp)
+            else:
+                assert bits([mp])[0] == 0
+            if neg:
+                assert within_half_ulp(mn, sum(neg) / len(neg)), (t, mn)
+            else:
+                assert bits([mn])[0] == 0
+            for q in range(first, last):
+                neg_q = bool(out.val[q] < 0)
+                bit = (int(out.sign_bits[q >> 5]) >> (q & 31)) & 1
+                assert bit == int(neg_q)
+                centre = mn if neg_q else mp
+                res = out.residual[out.idx[q]]
+                assert within_half_ulp(res, Fraction(float(out.val[q])) - Fraction(float(centre)))
+            first = last
+        assert first == k
+        # bits beyond k are zero
+        if k % 32:
+            assert int(out.sign_bits[-1]) >> (k % 32) == 0
+        # dropped residuals untouched by quantisation
+        dropped = np.ones(N, bool)
+        dropped[out.idx] = False
+        assert np.array_equal(bits(out.residual[dropped]), bits(acc[dropped]))
+
+
+def pin_apply_exact(lib):
+    rng = np.random.default_rng(5)
+    n = 5000
+    p = rng.normal(0, 0.1, n).astype(np.float32)
+    # no duplicates, lr = 1: one rounding, p - v
+    ix = np.sort(rng.choice(n, 300, replace=False)).astype(np.uint32)
+    v = (rng.standard_t(3, 300) * 1e-3).astype(np.float32)
+    got = oracle.apply_sparse(p, [ix], [v], 1.0, lib=lib)
+    want = p.copy()
+    want[ix] = p[ix] - v
+    assert np.array_equal(bits(got), bits(want))
+    # duplicates across 4 clients: within a few ulps of the exact rational result
+    idx, val = [], []
+    for c in range(4):
+        ixc = np.sort(rng.choice(400, 120, replace=False)).astype(np.uint32)
+        idx.append(ixc)
+        val.append((rng.standard_t(3, 120) * 1e-3).astype(np.float32))
+    lr = np.float32(0.5)
+    got = oracle.apply_sparse(p, idx, val, float(lr), lib=lib)
+    exact: Dict[int, Fraction] = {}
+    for ixc, vc in zip(idx, val):
+        for i, x in zip(ixc.tolist(), vc.tolist()):
+            exact[i] = exact.get(i, Fraction(0)) + Fraction(x)
+    touched = np.zeros(n, bool)
+    for i, s in exact.items():
+        touched[i] = True
+        want = Fraction(float(p[i])) - Fraction(float(lr)) * s
+        tol = 8 * ulp32(np.float32(abs(float(p[i])) + float(lr) * sum(abs(float(vc[j])) for ixc, vc in zip(idx, val)
+                                                                 for j in np.nonzero(ixc == i)[0])))
+        assert abs(Fraction(float(got[i])) - want) <= tol, i
+    assert np.array_equal(bits(got[~touched]), bits(p[~touched]))
+
+
+def pin_pull_delta(lib):
+    rng = np.random.default_rng(9)
+    p0 = rng.normal(0, 0.1, 3000).astype(np.float32)
+    p1 = p0.copy()
+    ix = rng.choice(3000, 200, replace=False)
+    p1[ix] -= rng.normal(0, 1e-2, 200).astype(np.float32)
+    res = rng.normal(0, 1e-4, 3000).astype(np.float32)
+    delta = p1 - p0
+    a = oracle.compress(p1, res, [0, 3000], 0.99, base=p0, lib=lib)
+    b = oracle.compress(delta, res, [0, 3000], 0.99, lib=lib)
+    assert np.array_equal(a.idx, b.idx) and np.array_equal(bits(a.residual), bits(b.residual))
+    assert np.any(delta != 0)
+    # a 99% drop of the delta keeps the 30 largest |delta + residual|
+    acc = delta + res
+    check_invariants(acc, [0, 3000], 10_000, False, a.idx, a.val, a.residual, a.tensor_counts)
+
+
+ALL_PINS = [
+    pin_keep_count,
+    pin_golden_compress,
+    pin_golden_apply,
+    pin_brute_exhaustive,
+    pin_brute_random_ties,
+    pin_invariants_large,
+    pin_special_cases,
+    pin_quant_exact,
+    pin_apply_exact,
+    pin_pull_delta,
+]

@@ -1,0 +1,43 @@
+"""Planted mistakes in the oracle must each trip at least one pin.
+
+Every mutant is the oracle source compiled with one ``-DGDO_MUTANT_*`` define
+(a dropped term, a wrong sign, a reversed order, an off-by-one k, ...).  This
+shows the pins in ``pins.py`` are strong enough to catch the plausible ways
+of getting the definition wrong.  Mutants exist only in the test build; the
+oracle library used everywhere else is compiled without any of them.
+"""
+import pytest
+
+import oracle
+from pins import ALL_PINS
+
+MUTANTS = [
+    "GDO_MUTANT_SIGNED_KEY",
+    "GDO_MUTANT_CEIL_K",
+    "GDO_MUTANT_GLOBAL_K_PER_TENSOR",
+    "GDO_MUTANT_NO_RESIDUAL",
+    "GDO_MUTANT_STRICT_ONLY",
+    "GDO_MUTANT_TIES_HIGH_INDEX",
+    "GDO_MUTANT_KEPT_RESIDUAL_KEEPS_ACC",
+    "GDO_MUTANT_SWAP_CENTRES",
+    "GDO_MUTANT_BITS_MSB_FIRST",
+    "GDO_MUTANT_APPLY_REVERSE_CLIENTS",
+    "GDO_MUTANT_APPLY_ADD",
+    "GDO_MUTANT_DELTA_REVERSED",
+]
+
+
+def failing_pins(lib):
+    failed = []
+    for pin in ALL_PINS:
+        try:
+            pin(lib)
+        except (AssertionError, ValueError, IndexError):
+            failed.append(pin.__name__)
+    return failed
+
+
+@pytest.mark.parametrize("mutant", MUTANTS)
+def test_mutant_is_caught(mutant):
+    lib = oracle.build_variant([mutant])
+    assert failing_pins(lib), f"{mutant} passed every pin"
