@@ -1,0 +1,164 @@
+/*
+ * gd.h - C ABI of the gradient-dropping compressor for AMD Instinct MI355X (gfx950).
+ *
+ * Aji & Heafield, "Sparse Communication for Distributed Gradient Descent"
+ * (EMNLP 2017).  Each call of gd_compress is one application of Algorithm 1
+ * (GradDrop, Section 4) to a worker's gradient: add the carried residual, pick
+ * the threshold that drops R of |gradient|, send the survivors as a sparse
+ * (offset, value) list and keep the rest as the next residual.  The threshold
+ * is global or per tensor (Section 4, last paragraph); survivors may be 1-bit
+ * quantised to per-tensor averages (Section 5.4); pulls are compressed as
+ * deltas from the last pulled copy (Section 4, paragraph on pulls).
+ * gd_apply_sparse is the server side of the sharded exchange (Section 3).
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers named "device" are HIP device allocations owned by the caller;
+ *     pointers named "host" are ordinary host memory.  The library never
+ *     frees or keeps a caller pointer beyond the call.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL means the default
+ *     stream) and the call returns without waiting for it.  No entry point
+ *     synchronises the host with the device.
+ *   - Argument, layout, alignment and capacity errors are reported before
+ *     anything is enqueued and leave every buffer untouched.  GD_ERR_HIP means
+ *     a launch failed; outputs and residual are then undefined.
+ *   - Floating point is IEEE binary32 with round-to-nearest-even, no fused
+ *     multiply-add and denormals preserved.
+ */
+#ifndef GD_H
+#define GD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GD_OK = 0,
+    GD_ERR_ARG = 1,      /* null pointer, drop ratio outside [0,1], bad enum */
+    GD_ERR_LAYOUT = 2,   /* offsets not starting at 0, decreasing, or N >= 2^32 */
+    GD_ERR_CAPACITY = 3, /* output capacity below the number of kept entries */
+    GD_ERR_ALIGN = 4,    /* grad, base or residual not 16-byte aligned */
+    GD_ERR_OOM = 5,      /* device scratch allocation failed (gd_create only) */
+    GD_ERR_HIP = 6       /* a HIP runtime call or kernel launch failed */
+} gd_status;
+
+/* Where one threshold is chosen (Section 4, last paragraph). */
+typedef enum {
+    GD_GLOBAL = 0,    /* one threshold over all tensors of the layout */
+    GD_PER_TENSOR = 1 /* one threshold per tensor ("per parameter matrix") */
+} gd_threshold;
+
+/* What is sent for the survivors (Section 5.4). */
+typedef enum {
+    GD_QUANT_NONE = 0,     /* (index, value) pairs */
+    GD_QUANT_SIGN_MEAN = 1 /* indices + one sign bit each + two centres per tensor */
+} gd_quant;
+
+/* Opaque handle: the tensor layout and the device scratch the kernels use.
+ * It owns no caller data; the compressor's only state is the caller's
+ * residual buffer. */
+typedef struct gd_ctx gd_ctx;
+
+/*
+ * gd_create - describe a gradient made of T tensors laid end to end.
+ *   tensor_offsets (host, T+1 entries): tensor t occupies flat indices
+ *     [tensor_offsets[t], tensor_offsets[t+1]); tensor_offsets[0] must be 0,
+ *     the sequence non-decreasing (empty tensors are allowed) and
+ *     N = tensor_offsets[T] below 2^32 (indices are sent as uint32).
+ *   Allocates all device scratch on the current HIP device (about 8 bytes per
+ *   element plus small tables); gd_compress never allocates.
+ *   Returns GD_ERR_LAYOUT for a bad layout, GD_ERR_OOM when allocation fails.
+ */
+gd_status gd_create(gd_ctx** out, const uint64_t* tensor_offsets, uint32_t num_tensors);
+
+/* Frees the scratch.  The caller must make sure no enqueued call still uses it. */
+void gd_destroy(gd_ctx* ctx);
+
+/*
+ * Number of entries kept out of n at drop ratio R (Algorithm 1: "R% of |grad|
+ * is smaller").  R is taken in parts per million: keep_ppm = round((1-R)*1e6)
+ * and k = floor(n * keep_ppm / 1e6).  Returns 0 for R outside [0,1].
+ */
+uint64_t gd_keep_count(uint64_t n, double drop_ratio);
+
+/* Total kept entries of one gd_compress call: k(N) for GD_GLOBAL, the sum of
+ * k(n_t) over tensors for GD_PER_TENSOR.  This is the exact output size. */
+uint64_t gd_keep_total(const gd_ctx* ctx, double drop_ratio, gd_threshold mode);
+
+/* Output buffers of gd_compress (all device pointers, caller-owned). */
+typedef struct {
+    uint32_t* idx;           /* [capacity] kept flat indices, ascending */
+    float* val;              /* [capacity] kept values acc[idx] (before quantisation) */
+    uint32_t* sign_bits;     /* GD_QUANT_SIGN_MEAN: [ceil(capacity/32)] words, bit j of
+                                word j/32 (LSB first) set when kept value j is negative;
+                                unused bits are 0.  Ignored for GD_QUANT_NONE. */
+    float* means;            /* GD_QUANT_SIGN_MEAN: [2*T] (positive centre, negative centre)
+                                per tensor.  Ignored for GD_QUANT_NONE. */
+    uint32_t* tensor_counts; /* [T] kept entries per tensor */
+    uint64_t capacity;       /* host value: entries idx/val can hold, >= gd_keep_total() */
+} gd_sparse;
+
+/*
+ * gd_compress - one application of Algorithm 1 (Section 4).
+ *   grad (device, N floats): the fresh gradient.  For a pull, the server's
+ *     current parameters.
+ *   base (device, N floats, or NULL): for a pull, the last pulled copy; the
+ *     compressed quantity is then grad - base (Section 4, paragraph on pulls).
+ *   residual (device, N floats, in/out): the carried residual.  On return it
+ *     holds the new residual: +0.0 at kept entries (or acc minus the sent
+ *     centre under GD_QUANT_SIGN_MEAN) and acc elsewhere.
+ *   With acc = (grad [- base]) + residual, exactly k entries are kept per
+ *   threshold segment: the k largest |acc|, equal magnitudes taken in
+ *   ascending flat index (so -0 ties +0; Inf ranks above finite values and
+ *   NaN above Inf).  Outputs are written in ascending index order.
+ *   grad, base and residual must be 16-byte aligned and must not overlap each
+ *   other or the outputs.  One call at a time per ctx (calls on one stream are
+ *   naturally ordered).
+ */
+gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* residual,
+                      double drop_ratio, gd_threshold mode, gd_quant quant, const gd_sparse* out,
+                      void* stream);
+
+/*
+ * gd_apply_sparse - server-side apply of sparse pushes to a parameter shard
+ * (Section 3: servers own a shard and receive the clients' pieces).
+ *   params (device, n floats, in/out).
+ *   idx, val (host arrays of num_pushes device pointers): push c holds nnz[c]
+ *     (host) entries; its indices must be ascending and unique within the push
+ *     and below n (entries at an index >= n are skipped).
+ *   For every index i that appears in any push: s = sum of the pushed values
+ *   at i, added in push order starting from +0.0; params[i] -= lr * s.
+ *   num_pushes may be 0 (nothing happens); at most 64 pushes per call.
+ *   The result is deterministic.
+ */
+gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const uint32_t* const* idx,
+                          const float* const* val, const uint64_t* nnz, float lr, void* stream);
+
+/* Static description of a status code. */
+const char* gd_status_string(gd_status status);
+
+/*
+ * Timing of the dense pass (the kernel that streams grad and residual).
+ * When enabled, gd_compress records a HIP event pair around that kernel on
+ * the call's stream.  gd_profile_read waits for the recorded events, returns
+ * the summed milliseconds and the number of launches, and resets both.
+ */
+gd_status gd_profile_enable(gd_ctx* ctx, int enable);
+gd_status gd_profile_read(gd_ctx* ctx, double* dense_ms, uint64_t* dense_launches);
+
+/*
+ * Test hook: override the sampled threshold bracket of later gd_compress
+ * calls on this ctx, to exercise paths that real samples rarely take.  The
+ * results do not change (they are exact whatever the bracket); only the
+ * work done does.  mode 0: normal; 1: bracket above every key, so every
+ * segment takes the exact fallback; 2: the dense pass zeroes every
+ * candidate; 3: every element is a candidate.  GD_ERR_ARG for other modes.
+ */
+gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GD_H */

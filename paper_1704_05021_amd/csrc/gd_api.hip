@@ -1,0 +1,366 @@
+// C ABI of the gradient-dropping compressor: argument checks, layout tables,
+// scratch ownership and the launch sequence.  The operations are defined in
+// include/gd.h; the kernels are in gd_kernels.hip.
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "gd.h"
+#include "gd_internal.h"
+#include "gd_kernels.h"
+
+namespace {
+
+using gd::kMaxUnits;
+using gd::kUnit;
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) return;
+        ok = prev == dev || hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+uint64_t keep_ppm_of(double drop_ratio) { return (uint64_t)std::llround((1.0 - drop_ratio) * 1e6); }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Units of 16 elements sampled for a segment [a, b) and the number of sample keys stored.
+uint32_t sample_keys_for(uint64_t a, uint64_t b) {
+    if (b <= a) return 0;
+    const uint64_t n16 = ((b - 1) >> 4) - (a >> 4) + 1;
+    return (uint32_t)(kUnit * std::min<uint64_t>(n16, kMaxUnits));
+}
+
+template <typename T>
+bool dev_alloc(gd_ctx* ctx, T** p, size_t count) {
+    void* q = nullptr;
+    if (hipMalloc(&q, std::max<size_t>(count, 1) * sizeof(T)) != hipSuccess) return false;
+    ctx->allocations.push_back(q);
+    *p = static_cast<T*>(q);
+    return true;
+}
+
+template <typename T>
+bool dev_upload(gd_ctx* ctx, T** p, const std::vector<T>& v) {
+    if (!dev_alloc(ctx, p, v.size())) return false;
+    if (v.empty()) return true;
+    return hipMemcpy(*p, v.data(), v.size() * sizeof(T), hipMemcpyHostToDevice) == hipSuccess;
+}
+
+void free_all(gd_ctx* ctx) {
+    for (void* p : ctx->allocations) (void)hipFree(p);
+    ctx->allocations.clear();
+    for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
+    ctx->events.clear();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gd_status_string(gd_status s) {
+    switch (s) {
+        case GD_OK: return "ok";
+        case GD_ERR_ARG: return "invalid argument";
+        case GD_ERR_LAYOUT: return "invalid tensor layout";
+        case GD_ERR_CAPACITY: return "output capacity below the number of kept entries";
+        case GD_ERR_ALIGN: return "buffer not 16-byte aligned";
+        case GD_ERR_OOM: return "device allocation failed";
+        case GD_ERR_HIP: return "HIP runtime or launch failure";
+    }
+    return "unknown status";
+}
+
+uint64_t gd_keep_count(uint64_t n, double drop_ratio) {
+    if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return 0;
+    return n * keep_ppm_of(drop_ratio) / 1000000ull;
+}
+
+uint64_t gd_keep_total(const gd_ctx* ctx, double drop_ratio, gd_threshold mode) {
+    if (!ctx) return 0;
+    if (mode == GD_GLOBAL) return gd_keep_count(ctx->N, drop_ratio);
+    uint64_t k = 0;
+    for (uint32_t t = 0; t < ctx->T; ++t) k += gd_keep_count(ctx->offsets[t + 1] - ctx->offsets[t], drop_ratio);
+    return k;
+}
+
+gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
+    if (!out) return GD_ERR_ARG;
+    *out = nullptr;
+    if (!off || T == 0) return GD_ERR_ARG;
+    if (off[0] != 0) return GD_ERR_LAYOUT;
+    for (uint32_t t = 0; t < T; ++t)
+        if (off[t + 1] < off[t]) return GD_ERR_LAYOUT;
+    const uint64_t N = off[T];
+    if (N >= 0xFFFFFFFFull) return GD_ERR_LAYOUT;
+
+    gd_ctx* ctx = new (std::nothrow) gd_ctx();
+    if (!ctx) return GD_ERR_OOM;
+    if (hipGetDevice(&ctx->device) != hipSuccess) {
+        delete ctx;
+        return GD_ERR_HIP;
+    }
+    ctx->T = T;
+    ctx->N = N;
+    ctx->offsets.assign(off, off + T + 1);
+
+    // Chunk length: about 8192 chunks (one wave each) for large gradients,
+    // between 4096 and 16384 elements, a multiple of 1024.
+    uint64_t cl = (N + 8191) / 8192;
+    cl = (cl + 1023) / 1024 * 1024;
+    cl = std::min<uint64_t>(std::max<uint64_t>(cl, 4096), 16384);
+    ctx->chunk_len = (uint32_t)cl;
+    ctx->group_chunks = (uint32_t)std::min<uint64_t>(64, std::max<uint64_t>(1, 65536 / cl));
+
+    std::vector<uint32_t> cs, clen, ct, g0, gt, tg0(T + 1), toff(T + 1);
+    for (uint32_t t = 0; t < T; ++t) {
+        toff[t] = (uint32_t)off[t];
+        tg0[t] = (uint32_t)g0.size();
+        const uint64_t n = off[t + 1] - off[t];
+        const uint32_t first_chunk = (uint32_t)cs.size();
+        for (uint64_t j = 0; j < n; j += cl) {
+            cs.push_back((uint32_t)(off[t] + j));
+            clen.push_back((uint32_t)std::min<uint64_t>(cl, n - j));
+            ct.push_back(t);
+        }
+        const uint32_t nch = (uint32_t)cs.size() - first_chunk;
+        for (uint32_t c = 0; c < nch; c += ctx->group_chunks) {
+            g0.push_back(first_chunk + c);
+            gt.push_back(t);
+        }
+    }
+    toff[T] = (uint32_t)N;
+    tg0[T] = (uint32_t)g0.size();
+    g0.push_back((uint32_t)cs.size());
+    ctx->num_chunks = (uint32_t)cs.size();
+    ctx->num_groups = (uint32_t)gt.size();
+
+    std::vector<uint32_t> sk_t(T + 1), sk_g(2), goff = {0u, (uint32_t)N};
+    uint32_t acc = 0;
+    for (uint32_t t = 0; t < T; ++t) {
+        sk_t[t] = acc;
+        acc += sample_keys_for(off[t], off[t + 1]);
+    }
+    sk_t[T] = acc;
+    ctx->skeys_tensor = acc;
+    sk_g[0] = 0;
+    sk_g[1] = ctx->skeys_global = sample_keys_for(0, N);
+
+    const uint32_t S_max = T;
+    bool ok = dev_upload(ctx, &ctx->tab.chunk_start, cs) && dev_upload(ctx, &ctx->tab.chunk_len, clen) &&
+              dev_upload(ctx, &ctx->tab.chunk_tensor, ct) && dev_upload(ctx, &ctx->tab.group_chunk0, g0) &&
+              dev_upload(ctx, &ctx->tab.group_tensor, gt) && dev_upload(ctx, &ctx->tab.tensor_group0, tg0) &&
+              dev_upload(ctx, &ctx->tab.tensor_off, toff) && dev_upload(ctx, &ctx->tab.global_off, goff) &&
+              dev_upload(ctx, &ctx->tab.skey_base_tensor, sk_t) && dev_upload(ctx, &ctx->tab.skey_base_global, sk_g);
+    ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.cnt_lo, ctx->num_chunks) &&
+         dev_alloc(ctx, &ctx->scr.cnt_hi, ctx->num_chunks) && dev_alloc(ctx, &ctx->scr.grp_gt, ctx->num_groups) &&
+         dev_alloc(ctx, &ctx->scr.grp_eq, ctx->num_groups) && dev_alloc(ctx, &ctx->scr.grp_q, 4 * (size_t)ctx->num_groups) &&
+         dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) && dev_alloc(ctx, &ctx->scr.seg, S_max) &&
+         dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
+         dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&
+         dev_alloc(ctx, &ctx->scr.seg_done, S_max) && dev_alloc(ctx, &ctx->scr.qbase, T + 1);
+    if (!ok) {
+        free_all(ctx);
+        delete ctx;
+        return GD_ERR_OOM;
+    }
+    if (hipMemset(ctx->scr.seg_done, 0, S_max * sizeof(uint32_t)) != hipSuccess ||
+        hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+        free_all(ctx);
+        delete ctx;
+        return GD_ERR_HIP;
+    }
+    *out = ctx;
+    return GD_OK;
+}
+
+void gd_destroy(gd_ctx* ctx) {
+    if (!ctx) return;
+    DeviceGuard guard(ctx->device);
+    free_all(ctx);
+    delete ctx;
+}
+
+gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* residual, double drop_ratio,
+                      gd_threshold mode, gd_quant quant, const gd_sparse* out, void* stream) {
+    if (!ctx || !grad || !residual || !out) return GD_ERR_ARG;
+    if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
+    if (quant != GD_QUANT_NONE && quant != GD_QUANT_SIGN_MEAN) return GD_ERR_ARG;
+    if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
+    if (!out->idx || !out->val || !out->tensor_counts) return GD_ERR_ARG;
+    if (quant == GD_QUANT_SIGN_MEAN && (!out->sign_bits || !out->means)) return GD_ERR_ARG;
+    if (!aligned16(grad) || !aligned16(residual) || (base && !aligned16(base))) return GD_ERR_ALIGN;
+    const uint64_t k_total = gd_keep_total(ctx, drop_ratio, mode);
+    if (out->capacity < k_total) return GD_ERR_CAPACITY;
+
+    DeviceGuard guard(ctx->device);
+    if (!guard.ok) return GD_ERR_HIP;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool per = mode == GD_PER_TENSOR;
+    const uint32_t ppm = (uint32_t)keep_ppm_of(drop_ratio);
+    const uint32_t S = per ? ctx->T : 1u;
+    const uint32_t* seg_off = per ? ctx->tab.tensor_off : ctx->tab.global_off;
+
+    gd::SampleArgs sa{};
+    sa.grad = grad;
+    sa.base = base;
+    sa.res = residual;
+    sa.seg_off = seg_off;
+    sa.skey_base = per ? ctx->tab.skey_base_tensor : ctx->tab.skey_base_global;
+    sa.S = S;
+    sa.T = ctx->T;
+    sa.keep_ppm = ppm;
+    sa.debug_bracket = ctx->debug_bracket;
+    sa.skeys = ctx->scr.skeys;
+    sa.seg_done = ctx->scr.seg_done;
+    sa.seg = ctx->scr.seg;
+    sa.hist = ctx->scr.hist;
+    sa.out_base = ctx->scr.out_base;
+    sa.tensor_counts = out->tensor_counts;
+    if (gd::launch_sample(sa, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
+
+    gd::DenseArgs da{};
+    da.grad = grad;
+    da.base = base;
+    da.res = residual;
+    da.chunk_start = ctx->tab.chunk_start;
+    da.chunk_len = ctx->tab.chunk_len;
+    da.chunk_tensor = ctx->tab.chunk_tensor;
+    da.num_chunks = ctx->num_chunks;
+    da.per_tensor = per;
+    da.seg = ctx->scr.seg;
+    da.hist = ctx->scr.hist;
+    da.slots = ctx->scr.slots;
+    da.cnt_lo = ctx->scr.cnt_lo;
+    da.cnt_hi = ctx->scr.cnt_hi;
+    const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_chunks > 0;
+    if (timed && hipEventRecord(ctx->events[ctx->events_used], st) != hipSuccess) return GD_ERR_HIP;
+    if (gd::launch_dense(da, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
+    if (timed) {
+        if (hipEventRecord(ctx->events[ctx->events_used + 1], st) != hipSuccess) return GD_ERR_HIP;
+        ctx->events_used += 2;
+    }
+    if (ctx->num_chunks > 0) ++ctx->dense_launches;
+
+    gd::CandArgs ca{};
+    ca.res = residual;
+    ca.chunk_start = ctx->tab.chunk_start;
+    ca.chunk_len = ctx->tab.chunk_len;
+    ca.chunk_tensor = ctx->tab.chunk_tensor;
+    ca.group_chunk0 = ctx->tab.group_chunk0;
+    ca.group_tensor = ctx->tab.group_tensor;
+    ca.tensor_group0 = ctx->tab.tensor_group0;
+    ca.seg_off = seg_off;
+    ca.num_chunks = ctx->num_chunks;
+    ca.num_groups = ctx->num_groups;
+    ca.per_tensor = per;
+    ca.keep_ppm = ppm;
+    ca.seg = ctx->scr.seg;
+    ca.hist = ctx->scr.hist;
+    ca.slots = ctx->scr.slots;
+    ca.cnt_lo = ctx->scr.cnt_lo;
+    ca.grp_gt = ctx->scr.grp_gt;
+    ca.grp_eq = ctx->scr.grp_eq;
+    ca.grp_q = ctx->scr.grp_q;
+    ca.out_base = ctx->scr.out_base;
+    gd::EmitArgs ea{};
+    ea.idx = out->idx;
+    ea.val = out->val;
+    ea.tensor_counts = out->tensor_counts;
+    ea.capacity = out->capacity;
+    const bool q = quant == GD_QUANT_SIGN_MEAN;
+    if (gd::launch_candidates(ca, ea, q, st) != hipSuccess) return GD_ERR_HIP;
+
+    if (q) {
+        gd::QuantArgs qa{};
+        qa.res = residual;
+        qa.idx = out->idx;
+        qa.val = out->val;
+        qa.sign_bits = out->sign_bits;
+        qa.means = out->means;
+        qa.tensor_counts = out->tensor_counts;
+        qa.tensor_group0 = ctx->tab.tensor_group0;
+        qa.grp_q = ctx->scr.grp_q;
+        qa.qbase = ctx->scr.qbase;
+        qa.T = ctx->T;
+        qa.N = (uint32_t)ctx->N;
+        qa.k_total = k_total;
+        if (gd::launch_quant(qa, st) != hipSuccess) return GD_ERR_HIP;
+    }
+    return GD_OK;
+}
+
+gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const uint32_t* const* idx,
+                          const float* const* val, const uint64_t* nnz, float lr, void* stream) {
+    if (num_pushes > gd::kMaxPushes) return GD_ERR_ARG;
+    if (n >= 0xFFFFFFFFull) return GD_ERR_ARG;
+    if (num_pushes == 0 || n == 0) return GD_OK;
+    if (!params || !idx || !val || !nnz) return GD_ERR_ARG;
+    gd::ApplyArgs a{};
+    a.p = params;
+    a.n = (uint32_t)n;
+    a.C = num_pushes;
+    a.lr = lr;
+    uint32_t max_nnz = 0;
+    for (uint32_t c = 0; c < num_pushes; ++c) {
+        if (nnz[c] >= 0xFFFFFFFFull) return GD_ERR_ARG;
+        if (nnz[c] && (!idx[c] || !val[c])) return GD_ERR_ARG;
+        a.idx[c] = idx[c];
+        a.val[c] = val[c];
+        a.nnz[c] = (uint32_t)nnz[c];
+        max_nnz = std::max(max_nnz, a.nnz[c]);
+    }
+    if (gd::launch_apply(a, max_nnz, static_cast<hipStream_t>(stream)) != hipSuccess) return GD_ERR_HIP;
+    return GD_OK;
+}
+
+gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode) {
+    if (!ctx || mode < 0 || mode > 3) return GD_ERR_ARG;
+    ctx->debug_bracket = (uint32_t)mode;
+    return GD_OK;
+}
+
+gd_status gd_profile_enable(gd_ctx* ctx, int enable) {
+    if (!ctx) return GD_ERR_ARG;
+    DeviceGuard guard(ctx->device);
+    if (enable && ctx->events.empty()) {
+        ctx->events.resize(2 * 4096);
+        for (auto& e : ctx->events)
+            if (hipEventCreate(&e) != hipSuccess) return GD_ERR_HIP;
+    }
+    ctx->profile = enable != 0;
+    ctx->events_used = 0;
+    ctx->dense_launches = 0;
+    return GD_OK;
+}
+
+gd_status gd_profile_read(gd_ctx* ctx, double* dense_ms, uint64_t* dense_launches) {
+    if (!ctx || !dense_ms || !dense_launches) return GD_ERR_ARG;
+    DeviceGuard guard(ctx->device);
+    double total = 0.0;
+    for (size_t i = 0; i + 1 < ctx->events_used; i += 2) {
+        if (hipEventSynchronize(ctx->events[i + 1]) != hipSuccess) return GD_ERR_HIP;
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, ctx->events[i], ctx->events[i + 1]) != hipSuccess) return GD_ERR_HIP;
+        total += ms;
+    }
+    *dense_ms = total;
+    *dense_launches = ctx->events_used / 2;
+    ctx->events_used = 0;
+    ctx->dense_launches = 0;
+    return GD_OK;
+}
+
+}  // extern "C"

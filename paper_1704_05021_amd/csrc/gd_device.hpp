@@ -1,0 +1,153 @@
+// Device-side building blocks shared by the gradient-dropping kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gd {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / kWave;
+
+// Sort key of a value: its IEEE bit pattern with the sign cleared.  Unsigned
+// order of keys is the order of |x| (with -0 == +0, Inf above every finite
+// value and NaN above Inf).  Every key is below 2^31.
+constexpr uint32_t kNoKey = 0xFFFFFFFFu;  // above every key: "nothing qualifies"
+
+// The 31 key bits are resolved in three radix digits, most significant first.
+constexpr int kD0Shift = 21, kNB0 = 1024;  // key bits 30..21
+constexpr int kD1Shift = 10, kNB1 = 2048;  // key bits 20..10
+constexpr int kNB2 = 1024;                 // key bits  9..0
+
+// Histogram words per threshold segment: digit 0 (dense pass), digit 0
+// (fallback pass), digit 1, digit 2.
+constexpr int kHistH0 = 0, kHistH0Fb = kNB0, kHistH1 = 2 * kNB0, kHistH2 = 2 * kNB0 + kNB1;
+constexpr int kHistWords = 2 * kNB0 + kNB1 + kNB2;
+
+// Sampling: units of 16 consecutive elements (one 64-byte line per array),
+// at most kMaxUnits units per segment.
+constexpr int kUnit = 16;
+constexpr int kMaxUnits = 2048;
+constexpr int kSampleThreads = 1024;
+
+// Per threshold segment state, written by one kernel and read by later ones.
+struct SegState {
+    uint32_t lo;    // candidates: key >= lo
+    uint32_t hi;    // the dense pass wrote residual = +0 where key >= hi
+    uint32_t clo;   // number of candidates (key >= lo)
+    uint32_t chi;   // number of entries with key >= hi
+    uint32_t d0;    // digit 0 of the threshold key
+    uint32_t r1;    // rank of the threshold among candidates with that digit 0
+    uint32_t p21;   // digits 0 and 1 of the threshold key
+    uint32_t r2;    // rank among candidates with that 21-bit prefix
+    uint32_t thr;   // the threshold key T (kNoKey when nothing is kept)
+    uint32_t need;  // entries with key == T to keep, lowest index first
+    uint32_t pad[6];
+};
+
+__device__ __forceinline__ uint32_t key_of(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// Number of set bits of m in lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+
+__device__ __forceinline__ uint32_t popc64(uint64_t m) { return (uint32_t)__popcll(m); }
+
+// Orders this wave's LDS accesses around the call (a wave runs its LDS
+// operations in order; this stops the compiler moving them across).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        uint32_t t = __shfl_up(v, d, kWave);
+        if (lane >= d) v += t;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, kWave);
+    return v;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, kWave);
+    return v;
+}
+
+// Rank query on a histogram of NB bins (bin = digit value): find the digit
+// holding the r-th largest element (r >= 1) and the number of elements in
+// higher digits.  Returns false when the histogram holds fewer than r
+// elements.  Called by a whole wave; hist may be global or LDS memory.
+template <int NB>
+__device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uint32_t& above) {
+    constexpr int B = NB / kWave;
+    const int lane = lane_id();
+    const int top = NB - lane * B;  // this lane owns bins [top - B, top), high to low
+    uint32_t c[B];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+        c[i] = hist[top - 1 - i];
+        sum += c[i];
+    }
+    const uint32_t incl = wave_incl_scan(sum);
+    const uint32_t excl = incl - sum;
+    const bool mine = excl < r && r <= incl;
+    const uint64_t m = ballot(mine);
+    if (m == 0) {
+        digit = 0;
+        above = __shfl(incl, kWave - 1, kWave);
+        return false;
+    }
+    const int src = __ffsll((unsigned long long)m) - 1;
+    uint32_t d = 0, ab = 0;
+    if (mine) {
+        bool found = false;
+        uint32_t acc = excl;
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+            if (!found && acc + c[i] >= r) {
+                d = (uint32_t)(top - 1 - i);
+                ab = acc;
+                found = true;
+            }
+            acc += c[i];
+        }
+    }
+    digit = __shfl(d, src, kWave);
+    above = __shfl(ab, src, kWave);
+    return true;
+}
+
+// Stateless 32-bit mixer (a fixed integer hash) for sample positions.
+__device__ __forceinline__ uint32_t mix32(uint32_t x) {
+    x ^= x >> 16;
+    x *= 0x7feb352dU;
+    x ^= x >> 15;
+    x *= 0x846ca68bU;
+    x ^= x >> 16;
+    return x;
+}
+
+__device__ __forceinline__ uint32_t keep_of(uint32_t n, uint32_t keep_ppm) {
+    return (uint32_t)(((uint64_t)n * keep_ppm) / 1000000ull);
+}
+
+}  // namespace gd

@@ -1,0 +1,246 @@
+"""Python binding of the HIP gradient-dropping library (``libgd.so``).
+
+Argument marshalling only: torch supplies device memory and the current HIP
+stream; every step of the compressor runs in the library's kernels.  There is
+no CPU fallback: if ``libgd.so`` has not been built, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgd.so")
+
+GD_GLOBAL, GD_PER_TENSOR = 0, 1
+GD_QUANT_NONE, GD_QUANT_SIGN_MEAN = 0, 1
+
+STATUS = {
+    0: "GD_OK",
+    1: "GD_ERR_ARG",
+    2: "GD_ERR_LAYOUT",
+    3: "GD_ERR_CAPACITY",
+    4: "GD_ERR_ALIGN",
+    5: "GD_ERR_OOM",
+    6: "GD_ERR_HIP",
+}
+
+EXPORTS = [
+    "gd_create",
+    "gd_destroy",
+    "gd_keep_count",
+    "gd_keep_total",
+    "gd_compress",
+    "gd_apply_sparse",
+    "gd_status_string",
+    "gd_profile_enable",
+    "gd_profile_read",
+    "gd_debug_force_bracket",
+]
+
+
+class GDError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {STATUS.get(status, status)} ({_lib().gd_status_string(status).decode()})")
+
+
+class _Sparse(ctypes.Structure):
+    _fields_ = [
+        ("idx", ctypes.c_void_p),
+        ("val", ctypes.c_void_p),
+        ("sign_bits", ctypes.c_void_p),
+        ("means", ctypes.c_void_p),
+        ("tensor_counts", ctypes.c_void_p),
+        ("capacity", ctypes.c_uint64),
+    ]
+
+
+_LIB = None
+
+
+def _lib() -> ctypes.CDLL:
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build the HIP library first (python -c "
+                          "'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, u64, u32, dbl, i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_double, ctypes.c_int
+    lib.gd_create.argtypes = [ctypes.POINTER(vp), vp, u32]
+    lib.gd_create.restype = i32
+    lib.gd_destroy.argtypes = [vp]
+    lib.gd_destroy.restype = None
+    lib.gd_keep_count.argtypes = [u64, dbl]
+    lib.gd_keep_count.restype = u64
+    lib.gd_keep_total.argtypes = [vp, dbl, i32]
+    lib.gd_keep_total.restype = u64
+    lib.gd_compress.argtypes = [vp, vp, vp, vp, dbl, i32, i32, ctypes.POINTER(_Sparse), vp]
+    lib.gd_compress.restype = i32
+    lib.gd_apply_sparse.argtypes = [vp, u64, u32, vp, vp, vp, ctypes.c_float, vp]
+    lib.gd_apply_sparse.restype = i32
+    lib.gd_status_string.argtypes = [i32]
+    lib.gd_status_string.restype = ctypes.c_char_p
+    lib.gd_profile_enable.argtypes = [vp, i32]
+    lib.gd_profile_enable.restype = i32
+    lib.gd_profile_read.argtypes = [vp, ctypes.POINTER(dbl), ctypes.POINTER(u64)]
+    lib.gd_profile_read.restype = i32
+    lib.gd_debug_force_bracket.argtypes = [vp, i32]
+    lib.gd_debug_force_bracket.restype = i32
+    _LIB = lib
+    return lib
+
+
+def load() -> ctypes.CDLL:
+    """Load ``libgd.so`` (raises ImportError when it has not been built)."""
+    return _lib()
+
+
+def keep_count(n: int, drop_ratio: float) -> int:
+    return int(_lib().gd_keep_count(n, float(drop_ratio)))
+
+
+def _stream_handle(stream: Optional[torch.cuda.Stream]) -> Optional[int]:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream or None
+
+
+def _check_f32(t: torch.Tensor, name: str, n: int) -> None:
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous float32 tensor on the GPU")
+    if t.numel() != n:
+        raise ValueError(f"{name} has {t.numel()} elements, the layout has {n}")
+
+
+@dataclass
+class SparseOut:
+    """Device buffers of one compressed gradient (views of length k)."""
+
+    idx: torch.Tensor  # int32 storage holding uint32 indices
+    val: torch.Tensor  # float32
+    tensor_counts: torch.Tensor  # int32 storage holding uint32 counts
+    sign_bits: Optional[torch.Tensor] = None  # int32 storage holding uint32 words
+    means: Optional[torch.Tensor] = None  # float32 [2T]
+    k: int = 0
+
+
+class Compressor:
+    """A gradient layout (tensor offsets) bound to the device scratch of ``gd_create``."""
+
+    def __init__(self, offsets: Sequence[int], device: Optional[torch.device] = None):
+        lib = _lib()
+        off = (ctypes.c_uint64 * len(offsets))(*[int(o) for o in offsets])
+        self.offsets = [int(o) for o in offsets]
+        self.T = len(offsets) - 1
+        self.N = self.offsets[-1]
+        self.device = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        h = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            st = lib.gd_create(ctypes.byref(h), off, self.T)
+        if st != 0:
+            raise GDError(st, "gd_create")
+        self._h = h
+
+    def close(self) -> None:
+        if getattr(self, "_h", None):
+            _lib().gd_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def keep_total(self, drop_ratio: float, per_tensor: bool = False) -> int:
+        return int(_lib().gd_keep_total(self._h, float(drop_ratio), GD_PER_TENSOR if per_tensor else GD_GLOBAL))
+
+    def alloc_out(self, drop_ratio: float, per_tensor: bool = False, quant: bool = False,
+                  capacity: Optional[int] = None) -> SparseOut:
+        k = self.keep_total(drop_ratio, per_tensor)
+        cap = max(k if capacity is None else capacity, 1)
+        dev = self.device
+        out = SparseOut(
+            idx=torch.empty(cap, dtype=torch.int32, device=dev),
+            val=torch.empty(cap, dtype=torch.float32, device=dev),
+            tensor_counts=torch.empty(max(self.T, 1), dtype=torch.int32, device=dev),
+            k=k,
+        )
+        if quant:
+            out.sign_bits = torch.empty(max((cap + 31) // 32, 1), dtype=torch.int32, device=dev)
+            out.means = torch.empty(max(2 * self.T, 1), dtype=torch.float32, device=dev)
+        return out
+
+    def compress(self, grad: torch.Tensor, residual: torch.Tensor, drop_ratio: float = 0.99,
+                 per_tensor: bool = False, quant: bool = False, base: Optional[torch.Tensor] = None,
+                 out: Optional[SparseOut] = None, stream: Optional[torch.cuda.Stream] = None) -> SparseOut:
+        """One gd_compress call; ``residual`` is updated in place."""
+        _check_f32(grad, "grad", self.N)
+        _check_f32(residual, "residual", self.N)
+        if base is not None:
+            _check_f32(base, "base", self.N)
+        if out is None:
+            out = self.alloc_out(drop_ratio, per_tensor, quant)
+        sp = _Sparse(
+            out.idx.data_ptr(),
+            out.val.data_ptr(),
+            out.sign_bits.data_ptr() if (quant and out.sign_bits is not None) else None,
+            out.means.data_ptr() if (quant and out.means is not None) else None,
+            out.tensor_counts.data_ptr(),
+            out.idx.numel(),
+        )
+        st = _lib().gd_compress(
+            self._h, grad.data_ptr(), None if base is None else base.data_ptr(), residual.data_ptr(),
+            float(drop_ratio), GD_PER_TENSOR if per_tensor else GD_GLOBAL,
+            GD_QUANT_SIGN_MEAN if quant else GD_QUANT_NONE, ctypes.byref(sp), _stream_handle(stream))
+        if st != 0:
+            raise GDError(st, "gd_compress")
+        out.k = self.keep_total(drop_ratio, per_tensor)
+        return out
+
+    def debug_force_bracket(self, mode: int) -> None:
+        st = _lib().gd_debug_force_bracket(self._h, int(mode))
+        if st != 0:
+            raise GDError(st, "gd_debug_force_bracket")
+
+    def profile_enable(self, on: bool = True) -> None:
+        st = _lib().gd_profile_enable(self._h, int(on))
+        if st != 0:
+            raise GDError(st, "gd_profile_enable")
+
+    def profile_read(self):
+        """(summed milliseconds of the dense pass, number of timed launches)."""
+        ms = ctypes.c_double(0.0)
+        n = ctypes.c_uint64(0)
+        st = _lib().gd_profile_read(self._h, ctypes.byref(ms), ctypes.byref(n))
+        if st != 0:
+            raise GDError(st, "gd_profile_read")
+        return ms.value, n.value
+
+
+def apply_sparse(params: torch.Tensor, idx: List[torch.Tensor], val: List[torch.Tensor], lr: float = 1.0,
+                 stream: Optional[torch.cuda.Stream] = None) -> None:
+    """gd_apply_sparse: params[i] -= lr * (sum of pushed values at i, in push order)."""
+    if params.dtype != torch.float32 or not params.is_cuda or not params.is_contiguous():
+        raise TypeError("params must be a contiguous float32 tensor on the GPU")
+    C = len(idx)
+    if len(val) != C:
+        raise ValueError("idx and val must have the same number of pushes")
+    for a, b in zip(idx, val):
+        if a.dtype != torch.int32 or b.dtype != torch.float32 or a.numel() != b.numel():
+            raise TypeError("each push is an int32 (uint32 bits) index tensor and a float32 value tensor")
+        if not (a.is_cuda and b.is_cuda and a.is_contiguous() and b.is_contiguous()):
+            raise TypeError("push tensors must be contiguous GPU tensors")
+    ip = (ctypes.c_void_p * max(C, 1))(*[a.data_ptr() for a in idx])
+    vp = (ctypes.c_void_p * max(C, 1))(*[b.data_ptr() for b in val])
+    nz = (ctypes.c_uint64 * max(C, 1))(*[a.numel() for a in idx])
+    st = _lib().gd_apply_sparse(params.data_ptr(), params.numel(), C, ctypes.cast(ip, ctypes.c_void_p),
+                                ctypes.cast(vp, ctypes.c_void_p), ctypes.cast(nz, ctypes.c_void_p), float(lr),
+                                _stream_handle(stream))
+    if st != 0:
+        raise GDError(st, "gd_apply_sparse")

@@ -1,0 +1,101 @@
+"""Helpers for GPU-vs-oracle parity tests (imported by the ``-m gpu`` tests).
+
+The GPU side always goes through the C ABI (``paper_1704_05021_amd.gd``); the
+reference side is the CPU oracle.  Both receive the same bytes.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+import oracle
+from paper_1704_05021_amd import gd
+
+# Tolerance for results whose float reductions may be reordered on the GPU
+# (quantisation centres summed in fp64 in a different order).
+REL_TOL = 1e-6
+
+
+def bits(a: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+
+
+@dataclass
+class Result:
+    idx: np.ndarray
+    val: np.ndarray
+    residual: np.ndarray
+    tensor_counts: np.ndarray
+    sign_bits: Optional[np.ndarray] = None
+    means: Optional[np.ndarray] = None
+
+
+def gpu_compress(comp: gd.Compressor, grad: np.ndarray, residual: np.ndarray, drop: float, per_tensor: bool,
+                 quant: bool, base: Optional[np.ndarray] = None, out: Optional[gd.SparseOut] = None) -> Result:
+    dev = comp.device
+    g = torch.from_numpy(np.ascontiguousarray(grad, np.float32)).to(dev)
+    r = torch.from_numpy(np.ascontiguousarray(residual, np.float32)).to(dev)
+    b = None if base is None else torch.from_numpy(np.ascontiguousarray(base, np.float32)).to(dev)
+    o = comp.compress(g, r, drop, per_tensor=per_tensor, quant=quant, base=b, out=out)
+    torch.cuda.synchronize()
+    k = o.k
+    res = Result(
+        idx=o.idx[:k].cpu().numpy().view(np.uint32).copy(),
+        val=o.val[:k].cpu().numpy().copy(),
+        residual=r.cpu().numpy(),
+        tensor_counts=o.tensor_counts[:comp.T].cpu().numpy().view(np.uint32).copy(),
+    )
+    if quant:
+        res.sign_bits = o.sign_bits[:(k + 31) // 32].cpu().numpy().view(np.uint32).copy()
+        res.means = o.means[:2 * comp.T].cpu().numpy().copy()
+    return res
+
+
+def oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base=None) -> Result:
+    o = oracle.compress(grad, residual, offsets, drop, per_tensor=per_tensor, quant=quant, base=base)
+    return Result(o.idx, o.val, o.residual, o.tensor_counts, o.sign_bits, o.means)
+
+
+def assert_parity(g: Result, o: Result, quant: bool, what: str = "") -> None:
+    """Bit-exact on indices, values, counts, sign bits and unquantised residuals;
+    quantisation centres and the residuals built from them within REL_TOL."""
+    assert g.idx.shape == o.idx.shape, f"{what}: kept {g.idx.size} vs oracle {o.idx.size}"
+    if not np.array_equal(g.idx, o.idx):
+        bad = np.nonzero(g.idx != o.idx)[0]
+        raise AssertionError(f"{what}: {bad.size} index mismatches, first at {bad[0]}: gpu {g.idx[bad[0]]} "
+                             f"oracle {o.idx[bad[0]]}")
+    assert np.array_equal(bits(g.val), bits(o.val)), f"{what}: kept values differ"
+    assert np.array_equal(g.tensor_counts, o.tensor_counts), f"{what}: tensor counts {g.tensor_counts} vs {o.tensor_counts}"
+    if not quant:
+        if not np.array_equal(bits(g.residual), bits(o.residual)):
+            bad = np.nonzero(bits(g.residual) != bits(o.residual))[0]
+            raise AssertionError(f"{what}: {bad.size} residual mismatches, first at {bad[0]}: "
+                                 f"gpu {g.residual[bad[0]]!r} oracle {o.residual[bad[0]]!r}")
+        return
+    assert np.array_equal(g.sign_bits, o.sign_bits), f"{what}: sign bits differ"
+    m_g, m_o = g.means.astype(np.float64), o.means.astype(np.float64)
+    assert np.all(np.abs(m_g - m_o) <= REL_TOL * np.abs(m_o)), f"{what}: centres {m_g} vs {m_o}"
+    kept = np.zeros(o.residual.size, bool)
+    kept[o.idx] = True
+    assert np.array_equal(bits(g.residual[~kept]), bits(o.residual[~kept])), f"{what}: dropped residuals differ"
+    scale = np.max(np.abs(m_o)) if m_o.size else 0.0
+    diff = np.abs(g.residual[kept].astype(np.float64) - o.residual[kept].astype(np.float64))
+    assert np.all(diff <= REL_TOL * scale), f"{what}: quantised residuals differ by {diff.max()}"
+    if np.array_equal(bits(g.means), bits(o.means)):
+        assert np.array_equal(bits(g.residual), bits(o.residual)), f"{what}: equal centres but residuals differ"
+
+
+def check_case(grad, residual, offsets: Sequence[int], drop: float, per_tensor: bool, quant: bool,
+               base=None, comp: Optional[gd.Compressor] = None, debug_bracket: int = 0, what: str = "") -> Result:
+    comp = comp or gd.Compressor(offsets)
+    comp.debug_force_bracket(debug_bracket)
+    try:
+        g = gpu_compress(comp, grad, residual, drop, per_tensor, quant, base)
+    finally:
+        comp.debug_force_bracket(0)
+    o = oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base)
+    assert_parity(g, o, quant, what)
+    return o

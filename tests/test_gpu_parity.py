@@ -1,0 +1,259 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bar: bit-exact on kept indices, kept values, tensor counts, sign bits and
+unquantised residuals; quantisation centres (fp64 sums in another order)
+within 1e-6 relative, and the quantised residuals built from them within
+1e-6 of the largest centre.  Multi-step workloads are teacher-forced: every
+GPU step starts from the oracle's residual, so one step's tolerance cannot
+flip the next step's selection.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1704_05021_amd import gd, workloads as wl
+from parity import assert_parity, bits, check_case, gpu_compress, oracle_compress
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "hand_examples.json")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gd.load()
+    torch.cuda.set_device(0)
+
+
+def test_hand_examples():
+    gold = json.load(open(GOLDEN))
+    for case in gold["compress"]:
+        comp = gd.Compressor(case["offsets"])
+        res = None
+        for st in case["steps"]:
+            r_in = res if st["residual_in"] == "previous" else np.array(st["residual_in"], np.float32)
+            g = gpu_compress(comp, np.array(st["grad"], np.float32), r_in, case["drop"],
+                             case.get("per_tensor", False), case.get("quant", False))
+            assert g.idx.tolist() == st["idx"], case["name"]
+            assert np.array_equal(bits(g.val), bits(np.array(st["val"], np.float32))), case["name"]
+            assert np.array_equal(bits(g.residual), bits(np.array(st["residual_out"], np.float32))), case["name"]
+            assert g.tensor_counts.tolist() == st["tensor_counts"], case["name"]
+            if "sign_bits" in st:
+                assert g.sign_bits.tolist() == st["sign_bits"]
+                assert np.array_equal(bits(g.means), bits(np.array(st["means"], np.float32)))
+            res = g.residual
+
+
+def _tie_heavy(rng, n):
+    levels = np.array([0.0, 0.25, 0.5, 1.0, 1.5, 3.0, 1e-3, 2.0 ** -130], np.float32)
+    v = levels[rng.integers(0, levels.size, n)] * np.where(rng.random(n) < 0.5, -1, 1).astype(np.float32)
+    return v.astype(np.float32)
+
+
+@pytest.mark.parametrize("debug", [0, 1, 2, 3], ids=["sampled", "fallback", "zero_all_cands", "all_cands"])
+@pytest.mark.parametrize("seed", range(6))
+def test_random_layouts(seed, debug):
+    rng = np.random.default_rng(100 + seed)
+    T = int(rng.integers(1, 7))
+    sizes = rng.integers(0, 30000, size=T)
+    sizes[rng.integers(0, T)] = int(rng.choice([0, 1, 3, 17, 4095, 4096, 4097, 16385, 70001]))
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64).tolist()
+    N = offsets[-1]
+    if N == 0:
+        offsets[-1] = N = 5
+    for step, (drop, per, quant) in enumerate([(0.99, False, False), (0.99, True, False), (0.9, False, True),
+                                               (0.5, True, True), (0.999, True, False)]):
+        if seed % 2:
+            g = _tie_heavy(rng, N)
+            r = _tie_heavy(rng, N)
+        else:
+            g = (rng.standard_t(3, N) * 1e-3).astype(np.float32)
+            r = (rng.normal(0, 1e-3, N) * (rng.random(N) < 0.7)).astype(np.float32)
+        comp = gd.Compressor(offsets)
+        check_case(g, r, offsets, drop, per, quant, comp=comp, debug_bracket=debug,
+                   what=f"seed={seed} debug={debug} step={step} N={N} T={T}")
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 63, 64, 65, 1023, 1024, 1025, 4095, 4096, 4097, 16383, 16384, 16385,
+                               65536, 65537, 300001])
+def test_edge_sizes(n):
+    rng = np.random.default_rng(n)
+    g = rng.normal(0, 1, n).astype(np.float32)
+    r = rng.normal(0, 1, n).astype(np.float32)
+    comp = gd.Compressor([0, n])
+    for drop in (0.0, 0.5, 0.99, 1.0):
+        for debug in (0, 1):
+            check_case(g, r, [0, n], drop, False, False, comp=comp, debug_bracket=debug, what=f"n={n} drop={drop}")
+
+
+def test_unaligned_tensor_offsets():
+    # tensors whose offsets are not multiples of 4: vectors straddle tensor boundaries
+    offsets = [0, 5, 6, 4103, 4103, 9001, 20003, 20010]
+    rng = np.random.default_rng(7)
+    N = offsets[-1]
+    g = (rng.standard_t(3, N) * 1e-2).astype(np.float32)
+    r = rng.normal(0, 1e-2, N).astype(np.float32)
+    comp = gd.Compressor(offsets)
+    for per in (False, True):
+        for quant in (False, True):
+            for debug in (0, 1, 2, 3):
+                check_case(g, r, offsets, 0.9, per, quant, comp=comp, debug_bracket=debug, what=f"per={per} q={quant}")
+
+
+def test_special_values():
+    v = np.array([1.0, np.inf, np.nan, -np.inf, 2.0, -0.0, 0.0, 2.0 ** -149, -(2.0 ** -148), 3.0], np.float32)
+    z = np.array([0.0, 0.0, 0.0, 0.0, 0.0, -0.0, -0.0, 2.0 ** -149, 0.0, -3.0], np.float32)
+    comp = gd.Compressor([0, v.size])
+    for drop in (0.0, 0.3, 0.5, 0.8, 0.9, 1.0):
+        for debug in (0, 1, 3):
+            check_case(v, z, [0, v.size], drop, False, False, comp=comp, debug_bracket=debug, what=f"drop={drop}")
+
+
+def test_all_zero_and_all_equal():
+    n = 50000
+    comp = gd.Compressor([0, 20000, n])
+    z = np.zeros(n, np.float32)
+    for per in (False, True):
+        check_case(z, z, [0, 20000, n], 0.99, per, False, comp=comp, what="zeros")
+        s = np.where(np.random.default_rng(1).random(n) < 0.5, -0.75, 0.75).astype(np.float32)
+        check_case(s, z, [0, 20000, n], 0.99, per, True, comp=comp, what="equal magnitudes")
+
+
+def _run_workload(name, steps=None, debug=0):
+    w = wl.workload(name)
+    off = w.layout.offsets.astype(np.int64).tolist()
+    comp = gd.Compressor(off)
+    comp.debug_force_bracket(debug)
+    residual = np.zeros(w.layout.numel, np.float32)
+    for step in range(steps or w.steps):
+        grad = w.grad(step)
+        g = gpu_compress(comp, grad, residual, w.drop, w.per_tensor, w.quant)
+        o = oracle_compress(grad, residual, off, w.drop, w.per_tensor, w.quant)
+        assert_parity(g, o, w.quant, f"{name} step {step}")
+        residual = o.residual  # teacher forcing
+    comp.close()
+
+
+def test_mnist_mlp_full():
+    _run_workload("mnist_mlp_784_512_512_10")
+
+
+@pytest.mark.parametrize("name", ["mlp_784_256_256_10_t3_small", "nmt_small_per_tensor", "nmt_small_global_signmean"])
+def test_small_workloads(name):
+    _run_workload(name)
+    _run_workload(name, steps=2, debug=1)
+
+
+@pytest.mark.parametrize("name,steps", [("mlp_784_4096_4096_10_t3", 3), ("nmt_85k_per_tensor", 2),
+                                        ("nmt_85k_global_signmean", 2)])
+def test_full_size_workloads(name, steps):
+    _run_workload(name, steps=steps)
+
+
+def test_determinism():
+    w = wl.workload("nmt_small_global_signmean")
+    off = w.layout.offsets.astype(np.int64).tolist()
+    comp = gd.Compressor(off)
+    grad = w.grad(0)
+    r0 = np.random.default_rng(3).normal(0, 1e-3, grad.size).astype(np.float32)
+    a = gpu_compress(comp, grad, r0, 0.99, False, True)
+    b = gpu_compress(comp, grad, r0, 0.99, False, True)
+    assert np.array_equal(a.idx, b.idx) and np.array_equal(bits(a.residual), bits(b.residual))
+    assert np.array_equal(bits(a.means), bits(b.means)) and np.array_equal(a.sign_bits, b.sign_bits)
+
+
+def test_pull_delta_base():
+    rng = np.random.default_rng(4)
+    n = 200003
+    p0 = rng.normal(0, 0.1, n).astype(np.float32)
+    p1 = p0.copy()
+    ix = rng.choice(n, 5000, replace=False)
+    p1[ix] -= rng.normal(0, 1e-2, 5000).astype(np.float32)
+    res = np.zeros(n, np.float32)
+    comp = gd.Compressor([0, n])
+    for debug in (0, 1):
+        check_case(p1, res, [0, n], 0.99, False, False, base=p0, comp=comp, debug_bracket=debug, what="pull")
+
+
+def _apply_case(n, C, nnz, dup, seed, lr=1.0):
+    s = wl.server_shard(n=n, clients=C, nnz=nnz, dup_frac=dup, seed=seed)
+    want = oracle.apply_sparse(s.params, s.idx, s.val, lr)
+    p = torch.from_numpy(s.params).cuda()
+    idx = [torch.from_numpy(a.view(np.int32)).cuda() for a in s.idx]
+    val = [torch.from_numpy(a).cuda() for a in s.val]
+    gd.apply_sparse(p, idx, val, lr)
+    torch.cuda.synchronize()
+    got = p.cpu().numpy()
+    assert np.array_equal(bits(got), bits(want)), f"apply n={n} C={C}: {np.sum(bits(got) != bits(want))} differ"
+    return s, got
+
+
+@pytest.mark.parametrize("C,dup,lr", [(1, 0.0, 1.0), (2, 0.05, 1.0), (4, 0.05, 1.0), (4, 0.5, 0.25), (7, 0.3, 1.0)])
+def test_apply_small(C, dup, lr):
+    _apply_case(60_000, C, 1500, dup, seed=C, lr=lr)
+
+
+def test_apply_and_pull_full_shard():
+    cfg = wl.SHARD_FULL
+    s, p1 = _apply_case(cfg["n"], cfg["clients"], cfg["nnz"], cfg["dup_frac"], cfg["seed"])
+    comp = gd.Compressor([0, cfg["n"]])
+    zeros = np.zeros(cfg["n"], np.float32)
+    check_case(p1, zeros, [0, cfg["n"]], 0.99, False, False, base=s.params, comp=comp, what="pull of full shard")
+
+
+def test_errors():
+    comp = gd.Compressor([0, 1000])
+    g = torch.zeros(1000, device="cuda")
+    r = torch.zeros(1000, device="cuda")
+    out = comp.alloc_out(0.99)
+    small = comp.alloc_out(0.99, capacity=5)
+    with pytest.raises(gd.GDError) as e:
+        comp.compress(g, r, 0.99, out=small)
+    assert e.value.status == 3
+    big = torch.zeros(1001, device="cuda")
+    with pytest.raises(gd.GDError) as e:
+        comp.compress(big[1:], r, 0.99, out=out)
+    assert e.value.status == 4
+    with pytest.raises(gd.GDError) as e:
+        comp.compress(g, r, 1.5, out=out)
+    assert e.value.status == 1
+    with pytest.raises(gd.GDError) as e:
+        gd.Compressor([0, 10, 5])
+    assert e.value.status == 2
+    with pytest.raises(gd.GDError) as e:
+        gd.Compressor([3, 10])
+    assert e.value.status == 2
+    p = torch.zeros(10, device="cuda")
+    ix = [torch.zeros(1, dtype=torch.int32, device="cuda")] * 65
+    vx = [torch.zeros(1, device="cuda")] * 65
+    with pytest.raises(gd.GDError) as e:
+        gd.apply_sparse(p, ix, vx)
+    assert e.value.status == 1
+    # failed calls leave buffers untouched
+    r.fill_(1.5)
+    with pytest.raises(gd.GDError):
+        comp.compress(g, r, 0.99, out=small)
+    torch.cuda.synchronize()
+    assert torch.all(r == 1.5)
+
+
+def test_non_default_stream():
+    w = wl.workload("nmt_small_per_tensor")
+    off = w.layout.offsets.astype(np.int64).tolist()
+    comp = gd.Compressor(off)
+    grad = w.grad(0)
+    o = oracle_compress(grad, np.zeros_like(grad), off, 0.99, True, False)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        gt = torch.from_numpy(grad).cuda()
+        rt = torch.zeros_like(gt)
+        out = comp.compress(gt, rt, 0.99, per_tensor=True)
+    s.synchronize()
+    assert np.array_equal(out.idx[:out.k].cpu().numpy().view(np.uint32), o.idx)
+    assert np.array_equal(bits(rt.cpu().numpy()), bits(o.residual))
