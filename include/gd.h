@@ -157,6 +157,16 @@ gd_status gd_profile_read(gd_ctx* ctx, double* dense_ms, uint64_t* dense_launche
  */
 gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode);
 
+/*
+ * Test hook: waits for the device, then copies the per-segment state of the
+ * last gd_compress call (16 uint32 words per threshold segment: candidate
+ * bracket lo and hi, candidate count, bracket-miss flag, radix digits and
+ * ranks, threshold key, ties kept) for up to max_segments segments into
+ * seg_words (host), and the decomposition into info (host, 4 entries:
+ * chunk length, chunks, chunks per group, groups).  Synchronises the host.
+ */
+gd_status gd_debug_state(gd_ctx* ctx, uint32_t* seg_words, uint32_t max_segments, uint64_t* info);
+
 #ifdef __cplusplus
 }
 #endif

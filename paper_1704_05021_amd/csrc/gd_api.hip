@@ -115,36 +115,27 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
     ctx->N = N;
     ctx->offsets.assign(off, off + T + 1);
 
-    // Chunk length: about 8192 chunks (one wave each) for large gradients,
-    // between 4096 and 16384 elements, a multiple of 1024.
-    uint64_t cl = (N + 8191) / 8192;
-    cl = (cl + 1023) / 1024 * 1024;
-    cl = std::min<uint64_t>(std::max<uint64_t>(cl, 4096), 16384);
+    // Units of the dense pass: up to 1024 consecutive elements of one tensor.
+    const uint64_t cl = gd::kUnitLen;
     ctx->chunk_len = (uint32_t)cl;
-    ctx->group_chunks = (uint32_t)std::min<uint64_t>(64, std::max<uint64_t>(1, 65536 / cl));
 
-    std::vector<uint32_t> cs, clen, ct, g0, gt, tg0(T + 1), toff(T + 1);
+    std::vector<uint32_t> cs, clen, ct, tc0(T + 1), toff(T + 1);
+    uint64_t max_tiles = 0;
     for (uint32_t t = 0; t < T; ++t) {
         toff[t] = (uint32_t)off[t];
-        tg0[t] = (uint32_t)g0.size();
+        tc0[t] = (uint32_t)cs.size();
         const uint64_t n = off[t + 1] - off[t];
-        const uint32_t first_chunk = (uint32_t)cs.size();
         for (uint64_t j = 0; j < n; j += cl) {
             cs.push_back((uint32_t)(off[t] + j));
             clen.push_back((uint32_t)std::min<uint64_t>(cl, n - j));
             ct.push_back(t);
         }
-        const uint32_t nch = (uint32_t)cs.size() - first_chunk;
-        for (uint32_t c = 0; c < nch; c += ctx->group_chunks) {
-            g0.push_back(first_chunk + c);
-            gt.push_back(t);
-        }
+        max_tiles += (n + gd::kTile - 1) / gd::kTile;
     }
     toff[T] = (uint32_t)N;
-    tg0[T] = (uint32_t)g0.size();
-    g0.push_back((uint32_t)cs.size());
+    tc0[T] = (uint32_t)cs.size();
     ctx->num_chunks = (uint32_t)cs.size();
-    ctx->num_groups = (uint32_t)gt.size();
+    ctx->max_tiles = (uint32_t)max_tiles;
 
     std::vector<uint32_t> sk_t(T + 1), sk_g(2), goff = {0u, (uint32_t)N};
     uint32_t acc = 0;
@@ -158,24 +149,29 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
     sk_g[1] = ctx->skeys_global = sample_keys_for(0, N);
 
     const uint32_t S_max = T;
+    const uint32_t scan_blocks = (ctx->num_chunks + gd::kScanUnits - 1) / gd::kScanUnits;
     bool ok = dev_upload(ctx, &ctx->tab.chunk_start, cs) && dev_upload(ctx, &ctx->tab.chunk_len, clen) &&
-              dev_upload(ctx, &ctx->tab.chunk_tensor, ct) && dev_upload(ctx, &ctx->tab.group_chunk0, g0) &&
-              dev_upload(ctx, &ctx->tab.group_tensor, gt) && dev_upload(ctx, &ctx->tab.tensor_group0, tg0) &&
+              dev_upload(ctx, &ctx->tab.chunk_tensor, ct) && dev_upload(ctx, &ctx->tab.tensor_chunk0, tc0) &&
               dev_upload(ctx, &ctx->tab.tensor_off, toff) && dev_upload(ctx, &ctx->tab.global_off, goff) &&
               dev_upload(ctx, &ctx->tab.skey_base_tensor, sk_t) && dev_upload(ctx, &ctx->tab.skey_base_global, sk_g);
     ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.cnt_lo, ctx->num_chunks) &&
-         dev_alloc(ctx, &ctx->scr.cnt_hi, ctx->num_chunks) && dev_alloc(ctx, &ctx->scr.grp_gt, ctx->num_groups) &&
-         dev_alloc(ctx, &ctx->scr.grp_eq, ctx->num_groups) && dev_alloc(ctx, &ctx->scr.grp_q, 4 * (size_t)ctx->num_groups) &&
+         dev_alloc(ctx, &ctx->scr.tile_unit0, ctx->max_tiles) && dev_alloc(ctx, &ctx->scr.flags, 4) &&
+         dev_alloc(ctx, &ctx->scr.cand, N) &&
+         dev_alloc(ctx, &ctx->scr.cand_off, ctx->num_chunks + 1) && dev_alloc(ctx, &ctx->scr.ten_cbase, T + 1) &&
+         dev_alloc(ctx, &ctx->scr.tile_base, T + 1) && dev_alloc(ctx, &ctx->scr.tile_gt, ctx->max_tiles) &&
+         dev_alloc(ctx, &ctx->scr.tile_eq, ctx->max_tiles) && dev_alloc(ctx, &ctx->scr.tile_q, 4 * (size_t)ctx->max_tiles) &&
          dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) && dev_alloc(ctx, &ctx->scr.seg, S_max) &&
          dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
          dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&
-         dev_alloc(ctx, &ctx->scr.seg_done, S_max) && dev_alloc(ctx, &ctx->scr.qbase, T + 1);
+         dev_alloc(ctx, &ctx->scr.loc, ctx->num_chunks) && dev_alloc(ctx, &ctx->scr.btot, scan_blocks) &&
+         dev_alloc(ctx, &ctx->scr.boff, scan_blocks) && dev_alloc(ctx, &ctx->scr.scan_done, 1) &&
+         dev_alloc(ctx, &ctx->scr.raw_tbase, T + 1) && dev_alloc(ctx, &ctx->scr.qbase, T + 1);
     if (!ok) {
         free_all(ctx);
         delete ctx;
         return GD_ERR_OOM;
     }
-    if (hipMemset(ctx->scr.seg_done, 0, S_max * sizeof(uint32_t)) != hipSuccess ||
+    if (hipMemset(ctx->scr.scan_done, 0, sizeof(uint32_t)) != hipSuccess ||
         hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
         free_all(ctx);
@@ -224,7 +220,6 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     sa.keep_ppm = ppm;
     sa.debug_bracket = ctx->debug_bracket;
     sa.skeys = ctx->scr.skeys;
-    sa.seg_done = ctx->scr.seg_done;
     sa.seg = ctx->scr.seg;
     sa.hist = ctx->scr.hist;
     sa.out_base = ctx->scr.out_base;
@@ -241,10 +236,8 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     da.num_chunks = ctx->num_chunks;
     da.per_tensor = per;
     da.seg = ctx->scr.seg;
-    da.hist = ctx->scr.hist;
     da.slots = ctx->scr.slots;
     da.cnt_lo = ctx->scr.cnt_lo;
-    da.cnt_hi = ctx->scr.cnt_hi;
     const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_chunks > 0;
     if (timed && hipEventRecord(ctx->events[ctx->events_used], st) != hipSuccess) return GD_ERR_HIP;
     if (gd::launch_dense(da, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
@@ -259,21 +252,31 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ca.chunk_start = ctx->tab.chunk_start;
     ca.chunk_len = ctx->tab.chunk_len;
     ca.chunk_tensor = ctx->tab.chunk_tensor;
-    ca.group_chunk0 = ctx->tab.group_chunk0;
-    ca.group_tensor = ctx->tab.group_tensor;
-    ca.tensor_group0 = ctx->tab.tensor_group0;
+    ca.tensor_chunk0 = ctx->tab.tensor_chunk0;
+    ca.tensor_off = ctx->tab.tensor_off;
     ca.seg_off = seg_off;
     ca.num_chunks = ctx->num_chunks;
-    ca.num_groups = ctx->num_groups;
+    ca.T = ctx->T;
     ca.per_tensor = per;
     ca.keep_ppm = ppm;
     ca.seg = ctx->scr.seg;
     ca.hist = ctx->scr.hist;
     ca.slots = ctx->scr.slots;
     ca.cnt_lo = ctx->scr.cnt_lo;
-    ca.grp_gt = ctx->scr.grp_gt;
-    ca.grp_eq = ctx->scr.grp_eq;
-    ca.grp_q = ctx->scr.grp_q;
+    ca.loc = ctx->scr.loc;
+    ca.btot = ctx->scr.btot;
+    ca.boff = ctx->scr.boff;
+    ca.scan_done = ctx->scr.scan_done;
+    ca.raw_tbase = ctx->scr.raw_tbase;
+    ca.cand = ctx->scr.cand;
+    ca.cand_off = ctx->scr.cand_off;
+    ca.ten_cbase = ctx->scr.ten_cbase;
+    ca.tile_base = ctx->scr.tile_base;
+    ca.tile_unit0 = ctx->scr.tile_unit0;
+    ca.flags = ctx->scr.flags;
+    ca.tile_gt = ctx->scr.tile_gt;
+    ca.tile_eq = ctx->scr.tile_eq;
+    ca.tile_q = ctx->scr.tile_q;
     ca.out_base = ctx->scr.out_base;
     gd::EmitArgs ea{};
     ea.idx = out->idx;
@@ -281,7 +284,8 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ea.tensor_counts = out->tensor_counts;
     ea.capacity = out->capacity;
     const bool q = quant == GD_QUANT_SIGN_MEAN;
-    if (gd::launch_candidates(ca, ea, q, st) != hipSuccess) return GD_ERR_HIP;
+    if (gd::launch_layout(ca, st) != hipSuccess) return GD_ERR_HIP;
+    if (gd::launch_candidates(ca, ea, q, ctx->max_tiles, st) != hipSuccess) return GD_ERR_HIP;
 
     if (q) {
         gd::QuantArgs qa{};
@@ -291,8 +295,8 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
         qa.sign_bits = out->sign_bits;
         qa.means = out->means;
         qa.tensor_counts = out->tensor_counts;
-        qa.tensor_group0 = ctx->tab.tensor_group0;
-        qa.grp_q = ctx->scr.grp_q;
+        qa.tile_base = ctx->scr.tile_base;
+        qa.tile_q = ctx->scr.tile_q;
         qa.qbase = ctx->scr.qbase;
         qa.T = ctx->T;
         qa.N = (uint32_t)ctx->N;
@@ -329,6 +333,21 @@ gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const 
 gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode) {
     if (!ctx || mode < 0 || mode > 3) return GD_ERR_ARG;
     ctx->debug_bracket = (uint32_t)mode;
+    return GD_OK;
+}
+
+gd_status gd_debug_state(gd_ctx* ctx, uint32_t* seg_words, uint32_t max_segments, uint64_t* info) {
+    if (!ctx || !info || (max_segments && !seg_words)) return GD_ERR_ARG;
+    DeviceGuard guard(ctx->device);
+    info[0] = ctx->chunk_len;
+    info[1] = ctx->num_chunks;
+    info[2] = gd::kTile;
+    info[3] = ctx->max_tiles;
+    const uint32_t n = std::min(max_segments, ctx->T);
+    if (n == 0) return GD_OK;
+    if (hipDeviceSynchronize() != hipSuccess) return GD_ERR_HIP;
+    if (hipMemcpy(seg_words, ctx->scr.seg, n * sizeof(gd::SegState), hipMemcpyDeviceToHost) != hipSuccess)
+        return GD_ERR_HIP;
     return GD_OK;
 }
 

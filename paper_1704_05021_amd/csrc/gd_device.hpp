@@ -28,17 +28,29 @@ constexpr int kHistH0 = 0, kHistH0Fb = kNB0, kHistH1 = 2 * kNB0, kHistH2 = 2 * k
 constexpr int kHistWords = 2 * kNB0 + kNB1 + kNB2;
 
 // Sampling: units of 16 consecutive elements (one 64-byte line per array),
-// at most kMaxUnits units per segment.
+// at most kMaxUnits units per segment.  A sample key is the top 16 bits of
+// the 31-bit key (relative resolution 2^-8), kNoKey16 marks a missing one.
 constexpr int kUnit = 16;
-constexpr int kMaxUnits = 2048;
-constexpr int kSampleThreads = 1024;
+constexpr int kMaxUnits = 1024;
+constexpr int kSampleThreads = 128;    // gather blocks: one unit per thread
+constexpr int kBracketThreads = 1024;  // one block per segment: one unit per thread
+constexpr int kSampleBlocks = kMaxUnits / kSampleThreads;
+constexpr uint32_t kNoKey16 = 0xFFFFu;
+constexpr int kK16Shift = 15;           // key16 = key >> 15
+constexpr int kS0Shift = 6, kSNB1 = 64;  // key16 digits: bits 15..6 (= key digit 0), bits 5..0
+
+// Elements per unit of the dense pass (one wave).
+constexpr uint32_t kUnitLen = 1024;
+// Units per block of the candidate-count scan.
+constexpr uint32_t kScanUnits = 1024;
+constexpr int kScanThreads = 256;
 
 // Per threshold segment state, written by one kernel and read by later ones.
 struct SegState {
     uint32_t lo;    // candidates: key >= lo
     uint32_t hi;    // the dense pass wrote residual = +0 where key >= hi
     uint32_t clo;   // number of candidates (key >= lo)
-    uint32_t chi;   // number of entries with key >= hi
+    uint32_t miss;  // 1 when fewer than k candidates: every element becomes one
     uint32_t d0;    // digit 0 of the threshold key
     uint32_t r1;    // rank of the threshold among candidates with that digit 0
     uint32_t p21;   // digits 0 and 1 of the threshold key
@@ -134,6 +146,46 @@ __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uin
     digit = __shfl(d, src, kWave);
     above = __shfl(ab, src, kWave);
     return true;
+}
+
+// Adds 1 to h[bin] for every active lane.  Up to three times, the lanes that
+// share the first remaining lane's bin are combined into one LDS atomic, so a
+// wave whose entries fall in a few bins (exact zeros, equal values, the
+// exponent bins of a Gaussian) does not serialise on them.  Must be called
+// by the whole wave.
+__device__ __forceinline__ void lds_hist_add(uint32_t* h, uint32_t bin, bool active) {
+    uint64_t act = ballot(active);
+#pragma unroll
+    for (int round = 0; round < 3; ++round) {
+        if (act == 0) return;
+        const int leader = __ffsll((unsigned long long)act) - 1;
+        const uint32_t lbin = __shfl(bin, leader, kWave);
+        const uint64_t ms = ballot(active && bin == lbin) & act;
+        if (lane_id() == leader) atomicAdd(&h[lbin], popc64(ms));
+        act &= ~ms;
+    }
+    if ((act >> lane_id()) & 1ull) atomicAdd(&h[bin], 1u);
+}
+
+// Exclusive prefix over a block of NT threads; *total receives the block sum.
+// lds must hold NT / 64 + 1 words.  Every thread of the block must call it.
+template <int NT>
+__device__ uint32_t block_excl_scan(uint32_t v, uint32_t* lds, uint32_t* total) {
+    constexpr int NW = NT / kWave;
+    const int w = threadIdx.x / kWave, lane = lane_id();
+    const uint32_t incl = wave_incl_scan(v);
+    if (lane == kWave - 1) lds[w] = incl;
+    __syncthreads();
+    uint32_t carry = 0, sum = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        const uint32_t x = lds[i];
+        carry += i < w ? x : 0u;
+        sum += x;
+    }
+    __syncthreads();
+    *total = sum;
+    return incl - v + carry;
 }
 
 // Stateless 32-bit mixer (a fixed integer hash) for sample positions.

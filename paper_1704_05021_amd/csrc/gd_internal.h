@@ -14,15 +14,13 @@ namespace gd {
 //  * chunk: up to `chunk_len` consecutive elements of one tensor, processed
 //    by one wave in the dense pass; candidates of chunk c are stored at
 //    slots[chunk_start[c] ...].
-//  * group: up to `group_chunks` consecutive chunks of one tensor, processed
-//    by one wave in the candidate passes.
+//  * tile: up to kTile consecutive candidates of one tensor, processed by one
+//    wave in the candidate passes (at most `max_tiles` of them).
 struct Tables {
     uint32_t* chunk_start = nullptr;   // [C]
     uint32_t* chunk_len = nullptr;     // [C]
     uint32_t* chunk_tensor = nullptr;  // [C]
-    uint32_t* group_chunk0 = nullptr;  // [NG + 1]
-    uint32_t* group_tensor = nullptr;  // [NG]
-    uint32_t* tensor_group0 = nullptr; // [T + 1]
+    uint32_t* tensor_chunk0 = nullptr; // [T + 1]
     uint32_t* tensor_off = nullptr;    // [T + 1] element offsets (u32)
     uint32_t* global_off = nullptr;    // [2] = {0, N}
     uint32_t* skey_base_tensor = nullptr;  // [T + 1] sample-key offsets per tensor segment
@@ -32,15 +30,24 @@ struct Tables {
 struct Scratch {
     uint2* slots = nullptr;         // [max(N,1)] candidate (index, value bits)
     uint32_t* cnt_lo = nullptr;     // [C] candidates per chunk
-    uint32_t* cnt_hi = nullptr;     // [C] entries with key >= hi per chunk
-    uint32_t* grp_gt = nullptr;     // [NG] candidates above the threshold per group
-    uint32_t* grp_eq = nullptr;     // [NG] candidates equal to the threshold per group
-    double* grp_q = nullptr;        // [NG * 4] kept positive sum, negative sum, counts
+    uint32_t* tile_unit0 = nullptr; // [max_tiles] unit holding each tile's first candidate
+    uint32_t* flags = nullptr;      // [4] device flags (0: some bracket missed)
+    uint2* cand = nullptr;          // [max(N,1)] candidates in ascending index order
+    uint32_t* cand_off = nullptr;   // [C + 1] first compact candidate of each chunk
+    uint32_t* ten_cbase = nullptr;  // [T + 1] first compact candidate of each tensor
+    uint32_t* tile_base = nullptr;  // [T + 1] first tile of each tensor
+    uint32_t* tile_gt = nullptr;    // [max_tiles] candidates above the threshold per tile
+    uint32_t* tile_eq = nullptr;    // [max_tiles] candidates equal to the threshold per tile
+    double* tile_q = nullptr;       // [max_tiles * 4] kept positive sum, negative sum, counts
     uint32_t* hist = nullptr;       // [S_max * kHistWords]
     SegState* seg = nullptr;        // [S_max]
     uint64_t* out_base = nullptr;   // [S_max] first output slot of each segment
-    uint32_t* skeys = nullptr;      // sample keys
-    uint32_t* seg_done = nullptr;   // [S_max] completion counters of the sample kernel
+    uint16_t* skeys = nullptr;      // 16-bit sample keys
+    uint32_t* loc = nullptr;        // [C] candidate offset of each unit inside its scan block
+    uint32_t* btot = nullptr;       // [scan blocks]
+    uint32_t* boff = nullptr;       // [scan blocks]
+    uint32_t* scan_done = nullptr;  // [1] completion counter of the scan blocks
+    uint32_t* raw_tbase = nullptr;  // [T + 1]
     uint32_t* qbase = nullptr;      // [T + 1] first output slot of each tensor
 };
 
@@ -52,9 +59,8 @@ struct gd_ctx {
     uint64_t N = 0;
     std::vector<uint64_t> offsets;
     uint32_t chunk_len = 0;
-    uint32_t group_chunks = 0;
     uint32_t num_chunks = 0;
-    uint32_t num_groups = 0;
+    uint32_t max_tiles = 0;
     uint32_t skeys_tensor = 0;
     uint32_t skeys_global = 0;
     gd::Tables tab;

@@ -1,0 +1,78 @@
+// Sign-mean 1-bit quantisation of the kept values (Section 5.4), with the
+// quantisation error fed back into the residual (gfx950, wave64).
+//
+// After dropping, each kept value is replaced by one of two centres per
+// tensor: the average of that tensor's kept positive values (values not
+// below zero) or of its kept negative values.  Sums are taken in fp64 in a
+// fixed order (per candidate tile, then tiles in order), so results are
+// deterministic.  The sent bits are packed LSB-first, 32 per word, and
+// residual[idx] becomes acc - centre.
+
+#include "gd_kernels.h"
+
+namespace gd {
+
+__global__ __launch_bounds__(kBlock) void k_means(QuantArgs q) {
+    const int w = threadIdx.x >> 6, lane = lane_id();
+    const uint32_t t = blockIdx.x * kWavesPerBlock + w;
+    if (t >= q.T) return;
+    const uint32_t g0 = q.tile_base[t], g1 = q.tile_base[t + 1];
+    double sp = 0.0, sn = 0.0, np = 0.0, nn = 0.0;
+    for (uint32_t g = g0 + lane; g < g1; g += kWave) {
+        sp += q.tile_q[4 * (size_t)g + 0];
+        sn += q.tile_q[4 * (size_t)g + 1];
+        np += q.tile_q[4 * (size_t)g + 2];
+        nn += q.tile_q[4 * (size_t)g + 3];
+    }
+    sp = wave_sum(sp);
+    sn = wave_sum(sn);
+    np = wave_sum(np);
+    nn = wave_sum(nn);
+    uint32_t before = 0;
+    for (uint32_t u = lane; u < t; u += kWave) before += q.tensor_counts[u];
+    before = wave_sum(before);
+    if (lane == 0) {
+        q.means[2 * t + 0] = np > 0.0 ? (float)(sp / np) : 0.0f;
+        q.means[2 * t + 1] = nn > 0.0 ? (float)(sn / nn) : 0.0f;
+        q.qbase[t] = before;
+        if (t + 1 == q.T) q.qbase[q.T] = before + q.tensor_counts[t];
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_quant(QuantArgs q) {
+    const uint64_t j = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+    const bool valid = j < q.k_total;
+    bool neg = false;
+    if (valid) {
+        // tensor of output slot j: the last t with qbase[t] <= j
+        uint32_t lo = 0, hi = q.T;
+        while (hi - lo > 1) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (q.qbase[mid] <= j) lo = mid;
+            else hi = mid;
+        }
+        const float x = q.val[j];
+        neg = x < 0.0f;
+        const float centre = neg ? q.means[2 * lo + 1] : q.means[2 * lo + 0];
+        const uint32_t i = q.idx[j];
+        if (i < q.N) q.res[i] = x - centre;
+    }
+    const uint64_t m = ballot(valid && neg);
+    const uint64_t jw = j - lane_id();  // first slot of this wave, a multiple of 64
+    const uint64_t words = (q.k_total + 31) / 32;
+    if (lane_id() == 0 && jw / 32 < words) q.sign_bits[jw / 32] = (uint32_t)m;
+    if (lane_id() == 1 && jw / 32 + 1 < words) q.sign_bits[jw / 32 + 1] = (uint32_t)(m >> 32);
+}
+
+static inline uint32_t blocks_for_waves(uint32_t waves) { return (waves + kWavesPerBlock - 1) / kWavesPerBlock; }
+
+hipError_t launch_quant(const QuantArgs& q, hipStream_t st) {
+    hipLaunchKernelGGL(k_means, dim3(blocks_for_waves(q.T)), dim3(kBlock), 0, st, q);
+    if (q.k_total > 0) {
+        const uint64_t blocks = (q.k_total + kBlock - 1) / kBlock;
+        hipLaunchKernelGGL(k_quant, dim3((uint32_t)blocks), dim3(kBlock), 0, st, q);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace gd
