@@ -115,27 +115,25 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
     ctx->N = N;
     ctx->offsets.assign(off, off + T + 1);
 
-    // Units of the dense pass: up to 1024 consecutive elements of one tensor.
-    const uint64_t cl = gd::kUnitLen;
-    ctx->chunk_len = (uint32_t)cl;
-
-    std::vector<uint32_t> cs, clen, ct, tc0(T + 1), toff(T + 1);
+    // Units of the dense pass: the 1024-element blocks of the flat gradient.
+    const uint32_t C = (uint32_t)((N + gd::kUnitLen - 1) / gd::kUnitLen);
+    ctx->num_units = C;
+    std::vector<uint32_t> toff(T + 1), info(C);
     uint64_t max_tiles = 0;
-    for (uint32_t t = 0; t < T; ++t) {
-        toff[t] = (uint32_t)off[t];
-        tc0[t] = (uint32_t)cs.size();
-        const uint64_t n = off[t + 1] - off[t];
-        for (uint64_t j = 0; j < n; j += cl) {
-            cs.push_back((uint32_t)(off[t] + j));
-            clen.push_back((uint32_t)std::min<uint64_t>(cl, n - j));
-            ct.push_back(t);
-        }
-        max_tiles += (n + gd::kTile - 1) / gd::kTile;
-    }
-    toff[T] = (uint32_t)N;
-    tc0[T] = (uint32_t)cs.size();
-    ctx->num_chunks = (uint32_t)cs.size();
+    for (uint32_t t = 0; t <= T; ++t) toff[t] = (uint32_t)off[t];
+    for (uint32_t t = 0; t < T; ++t) max_tiles += (off[t + 1] - off[t] + gd::kTile - 1) / gd::kTile;
     ctx->max_tiles = (uint32_t)max_tiles;
+    {
+        uint32_t t = 0;
+        for (uint32_t u = 0; u < C; ++u) {
+            const uint64_t us = (uint64_t)u * gd::kUnitLen, ue = std::min<uint64_t>(us + gd::kUnitLen, N);
+            while (t + 1 < T && off[t + 1] <= us) ++t;  // last tensor starting at or before us
+            bool starts_inside = false;
+            for (uint32_t x = t + 1; x < T && off[x] < ue; ++x)
+                if (off[x] > us) starts_inside = true;
+            info[u] = t | (starts_inside ? 0x80000000u : 0u);
+        }
+    }
 
     std::vector<uint32_t> sk_t(T + 1), sk_g(2), goff = {0u, (uint32_t)N};
     uint32_t acc = 0;
@@ -149,30 +147,32 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
     sk_g[1] = ctx->skeys_global = sample_keys_for(0, N);
 
     const uint32_t S_max = T;
-    const uint32_t scan_blocks = (ctx->num_chunks + gd::kScanUnits - 1) / gd::kScanUnits;
-    bool ok = dev_upload(ctx, &ctx->tab.chunk_start, cs) && dev_upload(ctx, &ctx->tab.chunk_len, clen) &&
-              dev_upload(ctx, &ctx->tab.chunk_tensor, ct) && dev_upload(ctx, &ctx->tab.tensor_chunk0, tc0) &&
-              dev_upload(ctx, &ctx->tab.tensor_off, toff) && dev_upload(ctx, &ctx->tab.global_off, goff) &&
-              dev_upload(ctx, &ctx->tab.skey_base_tensor, sk_t) && dev_upload(ctx, &ctx->tab.skey_base_global, sk_g);
-    ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.cnt_lo, ctx->num_chunks) &&
-         dev_alloc(ctx, &ctx->scr.tile_unit0, ctx->max_tiles) && dev_alloc(ctx, &ctx->scr.flags, 4) &&
-         dev_alloc(ctx, &ctx->scr.cand, N) &&
-         dev_alloc(ctx, &ctx->scr.cand_off, ctx->num_chunks + 1) && dev_alloc(ctx, &ctx->scr.ten_cbase, T + 1) &&
-         dev_alloc(ctx, &ctx->scr.tile_base, T + 1) && dev_alloc(ctx, &ctx->scr.tile_gt, ctx->max_tiles) &&
-         dev_alloc(ctx, &ctx->scr.tile_eq, ctx->max_tiles) && dev_alloc(ctx, &ctx->scr.tile_q, 4 * (size_t)ctx->max_tiles) &&
-         dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) && dev_alloc(ctx, &ctx->scr.seg, S_max) &&
-         dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
+    const uint32_t scan_blocks = (C + gd::kScanUnits - 1) / gd::kScanUnits;
+    bool ok = dev_upload(ctx, &ctx->tab.unit_info, info) && dev_upload(ctx, &ctx->tab.tensor_off, toff) &&
+              dev_upload(ctx, &ctx->tab.global_off, goff) && dev_upload(ctx, &ctx->tab.skey_base_tensor, sk_t) &&
+              dev_upload(ctx, &ctx->tab.skey_base_global, sk_g);
+    const uint32_t MT = ctx->max_tiles;
+    ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.cnt_lo, C) &&
+         dev_alloc(ctx, &ctx->scr.split, T) && dev_alloc(ctx, &ctx->scr.loc, C) &&
+         dev_alloc(ctx, &ctx->scr.neloc, C) && dev_alloc(ctx, &ctx->scr.btot, scan_blocks) &&
+         dev_alloc(ctx, &ctx->scr.betot, scan_blocks) && dev_alloc(ctx, &ctx->scr.boff, scan_blocks) &&
+         dev_alloc(ctx, &ctx->scr.beoff, scan_blocks) && dev_alloc(ctx, &ctx->scr.ne_unit, C) &&
+         dev_alloc(ctx, &ctx->scr.ne_off, C + 1) && dev_alloc(ctx, &ctx->scr.num_ne, 1) &&
+         dev_alloc(ctx, &ctx->scr.raw_tbase, T + 1) && dev_alloc(ctx, &ctx->scr.cand_idx, N) &&
+         dev_alloc(ctx, &ctx->scr.cand_val, N) && dev_alloc(ctx, &ctx->scr.ten_cbase, T + 1) &&
+         dev_alloc(ctx, &ctx->scr.tile_base, T + 1) && dev_alloc(ctx, &ctx->scr.tile_ne0, MT) &&
+         dev_alloc(ctx, &ctx->scr.tile_tensor, MT) && dev_alloc(ctx, &ctx->scr.tile_gt, MT) &&
+         dev_alloc(ctx, &ctx->scr.tile_eq, MT) && dev_alloc(ctx, &ctx->scr.tile_q, 4 * (size_t)MT) &&
+         dev_alloc(ctx, &ctx->scr.flags, 4) && dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) &&
+         dev_alloc(ctx, &ctx->scr.seg, S_max) && dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
          dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&
-         dev_alloc(ctx, &ctx->scr.loc, ctx->num_chunks) && dev_alloc(ctx, &ctx->scr.btot, scan_blocks) &&
-         dev_alloc(ctx, &ctx->scr.boff, scan_blocks) && dev_alloc(ctx, &ctx->scr.scan_done, 1) &&
-         dev_alloc(ctx, &ctx->scr.raw_tbase, T + 1) && dev_alloc(ctx, &ctx->scr.qbase, T + 1);
+         dev_alloc(ctx, &ctx->scr.qbase, T + 1);
     if (!ok) {
         free_all(ctx);
         delete ctx;
         return GD_ERR_OOM;
     }
-    if (hipMemset(ctx->scr.scan_done, 0, sizeof(uint32_t)) != hipSuccess ||
-        hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
+    if (hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
         free_all(ctx);
         delete ctx;
@@ -230,32 +230,32 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     da.grad = grad;
     da.base = base;
     da.res = residual;
-    da.chunk_start = ctx->tab.chunk_start;
-    da.chunk_len = ctx->tab.chunk_len;
-    da.chunk_tensor = ctx->tab.chunk_tensor;
-    da.num_chunks = ctx->num_chunks;
+    da.unit_info = ctx->tab.unit_info;
+    da.tensor_off = ctx->tab.tensor_off;
+    da.num_units = ctx->num_units;
+    da.N = (uint32_t)ctx->N;
+    da.T = ctx->T;
+    da.split = ctx->scr.split;
     da.per_tensor = per;
     da.seg = ctx->scr.seg;
     da.slots = ctx->scr.slots;
     da.cnt_lo = ctx->scr.cnt_lo;
-    const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_chunks > 0;
+    const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_units > 0;
     if (timed && hipEventRecord(ctx->events[ctx->events_used], st) != hipSuccess) return GD_ERR_HIP;
     if (gd::launch_dense(da, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
     if (timed) {
         if (hipEventRecord(ctx->events[ctx->events_used + 1], st) != hipSuccess) return GD_ERR_HIP;
         ctx->events_used += 2;
     }
-    if (ctx->num_chunks > 0) ++ctx->dense_launches;
+    if (ctx->num_units > 0) ++ctx->dense_launches;
 
     gd::CandArgs ca{};
     ca.res = residual;
-    ca.chunk_start = ctx->tab.chunk_start;
-    ca.chunk_len = ctx->tab.chunk_len;
-    ca.chunk_tensor = ctx->tab.chunk_tensor;
-    ca.tensor_chunk0 = ctx->tab.tensor_chunk0;
+    ca.unit_info = ctx->tab.unit_info;
     ca.tensor_off = ctx->tab.tensor_off;
     ca.seg_off = seg_off;
-    ca.num_chunks = ctx->num_chunks;
+    ca.num_units = ctx->num_units;
+    ca.N = (uint32_t)ctx->N;
     ca.T = ctx->T;
     ca.per_tensor = per;
     ca.keep_ppm = ppm;
@@ -263,16 +263,23 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ca.hist = ctx->scr.hist;
     ca.slots = ctx->scr.slots;
     ca.cnt_lo = ctx->scr.cnt_lo;
+    ca.split = ctx->scr.split;
     ca.loc = ctx->scr.loc;
+    ca.neloc = ctx->scr.neloc;
     ca.btot = ctx->scr.btot;
+    ca.betot = ctx->scr.betot;
     ca.boff = ctx->scr.boff;
-    ca.scan_done = ctx->scr.scan_done;
+    ca.beoff = ctx->scr.beoff;
+    ca.ne_unit = ctx->scr.ne_unit;
+    ca.ne_off = ctx->scr.ne_off;
+    ca.num_ne = ctx->scr.num_ne;
     ca.raw_tbase = ctx->scr.raw_tbase;
-    ca.cand = ctx->scr.cand;
-    ca.cand_off = ctx->scr.cand_off;
+    ca.cand_idx = ctx->scr.cand_idx;
+    ca.cand_val = ctx->scr.cand_val;
     ca.ten_cbase = ctx->scr.ten_cbase;
     ca.tile_base = ctx->scr.tile_base;
-    ca.tile_unit0 = ctx->scr.tile_unit0;
+    ca.tile_ne0 = ctx->scr.tile_ne0;
+    ca.tile_tensor = ctx->scr.tile_tensor;
     ca.flags = ctx->scr.flags;
     ca.tile_gt = ctx->scr.tile_gt;
     ca.tile_eq = ctx->scr.tile_eq;
@@ -339,8 +346,8 @@ gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode) {
 gd_status gd_debug_state(gd_ctx* ctx, uint32_t* seg_words, uint32_t max_segments, uint64_t* info) {
     if (!ctx || !info || (max_segments && !seg_words)) return GD_ERR_ARG;
     DeviceGuard guard(ctx->device);
-    info[0] = ctx->chunk_len;
-    info[1] = ctx->num_chunks;
+    info[0] = gd::kUnitLen;
+    info[1] = ctx->num_units;
     info[2] = gd::kTile;
     info[3] = ctx->max_tiles;
     const uint32_t n = std::min(max_segments, ctx->T);

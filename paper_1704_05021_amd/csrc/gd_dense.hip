@@ -10,8 +10,11 @@
 // surely kept, so their residual is written as +0 now; the emit pass fixes
 // the few that end up on the other side of the exact threshold.
 //
-// A unit is up to 1024 consecutive elements of one tensor, processed by one
-// wave: four 16-byte loads per lane per input array, all issued before use.
+// A unit is the 1024 elements [1024u, 1024u + 1024) of the flat gradient,
+// one block of 256 threads with one 16-byte vector per thread, so every
+// load is aligned and issued before any table lookup.  A unit that holds a
+// tensor boundary also records, for each tensor starting inside it, how many
+// of its candidates precede that start (the candidate layout needs it).
 
 #include "gd_kernels.h"
 
@@ -27,100 +30,126 @@ __device__ __forceinline__ float acc_of(float g, float b, float r) {
     return g + r;
 }
 
+// Tensor holding element e: the last t with off[t] <= e (empty tensors share
+// their successor's offset, so the last one is the tensor that holds e).
+__device__ __forceinline__ uint32_t tensor_of(const uint32_t* off, uint32_t T, uint32_t e) {
+    uint32_t lo = 0, hi = T;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (off[mid] <= e) lo = mid;
+        else hi = mid;
+    }
+    return lo;
+}
+
 template <bool BASE>
 __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
-    const int w = threadIdx.x >> 6, lane = lane_id();
-    const uint32_t c = blockIdx.x * kWavesPerBlock + w;
-    if (c >= a.num_chunks) return;
+    __shared__ uint32_t wcnt[kWavesPerBlock];
+    const uint32_t u = blockIdx.x;
+    const int tid = threadIdx.x, w = tid >> 6, lane = lane_id();
+    const uint32_t ustart = u * kUnitLen;
+    const uint32_t uend = ustart + kUnitLen < a.N ? ustart + kUnitLen : a.N;
+    const uint32_t e0 = ustart + 4 * tid;
 
-    const uint32_t start = a.chunk_start[c], len = a.chunk_len[c], end = start + len;
-    const uint32_t vb = start >> 2, ve = (end + 3) >> 2;
-    const f4* g4 = reinterpret_cast<const f4*>(a.grad);
-    const f4* b4 = reinterpret_cast<const f4*>(BASE ? a.base : a.grad);
-    f4* r4 = reinterpret_cast<f4*>(a.res);
-    uint2* out = a.slots + start;
-    uint32_t nc = 0;
-
-    for (uint32_t v0 = vb; v0 < ve; v0 += 4 * kWave) {
-        // Issue every load of this step before the table lookups they do not need.
-        f4 g[4], b[4], r[4];
+    f4 g = {0.f, 0.f, 0.f, 0.f}, b = g, r = g;
+    if (e0 + 4 <= uend) {
+        g = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.grad) + (e0 >> 2));
+        if (BASE) b = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.base) + (e0 >> 2));
+        r = reinterpret_cast<const f4*>(a.res)[e0 >> 2];
+    } else {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint32_t v = v0 + u * kWave + lane;
-            const uint32_t e0 = 4 * v;
-            const f4 z = {0.f, 0.f, 0.f, 0.f};
-            g[u] = z;
-            b[u] = z;
-            r[u] = z;
-            if (v < ve) {
-                if (e0 >= start && e0 + 4 <= end) {
-                    g[u] = __builtin_nontemporal_load(g4 + v);
-                    if (BASE) b[u] = __builtin_nontemporal_load(b4 + v);
-                    r[u] = r4[v];
-                } else {
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const uint32_t e = e0 + q;
-                        if (e >= start && e < end) {
-                            g[u][q] = a.grad[e];
-                            if (BASE) b[u][q] = a.base[e];
-                            r[u][q] = a.res[e];
-                        }
-                    }
-                }
-            }
-        }
-        const uint32_t s = a.per_tensor ? a.chunk_tensor[c] : 0u;
-        const uint32_t lo = a.seg[s].lo, hi = a.seg[s].hi;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint32_t v = v0 + u * kWave + lane;
-            const uint32_t e0 = 4 * v;
-            const bool inside = v < ve;
-            const bool full = inside && e0 >= start && e0 + 4 <= end;
-            float acc[4];
-            bool cand[4];
-            f4 ov;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const uint32_t e = e0 + q;
-                const bool valid = inside && e >= start && e < end;
-                acc[q] = acc_of<BASE>(g[u][q], b[u][q], r[u][q]);
-                const uint32_t key = key_of(acc[q]);
-                cand[q] = valid && key >= lo;
-                ov[q] = (valid && key >= hi) ? 0.0f : acc[q];
-            }
-            if (full) {
-                r4[v] = ov;
-            } else if (inside) {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const uint32_t e = e0 + q;
-                    if (e >= start && e < end) a.res[e] = ov[q];
-                }
-            }
-            const uint64_t m0 = ballot(cand[0]), m1 = ballot(cand[1]), m2 = ballot(cand[2]), m3 = ballot(cand[3]);
-            if ((m0 | m1 | m2 | m3) != 0) {
-                uint32_t pos = nc + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    if (cand[q]) {
-                        out[pos] = make_uint2(e0 + q, __float_as_uint(acc[q]));
-                        ++pos;
-                    }
-                }
-                nc += popc64(m0) + popc64(m1) + popc64(m2) + popc64(m3);
+        for (int q = 0; q < 4; ++q) {
+            if (e0 + q < uend) {
+                g[q] = a.grad[e0 + q];
+                if (BASE) b[q] = a.base[e0 + q];
+                r[q] = a.res[e0 + q];
             }
         }
     }
-    if (lane == 0) a.cnt_lo[c] = nc;
+    const uint32_t info = a.unit_info[u];
+    const bool boundary = (info >> 31) != 0;
+    uint32_t lo[4], hi[4];
+    if (!a.per_tensor || !boundary) {
+        const uint32_t s = a.per_tensor ? (info & 0x7FFFFFFFu) : 0u;
+        const uint32_t l = a.seg[s].lo, h = a.seg[s].hi;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            lo[q] = l;
+            hi[q] = h;
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            lo[q] = hi[q] = kNoKey;
+            if (e0 + q < uend) {
+                const uint32_t s = tensor_of(a.tensor_off, a.T, e0 + q);
+                lo[q] = a.seg[s].lo;
+                hi[q] = a.seg[s].hi;
+            }
+        }
+    }
+    float acc[4];
+    bool cand[4];
+    f4 ov;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const bool valid = e0 + q < uend;
+        acc[q] = acc_of<BASE>(g[q], b[q], r[q]);
+        const uint32_t key = key_of(acc[q]);
+        cand[q] = valid && key >= lo[q];
+        ov[q] = (valid && key >= hi[q]) ? 0.0f : acc[q];
+    }
+    if (e0 + 4 <= uend) {
+        reinterpret_cast<f4*>(a.res)[e0 >> 2] = ov;
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (e0 + q < uend) a.res[e0 + q] = ov[q];
+    }
+    // ordered compaction over the block: waves in order, lanes in order,
+    // then the four elements of a lane
+    const uint64_t m0 = ballot(cand[0]), m1 = ballot(cand[1]), m2 = ballot(cand[2]), m3 = ballot(cand[3]);
+    if (lane == 0) wcnt[w] = popc64(m0) + popc64(m1) + popc64(m2) + popc64(m3);
+    __syncthreads();
+    uint32_t base = 0, total = 0;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+        base += i < w ? wcnt[i] : 0u;
+        total += wcnt[i];
+    }
+    if ((m0 | m1 | m2 | m3) != 0) {
+        uint32_t pos = base + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
+        uint2* out = a.slots + ustart;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (cand[q]) {
+                out[pos] = make_uint2(e0 + q, __float_as_uint(acc[q]));
+                ++pos;
+            }
+        }
+    }
+    if (tid == 0) a.cnt_lo[u] = total;
+    if (boundary) {
+        // candidates before each tensor start strictly inside the unit
+        __shared__ uint32_t red[kWavesPerBlock];
+        for (uint32_t t = (info & 0x7FFFFFFFu) + 1; t < a.T && a.tensor_off[t] < uend; ++t) {
+            const uint32_t x = a.tensor_off[t];
+            if (x <= ustart) continue;
+            uint32_t c = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) c += cand[q] && e0 + q < x;
+            c = wave_sum(c);
+            __syncthreads();
+            if (lane == 0) red[w] = c;
+            __syncthreads();
+            if (tid == 0) a.split[t] = red[0] + red[1] + red[2] + red[3];
+        }
+    }
 }
 
-static inline uint32_t blocks_for_waves(uint32_t waves) { return (waves + kWavesPerBlock - 1) / kWavesPerBlock; }
-
 hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st) {
-    if (a.num_chunks == 0) return hipSuccess;
-    const dim3 grid(blocks_for_waves(a.num_chunks));
+    if (a.num_units == 0) return hipSuccess;
+    const dim3 grid(a.num_units);
     if (has_base) hipLaunchKernelGGL(k_dense<true>, grid, dim3(kBlock), 0, st, a);
     else hipLaunchKernelGGL(k_dense<false>, grid, dim3(kBlock), 0, st, a);
     return hipGetLastError();

@@ -17,15 +17,18 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 // value and NaN above Inf).  Every key is below 2^31.
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;  // above every key: "nothing qualifies"
 
-// The 31 key bits are resolved in three radix digits, most significant first.
+// The 31 key bits are resolved in four radix digits, most significant first.
+// The second digit is narrow: the candidates that share the threshold's
+// first digit are many and spread out, and a narrow digit keeps their
+// histogram (and its global atomics) small.
 constexpr int kD0Shift = 21, kNB0 = 1024;  // key bits 30..21
-constexpr int kD1Shift = 10, kNB1 = 2048;  // key bits 20..10
-constexpr int kNB2 = 1024;                 // key bits  9..0
+constexpr int kD1Shift = 15, kNB1 = 64;    // key bits 20..15
+constexpr int kD2Shift = 5, kNB2 = 1024;   // key bits 14..5
+constexpr int kNB3 = 32;                   // key bits  4..0
 
-// Histogram words per threshold segment: digit 0 (dense pass), digit 0
-// (fallback pass), digit 1, digit 2.
-constexpr int kHistH0 = 0, kHistH0Fb = kNB0, kHistH1 = 2 * kNB0, kHistH2 = 2 * kNB0 + kNB1;
-constexpr int kHistWords = 2 * kNB0 + kNB1 + kNB2;
+// Histogram words per threshold segment, one histogram per digit.
+constexpr int kHistH0 = 0, kHistH1 = kNB0, kHistH2 = kNB0 + kNB1, kHistH3 = kNB0 + kNB1 + kNB2;
+constexpr int kHistWords = kNB0 + kNB1 + kNB2 + kNB3;
 
 // Sampling: units of 16 consecutive elements (one 64-byte line per array),
 // at most kMaxUnits units per segment.  A sample key is the top 16 bits of
@@ -51,13 +54,15 @@ struct SegState {
     uint32_t hi;    // the dense pass wrote residual = +0 where key >= hi
     uint32_t clo;   // number of candidates (key >= lo)
     uint32_t miss;  // 1 when fewer than k candidates: every element becomes one
-    uint32_t d0;    // digit 0 of the threshold key
+    uint32_t d0;    // digit 0 of the threshold key (key >> 21)
     uint32_t r1;    // rank of the threshold among candidates with that digit 0
-    uint32_t p21;   // digits 0 and 1 of the threshold key
-    uint32_t r2;    // rank among candidates with that 21-bit prefix
+    uint32_t p16;   // key >> 15 of the threshold key
+    uint32_t r2;    // rank among candidates with that prefix
+    uint32_t p26;   // key >> 5 of the threshold key
+    uint32_t r3;    // rank among candidates with that prefix
     uint32_t thr;   // the threshold key T (kNoKey when nothing is kept)
     uint32_t need;  // entries with key == T to keep, lowest index first
-    uint32_t pad[6];
+    uint32_t pad[4];
 };
 
 __device__ __forceinline__ uint32_t key_of(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }
@@ -109,14 +114,14 @@ __device__ __forceinline__ double wave_sum(double v) {
 // elements.  Called by a whole wave; hist may be global or LDS memory.
 template <int NB>
 __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uint32_t& above) {
-    constexpr int B = NB / kWave;
+    constexpr int B = NB >= kWave ? NB / kWave : 1;
     const int lane = lane_id();
-    const int top = NB - lane * B;  // this lane owns bins [top - B, top), high to low
+    const int top = NB - lane * B;  // this lane owns bins [top - B, top), high to low (none when top <= 0)
     uint32_t c[B];
     uint32_t sum = 0;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-        c[i] = hist[top - 1 - i];
+        c[i] = top - 1 - i >= 0 ? hist[top - 1 - i] : 0u;
         sum += c[i];
     }
     const uint32_t incl = wave_incl_scan(sum);
@@ -148,23 +153,11 @@ __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uin
     return true;
 }
 
-// Adds 1 to h[bin] for every active lane.  Up to three times, the lanes that
-// share the first remaining lane's bin are combined into one LDS atomic, so a
-// wave whose entries fall in a few bins (exact zeros, equal values, the
-// exponent bins of a Gaussian) does not serialise on them.  Must be called
-// by the whole wave.
+// Adds 1 to h[bin] for every active lane (an LDS atomic; lanes that hit the
+// same bin are serialised by the hardware, which is cheaper than combining
+// them first with cross-lane operations).
 __device__ __forceinline__ void lds_hist_add(uint32_t* h, uint32_t bin, bool active) {
-    uint64_t act = ballot(active);
-#pragma unroll
-    for (int round = 0; round < 3; ++round) {
-        if (act == 0) return;
-        const int leader = __ffsll((unsigned long long)act) - 1;
-        const uint32_t lbin = __shfl(bin, leader, kWave);
-        const uint64_t ms = ballot(active && bin == lbin) & act;
-        if (lane_id() == leader) atomicAdd(&h[lbin], popc64(ms));
-        act &= ~ms;
-    }
-    if ((act >> lane_id()) & 1ull) atomicAdd(&h[bin], 1u);
+    if (active) atomicAdd(&h[bin], 1u);
 }
 
 // Exclusive prefix over a block of NT threads; *total receives the block sum.

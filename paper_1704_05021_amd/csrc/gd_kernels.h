@@ -34,28 +34,28 @@ struct DenseArgs {
     const float* grad;
     const float* base;  // nullable
     float* res;
-    const uint32_t* chunk_start;
-    const uint32_t* chunk_len;
-    const uint32_t* chunk_tensor;
-    uint32_t num_chunks;
+    const uint32_t* unit_info;   // [C] tensor of the unit's first element | (holds a tensor start) << 31
+    const uint32_t* tensor_off;  // [T + 1]
+    uint32_t num_units;
+    uint32_t N;
+    uint32_t T;
     uint32_t per_tensor;
     const SegState* seg;
     uint2* slots;
     uint32_t* cnt_lo;
+    uint32_t* split;             // [T] candidates of a tensor's first unit that precede the tensor
 };
 
-constexpr uint32_t kTile = 2048;        // candidates per tile of the candidate passes
-constexpr uint32_t kTileBlocks = 2048;  // most blocks a candidate pass launches (4 waves each)
+constexpr uint32_t kTile = 1024;        // candidates per tile of the candidate passes
+constexpr uint32_t kTileBlocks = 512;   // most blocks a candidate pass launches (4 waves each)
 
 struct CandArgs {
     float* res;
-    const uint32_t* chunk_start;
-    const uint32_t* chunk_len;
-    const uint32_t* chunk_tensor;
-    const uint32_t* tensor_chunk0;  // [T + 1]
+    const uint32_t* unit_info;      // [C]
     const uint32_t* tensor_off;     // [T + 1] element offsets
     const uint32_t* seg_off;
-    uint32_t num_chunks;
+    uint32_t num_units;
+    uint32_t N;
     uint32_t T;
     uint32_t per_tensor;
     uint32_t keep_ppm;
@@ -63,16 +63,23 @@ struct CandArgs {
     uint32_t* hist;
     uint2* slots;
     uint32_t* cnt_lo;
+    const uint32_t* split;  // [T]
     uint32_t* loc;        // [C] candidate offset of each unit inside its scan block
+    uint32_t* neloc;      // [C] index of each non-empty unit inside its scan block
     uint32_t* btot;       // [scan blocks] candidates per scan block
+    uint32_t* betot;      // [scan blocks] non-empty units per scan block
     uint32_t* boff;       // [scan blocks] first candidate of each scan block
-    uint32_t* scan_done;  // completion counter of the scan blocks
-    uint32_t* cand_off;   // [C + 1] first candidate of each unit (dense-pass order)
-    uint32_t* raw_tbase;  // [T + 1] cand_off of each tensor's first unit
-    uint2* cand;          // [N] compact candidates, ascending flat index
+    uint32_t* beoff;      // [scan blocks] first non-empty unit of each scan block
+    uint32_t* ne_unit;    // [C] the non-empty units, in order
+    uint32_t* ne_off;     // [C + 1] their first candidate (dense-pass order); [count] = total
+    uint32_t* num_ne;     // [1] number of non-empty units
+    uint32_t* raw_tbase;  // [T + 1] first candidate of each tensor (dense-pass order)
+    uint32_t* cand_idx;   // [N] compact candidates, ascending flat index
+    uint32_t* cand_val;   // [N] their value bits
     uint32_t* ten_cbase;  // [T + 1] first compact candidate of each tensor
     uint32_t* tile_base;  // [T + 1] first tile of each tensor
-    uint32_t* tile_unit0; // [max tiles] unit holding each tile's first candidate
+    uint32_t* tile_ne0;   // [max tiles] non-empty unit holding each tile's first candidate
+    uint32_t* tile_tensor; // [max tiles] tensor of each tile
     uint32_t* tile_gt;    // [max tiles]
     uint32_t* tile_eq;
     double* tile_q;       // [max tiles * 4]

@@ -1,35 +1,38 @@
 // Candidate layout after the dense pass (gfx950, wave64).
 //
 //   k_scan   : scan blocks of 1024 units each scan their units' candidate
-//              counts; the last block to finish scans the block totals and
-//              derives, per threshold segment, the candidate total and
+//              counts.
+//   k_scan_final : one block scans the block totals and derives, per
+//              threshold segment, the candidate total and
 //              whether the bracket missed (fewer than k candidates), and per
-//              tensor the first compact candidate and the first tile (tiles
-//              of kTile candidates never cross a tensor).  A tensor of a
-//              missed segment takes every element as a candidate, read
-//              straight from the restored residual.
+//              tensor the first candidate in dense-pass order, the first
+//              compact candidate and the first tile (tiles of kTile
+//              candidates never cross a tensor).  A tensor of a missed
+//              segment takes every element as a candidate, read straight
+//              from the restored residual.
 //   k_layout : per unit, the candidate offset in dense-pass order, the tiles
-//              whose first candidate it holds, and (missed segments only)
-//              the residual restored to acc where the dense pass wrote +0.
+//              that start in it (their tensor and first unit), and, for
+//              missed segments only, the residual restored to acc where the
+//              dense pass wrote +0.
 
 #include "gd_kernels.h"
 
 namespace gd {
 
-// raw(u): candidates of units [0, u) in dense-pass order.
-__device__ __forceinline__ uint32_t raw_off(const CandArgs& a, const uint32_t* boff, uint32_t total, uint32_t u) {
-    return u < a.num_chunks ? a.loc[u] + boff[u / kScanUnits] : total;
-}
-
 constexpr uint32_t kMaxScanBlocks = 4096;  // 2^32 elements / 1024 per unit / 1024 units per block
+
+// Candidates (dense-pass order) before element offset x, x a tensor start.
+__device__ __forceinline__ uint32_t raw_start(const CandArgs& a, const uint32_t* boff, uint32_t grand, uint32_t t) {
+    const uint32_t x = a.tensor_off[t];
+    if (x >= a.N) return grand;
+    const uint32_t u = x / kUnitLen;
+    return a.loc[u] + boff[u / kScanUnits] + ((x % kUnitLen) ? a.split[t] : 0u);
+}
 
 __global__ __launch_bounds__(kScanThreads) void k_scan(CandArgs a) {
     __shared__ uint32_t lds[kScanThreads / kWave + 1];
-    __shared__ uint32_t boff[kMaxScanBlocks];
-    __shared__ int s_last;
-    __shared__ uint32_t any_miss;
     const int tid = threadIdx.x;
-    const uint32_t C = a.num_chunks;
+    const uint32_t C = a.num_units;
 
     // 1. local scan of this block's 1024 units (4 per thread)
     const uint32_t x = blockIdx.x * kScanUnits + 4 * tid;
@@ -44,49 +47,66 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(CandArgs a) {
         for (int q = 0; q < 4; ++q)
             if (x + q < C) c[q] = a.cnt_lo[x + q];
     }
-    uint32_t total;
+    uint32_t total, ne_total;
     const uint32_t excl = block_excl_scan<kScanThreads>(c[0] + c[1] + c[2] + c[3], lds, &total);
+    const uint32_t f[4] = {c[0] != 0, c[1] != 0, c[2] != 0, c[3] != 0};
+    const uint32_t nexcl = block_excl_scan<kScanThreads>(f[0] + f[1] + f[2] + f[3], lds, &ne_total);
     const uint32_t o[4] = {excl, excl + c[0], excl + c[0] + c[1], excl + c[0] + c[1] + c[2]};
+    const uint32_t n[4] = {nexcl, nexcl + f[0], nexcl + f[0] + f[1], nexcl + f[0] + f[1] + f[2]};
     if (x + 4 <= C) {
         *reinterpret_cast<uint4*>(a.loc + x) = make_uint4(o[0], o[1], o[2], o[3]);
+        *reinterpret_cast<uint4*>(a.neloc + x) = make_uint4(n[0], n[1], n[2], n[3]);
     } else {
         for (int q = 0; q < 4; ++q)
-            if (x + q < C) a.loc[x + q] = o[q];
+            if (x + q < C) {
+                a.loc[x + q] = o[q];
+                a.neloc[x + q] = n[q];
+            }
     }
-    if (tid == 0) a.btot[blockIdx.x] = total;
-
-    // 2. the last block to finish lays out segments and tensors
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = atomicAdd(a.scan_done, 1u) == gridDim.x - 1;
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
     if (tid == 0) {
-        any_miss = 0;
-        *a.scan_done = 0;
+        a.btot[blockIdx.x] = total;
+        a.betot[blockIdx.x] = ne_total;
     }
-    uint32_t carry = 0;
-    for (uint32_t b0 = 0; b0 < gridDim.x; b0 += kScanThreads) {
+}
+
+// One block: offsets of the scan blocks, then segments and tensors.
+__global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_t nblocks) {
+    __shared__ uint32_t lds[kScanThreads / kWave + 1];
+    __shared__ uint32_t boff[kMaxScanBlocks];
+    __shared__ uint32_t any_miss;
+    const int tid = threadIdx.x;
+    if (tid == 0) any_miss = 0;
+    uint32_t carry = 0, necarry = 0;
+    for (uint32_t b0 = 0; b0 < nblocks; b0 += kScanThreads) {
         const uint32_t b = b0 + tid;
-        const uint32_t t = b < gridDim.x ? a.btot[b] : 0u;
-        uint32_t tot;
+        const uint32_t t = b < nblocks ? a.btot[b] : 0u;
+        const uint32_t te = b < nblocks ? a.betot[b] : 0u;
+        uint32_t tot, netot;
         const uint32_t e = block_excl_scan<kScanThreads>(t, lds, &tot);
-        if (b < gridDim.x) {
+        const uint32_t ne = block_excl_scan<kScanThreads>(te, lds, &netot);
+        if (b < nblocks) {
             boff[b] = carry + e;
             a.boff[b] = carry + e;
+            a.beoff[b] = necarry + ne;
         }
         carry += tot;
+        necarry += netot;
     }
     const uint32_t grand = carry;
+    if (tid == 0) {
+        a.num_ne[0] = necarry;
+        a.ne_off[necarry] = grand;
+    }
+    __syncthreads();
+    // per tensor: first candidate in dense-pass order
+    for (uint32_t t = tid; t <= a.T; t += kScanThreads) a.raw_tbase[t] = raw_start(a, boff, grand, t);
+    __threadfence_block();
     __syncthreads();
     const uint32_t S = a.per_tensor ? a.T : 1u;
     for (uint32_t s = tid; s < S; s += kScanThreads) {
         const uint32_t n = a.seg_off[s + 1] - a.seg_off[s];
         const uint32_t k = keep_of(n, a.keep_ppm);
-        const uint32_t c0 = a.per_tensor ? a.tensor_chunk0[s] : 0u;
-        const uint32_t c1 = a.per_tensor ? a.tensor_chunk0[s + 1] : C;
-        const uint32_t cnt = raw_off(a, boff, grand, c1) - raw_off(a, boff, grand, c0);
+        const uint32_t cnt = a.per_tensor ? a.raw_tbase[s + 1] - a.raw_tbase[s] : grand;
         const uint32_t miss = (k > 0 && cnt < k) ? 1u : 0u;
         a.seg[s].clo = cnt;
         a.seg[s].miss = miss;
@@ -99,12 +119,9 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(CandArgs a) {
         const uint32_t t = b0 + tid;
         uint32_t cc = 0, tiles = 0;
         if (t < a.T) {
-            const uint32_t rb = raw_off(a, boff, grand, a.tensor_chunk0[t]);
-            const uint32_t re = raw_off(a, boff, grand, a.tensor_chunk0[t + 1]);
             const uint32_t s = a.per_tensor ? t : 0u;
-            cc = a.seg[s].miss ? a.tensor_off[t + 1] - a.tensor_off[t] : re - rb;
+            cc = a.seg[s].miss ? a.tensor_off[t + 1] - a.tensor_off[t] : a.raw_tbase[t + 1] - a.raw_tbase[t];
             tiles = (cc + kTile - 1) / kTile;
-            a.raw_tbase[t] = rb;
         }
         uint32_t ctot, ttot;
         const uint32_t ce = block_excl_scan<kScanThreads>(cc, lds, &ctot);
@@ -117,51 +134,86 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(CandArgs a) {
         tcarry += ttot;
     }
     if (tid == 0) {
-        a.raw_tbase[a.T] = grand;
         a.ten_cbase[a.T] = ccarry;
         a.tile_base[a.T] = tcarry;
         a.flags[0] = any_miss;
     }
 }
 
+// Tiles of tensor t whose first candidate lies in [p, q) (dense-pass order
+// for a regular tensor, element order for a missed one): record t and the
+// non-empty unit index ne.
+__device__ __forceinline__ void mark_tiles(const CandArgs& a, uint32_t t, uint32_t base, uint32_t p, uint32_t q,
+                                           uint32_t ne) {
+    const uint32_t t0 = a.tile_base[t];
+    for (uint32_t j = p > base ? (p - base + kTile - 1) / kTile : 0u; base + j * kTile < q; ++j) {
+        a.tile_tensor[t0 + j] = t;
+        a.tile_ne0[t0 + j] = ne;
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
     const uint32_t u = blockIdx.x * kBlock + threadIdx.x;
-    const bool have = u < a.num_chunks;
-    uint32_t t = 0, s = 0, raw = 0, cnt = 0;
-    bool miss = false;
+    const bool have = u < a.num_units;
+    uint32_t raw = 0, cnt = 0, info = 0;
+    bool restore = false;
     if (have) {
         raw = a.loc[u] + a.boff[u / kScanUnits];
         cnt = a.cnt_lo[u];
-        a.cand_off[u] = raw;
-        if (u + 1 == a.num_chunks) a.cand_off[u + 1] = raw + cnt;
-        t = a.chunk_tensor[u];
-        s = a.per_tensor ? t : 0u;
-        miss = a.seg[s].miss != 0;
-        if (!miss && cnt) {
-            const uint32_t rt = a.raw_tbase[t], t0 = a.tile_base[t];
-            for (uint32_t j = (raw - rt + kTile - 1) / kTile; rt + j * kTile < raw + cnt; ++j) a.tile_unit0[t0 + j] = u;
+        const uint32_t ne = a.neloc[u] + a.beoff[u / kScanUnits];
+        if (cnt) {
+            a.ne_unit[ne] = u;
+            a.ne_off[ne] = raw;
+        }
+        info = a.unit_info[u];
+        const uint32_t ustart = u * kUnitLen, uend = ustart + kUnitLen < a.N ? ustart + kUnitLen : a.N;
+        // every tensor overlapping the unit (one, unless it holds a boundary)
+        for (uint32_t t = info & 0x7FFFFFFFu; t < a.T && a.tensor_off[t] < uend; ++t) {
+            const uint32_t ta = a.tensor_off[t], tb = a.tensor_off[t + 1];
+            if (tb <= ustart || tb == ta) continue;
+            const uint32_t s = a.per_tensor ? t : 0u;
+            if (a.seg[s].miss) {
+                // direct tiles start at element offsets ta + j * kTile
+                const uint32_t lo_e = ta > ustart ? ta : ustart, hi_e = tb < uend ? tb : uend;
+                mark_tiles(a, t, ta, lo_e, hi_e, ne);
+                restore = restore || cnt > 0;
+            } else {
+                const uint32_t rb = a.raw_tbase[t], re = a.raw_tbase[t + 1];
+                const uint32_t p = raw > rb ? raw : rb, q = raw + cnt < re ? raw + cnt : re;
+                if (p < q) mark_tiles(a, t, rb, p, q, ne);
+            }
         }
     }
     // Missed segments: the dense pass wrote +0 where key >= hi; put acc back
     // from the unit's candidate list (one unit at a time, the whole wave).
-    uint64_t todo = ballot(have && miss && cnt > 0);
+    uint64_t todo = ballot(restore);
     while (todo) {
         const int src = __ffsll((unsigned long long)todo) - 1;
         todo &= todo - 1;
-        const uint32_t uu = __shfl(u, src, kWave), nn = __shfl(cnt, src, kWave), ss = __shfl(s, src, kWave);
-        const uint32_t start = a.chunk_start[uu], hi = a.seg[ss].hi;
+        const uint32_t uu = __shfl(u, src, kWave), nn = __shfl(cnt, src, kWave);
         for (uint32_t i = lane_id(); i < nn; i += kWave) {
-            const uint2 e = a.slots[start + i];
-            if ((e.y & 0x7FFFFFFFu) >= hi) a.res[e.x] = __uint_as_float(e.y);
+            const uint2 e = a.slots[(size_t)uu * kUnitLen + i];
+            uint32_t s = 0;
+            if (a.per_tensor) {
+                uint32_t lo = 0, hi = a.T;
+                while (hi - lo > 1) {
+                    const uint32_t mid = (lo + hi) >> 1;
+                    if (a.tensor_off[mid] <= e.x) lo = mid;
+                    else hi = mid;
+                }
+                s = lo;
+            }
+            if (a.seg[s].miss && (e.y & 0x7FFFFFFFu) >= a.seg[s].hi) a.res[e.x] = __uint_as_float(e.y);
         }
     }
 }
 
 hipError_t launch_layout(const CandArgs& a, hipStream_t st) {
-    if (a.num_chunks == 0) return hipSuccess;
-    const uint32_t sb = (a.num_chunks + kScanUnits - 1) / kScanUnits;
+    if (a.num_units == 0) return hipSuccess;
+    const uint32_t sb = (a.num_units + kScanUnits - 1) / kScanUnits;
     hipLaunchKernelGGL(k_scan, dim3(sb), dim3(kScanThreads), 0, st, a);
-    hipLaunchKernelGGL(k_layout, dim3((a.num_chunks + kBlock - 1) / kBlock), dim3(kBlock), 0, st, a);
+    hipLaunchKernelGGL(k_scan_final, dim3(1), dim3(kScanThreads), 0, st, a, sb);
+    hipLaunchKernelGGL(k_layout, dim3((a.num_units + kBlock - 1) / kBlock), dim3(kBlock), 0, st, a);
     return hipGetLastError();
 }
 
