@@ -153,7 +153,10 @@ gd_status gd_profile_read(gd_ctx* ctx, double* dense_ms, uint64_t* dense_launche
  * results do not change (they are exact whatever the bracket); only the
  * work done does.  mode 0: normal; 1: bracket above every key, so every
  * segment takes the exact fallback; 2: the dense pass zeroes every
- * candidate; 3: every element is a candidate.  GD_ERR_ARG for other modes.
+ * candidate; 3: every element is a candidate; 4: only keys at or above the
+ * point estimate are candidates and all of them are zeroed, so about half
+ * the segments take the exact fallback after the dense pass has zeroed
+ * part of their residual.  GD_ERR_ARG for other modes.
  */
 gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode);
 
@@ -163,7 +166,8 @@ gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode);
  * bracket lo and hi, candidate count, bracket-miss flag, radix digits and
  * ranks, threshold key, ties kept) for up to max_segments segments into
  * seg_words (host), and the decomposition into info (host, 4 entries:
- * chunk length, chunks, chunks per group, groups).  Synchronises the host.
+ * elements per dense-pass unit, units, candidates per tile, most tiles).
+ * Synchronises the host.
  */
 gd_status gd_debug_state(gd_ctx* ctx, uint32_t* seg_words, uint32_t max_segments, uint64_t* info);
 

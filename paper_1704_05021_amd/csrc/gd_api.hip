@@ -39,7 +39,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 uint32_t sample_keys_for(uint64_t a, uint64_t b) {
     if (b <= a) return 0;
     const uint64_t n16 = ((b - 1) >> 4) - (a >> 4) + 1;
-    return (uint32_t)(kUnit * std::min<uint64_t>(n16, kMaxUnits));
+    return (uint32_t)kUnit * gd::sample_unit_count((uint32_t)n16);
 }
 
 template <typename T>
@@ -152,12 +152,12 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
               dev_upload(ctx, &ctx->tab.global_off, goff) && dev_upload(ctx, &ctx->tab.skey_base_tensor, sk_t) &&
               dev_upload(ctx, &ctx->tab.skey_base_global, sk_g);
     const uint32_t MT = ctx->max_tiles;
-    ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.cnt_lo, C) &&
+    ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.wcnt, 4 * (size_t)C) &&
          dev_alloc(ctx, &ctx->scr.split, T) && dev_alloc(ctx, &ctx->scr.loc, C) &&
          dev_alloc(ctx, &ctx->scr.neloc, C) && dev_alloc(ctx, &ctx->scr.btot, scan_blocks) &&
          dev_alloc(ctx, &ctx->scr.betot, scan_blocks) && dev_alloc(ctx, &ctx->scr.boff, scan_blocks) &&
          dev_alloc(ctx, &ctx->scr.beoff, scan_blocks) && dev_alloc(ctx, &ctx->scr.ne_unit, C) &&
-         dev_alloc(ctx, &ctx->scr.ne_off, C + 1) && dev_alloc(ctx, &ctx->scr.num_ne, 1) &&
+         dev_alloc(ctx, &ctx->scr.ne_off, C + 1) && dev_alloc(ctx, &ctx->scr.ne_sub, C) && dev_alloc(ctx, &ctx->scr.num_ne, 1) &&
          dev_alloc(ctx, &ctx->scr.raw_tbase, T + 1) && dev_alloc(ctx, &ctx->scr.cand_idx, N) &&
          dev_alloc(ctx, &ctx->scr.cand_val, N) && dev_alloc(ctx, &ctx->scr.ten_cbase, T + 1) &&
          dev_alloc(ctx, &ctx->scr.tile_base, T + 1) && dev_alloc(ctx, &ctx->scr.tile_ne0, MT) &&
@@ -166,13 +166,14 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
          dev_alloc(ctx, &ctx->scr.flags, 4) && dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) &&
          dev_alloc(ctx, &ctx->scr.seg, S_max) && dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
          dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&
-         dev_alloc(ctx, &ctx->scr.qbase, T + 1);
+         dev_alloc(ctx, &ctx->scr.qbase, T + 1) && dev_alloc(ctx, &ctx->scr.shist, (size_t)S_max * gd::kSHistWords);
     if (!ok) {
         free_all(ctx);
         delete ctx;
         return GD_ERR_OOM;
     }
     if (hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
+        hipMemset(ctx->scr.shist, 0, (size_t)S_max * gd::kSHistWords * sizeof(uint32_t)) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
         free_all(ctx);
         delete ctx;
@@ -222,6 +223,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     sa.skeys = ctx->scr.skeys;
     sa.seg = ctx->scr.seg;
     sa.hist = ctx->scr.hist;
+    sa.shist = ctx->scr.shist;
     sa.out_base = ctx->scr.out_base;
     sa.tensor_counts = out->tensor_counts;
     if (gd::launch_sample(sa, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
@@ -239,7 +241,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     da.per_tensor = per;
     da.seg = ctx->scr.seg;
     da.slots = ctx->scr.slots;
-    da.cnt_lo = ctx->scr.cnt_lo;
+    da.wcnt = ctx->scr.wcnt;
     const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_units > 0;
     if (timed && hipEventRecord(ctx->events[ctx->events_used], st) != hipSuccess) return GD_ERR_HIP;
     if (gd::launch_dense(da, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
@@ -262,7 +264,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ca.seg = ctx->scr.seg;
     ca.hist = ctx->scr.hist;
     ca.slots = ctx->scr.slots;
-    ca.cnt_lo = ctx->scr.cnt_lo;
+    ca.wcnt = ctx->scr.wcnt;
     ca.split = ctx->scr.split;
     ca.loc = ctx->scr.loc;
     ca.neloc = ctx->scr.neloc;
@@ -272,6 +274,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ca.beoff = ctx->scr.beoff;
     ca.ne_unit = ctx->scr.ne_unit;
     ca.ne_off = ctx->scr.ne_off;
+    ca.ne_sub = ctx->scr.ne_sub;
     ca.num_ne = ctx->scr.num_ne;
     ca.raw_tbase = ctx->scr.raw_tbase;
     ca.cand_idx = ctx->scr.cand_idx;
@@ -338,7 +341,7 @@ gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const 
 }
 
 gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode) {
-    if (!ctx || mode < 0 || mode > 3) return GD_ERR_ARG;
+    if (!ctx || mode < 0 || mode > 4) return GD_ERR_ARG;
     ctx->debug_bracket = (uint32_t)mode;
     return GD_OK;
 }

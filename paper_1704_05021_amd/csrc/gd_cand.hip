@@ -5,13 +5,13 @@
 // candidates of one tensor, one wave per tile, so the work is balanced
 // however unevenly the candidates fall across the gradient.
 //
-//   k_gather     : compacts each tile's candidates from the per-unit slots
-//                  (or, for a missed segment, straight from the residual)
-//                  into one array in ascending flat index, with the digit-0
-//                  histogram.
+//   k_gather     : compacts each tile's candidates from the per-quarter
+//                  slots (or, for a missed segment, straight from the
+//                  residual) into one array in ascending flat index, with
+//                  the digit-0 histogram.
 //   k_radix<L>   : digit L-1 of the k-th largest key from the previous
 //                  histogram; the histogram of digit L over the candidates
-//                  that share the prefix found so far (L = 1, 2, 3).
+//                  that share the prefix found so far (L = 1, 2).
 //   k_count      : the last digit, i.e. the exact threshold key T and the
 //                  number of candidates equal to T to keep (lowest index
 //                  first); per tile, the candidates above and equal to T.
@@ -22,6 +22,11 @@
 //
 // Together they realise the exact-k rule: keep the k largest |acc| of each
 // segment, ties broken by lower flat index (Algorithm 1, Section 4).
+//
+// The histogram passes run in rounds of four consecutive tiles per block;
+// each wave counts into its own LDS histogram and the block adds the four
+// to the segment histogram once per round (waves of one segment merged), so
+// the global atomics on the few hot bins are a quarter of one per tile.
 
 #include "gd_kernels.h"
 
@@ -49,16 +54,42 @@ __device__ __forceinline__ uint32_t* seg_hist(const CandArgs& a, uint32_t s, int
     return a.hist + (size_t)s * kHistWords + which;
 }
 
-__device__ __forceinline__ void flush_hist(uint32_t* hw, uint32_t* hg, int nb) {
-    wave_lds_sync();
-    for (int i = lane_id(); i < nb; i += kWave) {
-        const uint32_t x = hw[i];
-        if (x) {
-            atomicAdd(&hg[i], x);
-            hw[i] = 0;
+// Adds the block's four per-wave histograms (16-bit counters, two bins per
+// word: a wave counts at most one tile of kTile candidates per round) to
+// their segments' histograms and clears them.  wseg[w] is wave w's segment
+// this round (kNoKey: no tile); waves of one segment are summed first.
+// Called by the whole block.
+template <int NB>
+__device__ __forceinline__ void block_flush(const CandArgs& a, uint32_t (*lh)[NB / 2], const uint32_t* wseg,
+                                            int which) {
+    static_assert(kWavesPerBlock * kTile < 65536, "16-bit histogram counters");
+    __syncthreads();
+    uint32_t sg[kWavesPerBlock];
+    for (int i = threadIdx.x; i < NB / 2; i += kBlock) {
+        uint32_t h[kWavesPerBlock];
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) {
+            sg[w] = wseg[w];
+            h[w] = lh[w][i];
+            lh[w][i] = 0;
+        }
+#pragma unroll
+        for (int w = 0; w < kWavesPerBlock; ++w) {
+            if (sg[w] == kNoKey) continue;
+            uint32_t sum = h[w];
+#pragma unroll
+            for (int v = w + 1; v < kWavesPerBlock; ++v) {
+                if (sg[v] == sg[w]) {
+                    sum += h[v];
+                    sg[v] = kNoKey;
+                }
+            }
+            uint32_t* g = seg_hist(a, sg[w], which) + 2 * i;
+            if (sum & 0xFFFFu) atomicAdd(g, sum & 0xFFFFu);
+            if (sum >> 16) atomicAdd(g + 1, sum >> 16);
         }
     }
-    wave_lds_sync();
+    __syncthreads();
 }
 
 constexpr int kRows = kTile / kWave;  // rows of 64 candidates in a tile
@@ -68,19 +99,28 @@ constexpr uint32_t kWin = kTile;      // non-empty units held in the gather wind
 // units, so a window of kTile non-empty units starting at the unit that
 // holds the tile's first candidate always covers the tile.
 __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
-    __shared__ uint32_t lh[kWavesPerBlock][kNB0];
+    __shared__ uint32_t lh[kWavesPerBlock][kNB0 / 2];
     __shared__ uint32_t woff[kWavesPerBlock][kWin + 1];
     __shared__ uint32_t wunit[kWavesPerBlock][kWin];
+    __shared__ uint32_t wsub[kWavesPerBlock][kWin];
     __shared__ uint32_t srcmap[kWavesPerBlock][kTile];
+    __shared__ uint32_t wseg[kWavesPerBlock];
     const int w = threadIdx.x >> 6, lane = lane_id();
     uint32_t* hw = lh[w];
     uint32_t* wo = woff[w];
     uint32_t* wu = wunit[w];
+    uint32_t* ws = wsub[w];
     uint32_t* sm = srcmap[w];
-    for (int i = lane; i < kNB0; i += kWave) hw[i] = 0;
+    for (int i = lane; i < kNB0 / 2; i += kWave) hw[i] = 0;
     wave_lds_sync();
     const uint32_t ntiles = a.tile_base[a.T];
-    for (uint32_t tile = blockIdx.x * kWavesPerBlock + w; tile < ntiles; tile += gridDim.x * kWavesPerBlock) {
+    for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += gridDim.x * kWavesPerBlock) {
+        const uint32_t tile = t0 + w;
+        if (tile >= ntiles) {
+            if (lane == 0) wseg[w] = kNoKey;
+            block_flush<kNB0>(a, lh, wseg, kHistH0);
+            continue;
+        }
         TileView v;
         tile_setup(a, tile, v);
         uint32_t ix[kRows], vb[kRows];
@@ -97,25 +137,32 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
             // compact position p <-> dense-pass offset p + shift
             const uint32_t shift = a.raw_tbase[v.t] - a.ten_cbase[v.t];
             const uint32_t j0 = a.tile_ne0[tile];
+            const uint32_t nne = a.num_ne[0];
             {
                 constexpr int NW = (kWin + kWave) / kWave;
-                uint32_t xo[NW], xu[NW];
+                uint32_t xo[NW], xu[NW], xs[NW];
 #pragma unroll
                 for (int i = 0; i < NW; ++i) {
                     const uint32_t j = i * kWave + lane;
-                    xo[i] = (j <= kWin && j0 + j <= a.num_ne[0]) ? a.ne_off[j0 + j] : kNoKey;
-                    xu[i] = (j < kWin && j0 + j < a.num_ne[0]) ? a.ne_unit[j0 + j] : 0u;
+                    const bool in = j < kWin && j0 + j < nne;
+                    xo[i] = (j <= kWin && j0 + j <= nne) ? a.ne_off[j0 + j] : kNoKey;
+                    xu[i] = in ? a.ne_unit[j0 + j] : 0u;
+                    xs[i] = in ? a.ne_sub[j0 + j] : 0u;
                 }
 #pragma unroll
                 for (int i = 0; i < NW; ++i) {
                     const uint32_t j = i * kWave + lane;
                     if (j <= kWin) wo[j] = xo[i];
-                    if (j < kWin) wu[j] = xu[i];
+                    if (j < kWin) {
+                        wu[j] = xu[i];
+                        ws[j] = xs[i];
+                    }
                 }
                 wave_lds_sync();
             }
             // merge path: lane L maps the kRows consecutive candidates starting
-            // at kRows * L to slot indices (one search, then a forward walk)
+            // at kRows * L to slot indices (one search, then a forward walk);
+            // rank x inside a unit lies in quarter q = #{running counts <= x}
             const uint32_t q0 = kRows * lane, cnt = v.p1 - v.p0, r0 = v.p0 + shift;
             if (q0 < cnt) {
                 uint32_t lo = 0, hi = kWin;
@@ -125,7 +172,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
                     if (wo[mid] <= rp0) lo = mid;
                     else hi = mid;
                 }
-                uint32_t j = lo, cur = wo[j], nxt = wo[j + 1], ub = wu[j] * kUnitLen;
+                uint32_t j = lo, cur = wo[j], nxt = wo[j + 1], ub = wu[j] * kUnitLen, sub = ws[j];
                 for (int i = 0; i < kRows && q0 + i < cnt; ++i) {
                     const uint32_t rp = rp0 + i;
                     while (rp >= nxt) {
@@ -133,8 +180,13 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
                         cur = nxt;
                         nxt = wo[j + 1];
                         ub = wu[j] * kUnitLen;
+                        sub = ws[j];
                     }
-                    sm[q0 + i] = ub + (rp - cur);
+                    const uint32_t x = rp - cur;
+                    const uint32_t c1 = sub & 0x3FFu, c2 = (sub >> 10) & 0x3FFu, c3 = sub >> 20;
+                    const uint32_t q = (x >= c1) + (x >= c2) + (x >= c3);
+                    const uint32_t before = q == 0 ? 0u : q == 1 ? c1 : q == 2 ? c2 : c3;
+                    sm[q0 + i] = ub + q * kQuarter + (x - before);
                 }
             }
             wave_lds_sync();
@@ -146,7 +198,6 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
                 ix[r] = e.x;
                 vb[r] = e.y;
             }
-            wave_lds_sync();
         }
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
@@ -156,9 +207,10 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
                 a.cand_idx[pl] = ix[r];
                 a.cand_val[pl] = vb[r];
             }
-            lds_hist_add(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active);
+            lds_hist_add16(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active);
         }
-        flush_hist(hw, seg_hist(a, v.s, kHistH0), kNB0);
+        if (lane == 0) wseg[w] = v.s;
+        block_flush<kNB0>(a, lh, wseg, kHistH0);
     }
 }
 
@@ -183,12 +235,7 @@ struct Level<1> {
 template <>
 struct Level<2> {
     static constexpr int kPrevNB = kNB1, kPrevHist = kHistH1, kNB = kNB2, kHist = kHistH2;
-    static constexpr int kPrefixShift = kD1Shift, kDigitShift = kD2Shift, kPrevBits = 6;
-};
-template <>
-struct Level<3> {
-    static constexpr int kPrevNB = kNB2, kPrevHist = kHistH2, kNB = kNB3, kHist = kHistH3;
-    static constexpr int kPrefixShift = kD2Shift, kDigitShift = 0, kPrevBits = 10;
+    static constexpr int kPrefixShift = kD1Shift, kDigitShift = 0, kPrevBits = kD0Shift - kD1Shift;
 };
 
 template <int L>
@@ -196,12 +243,9 @@ __device__ __forceinline__ void read_level(const SegState& g, uint32_t k, uint32
     if (L == 1) {
         prefix = 0;
         rank = k;
-    } else if (L == 2) {
+    } else {
         prefix = g.d0;
         rank = g.r1;
-    } else {
-        prefix = g.p16;
-        rank = g.r2;
     }
 }
 
@@ -210,46 +254,50 @@ __device__ __forceinline__ void write_level(SegState& g, uint32_t prefix, uint32
     if (L == 1) {
         g.d0 = prefix;
         g.r1 = rank;
-    } else if (L == 2) {
-        g.p16 = prefix;
-        g.r2 = rank;
     } else {
-        g.p26 = prefix;
-        g.r3 = rank;
+        g.p20 = prefix;
+        g.r2 = rank;
     }
 }
 
 template <int L>
 __global__ __launch_bounds__(kBlock) void k_radix(CandArgs a) {
     using Lv = Level<L>;
-    __shared__ uint32_t lh[kWavesPerBlock][Lv::kNB];
+    __shared__ uint32_t lh[kWavesPerBlock][Lv::kNB / 2];
+    __shared__ uint32_t wseg[kWavesPerBlock];
     const int w = threadIdx.x >> 6, lane = lane_id();
     uint32_t* hw = lh[w];
-    for (int i = lane; i < Lv::kNB; i += kWave) hw[i] = 0;
+    for (int i = lane; i < Lv::kNB / 2; i += kWave) hw[i] = 0;
     wave_lds_sync();
     const uint32_t ntiles = a.tile_base[a.T];
     uint32_t cached_s = kNoKey, prefix = 0, rank = 0;
-    for (uint32_t tile = blockIdx.x * kWavesPerBlock + w; tile < ntiles; tile += gridDim.x * kWavesPerBlock) {
-        TileView v;
-        tile_setup(a, tile, v);
-        uint32_t key[kRows];
-        load_keys(a, v, key);
-        if (v.s != cached_s) {
-            uint32_t p0, r0, d, ab;
-            read_level<L>(a.seg[v.s], v.k, p0, r0);
-            wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
-            prefix = (p0 << Lv::kPrevBits) | d;
-            rank = r0 - ab;
-            cached_s = v.s;
-        }
-        if (tile == v.first_tile && lane == 0) write_level<L>(a.seg[v.s], prefix, rank);
+    for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += gridDim.x * kWavesPerBlock) {
+        const uint32_t tile = t0 + w;
+        if (tile < ntiles) {
+            TileView v;
+            tile_setup(a, tile, v);
+            uint32_t key[kRows];
+            load_keys(a, v, key);
+            if (v.s != cached_s) {
+                uint32_t p0, r0, d, ab;
+                read_level<L>(a.seg[v.s], v.k, p0, r0);
+                wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
+                prefix = (p0 << Lv::kPrevBits) | d;
+                rank = r0 - ab;
+                cached_s = v.s;
+            }
+            if (tile == v.first_tile && lane == 0) write_level<L>(a.seg[v.s], prefix, rank);
 #pragma unroll
-        for (int r = 0; r < kRows; ++r) {
-            const bool active = v.p0 + r * kWave + lane < v.p1;
-            lds_hist_add(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
-                         active && (key[r] >> Lv::kPrefixShift) == prefix);
+            for (int r = 0; r < kRows; ++r) {
+                const bool active = v.p0 + r * kWave + lane < v.p1;
+                lds_hist_add16(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
+                               active && (key[r] >> Lv::kPrefixShift) == prefix);
+            }
+            if (lane == 0) wseg[w] = v.s;
+        } else if (lane == 0) {
+            wseg[w] = kNoKey;
         }
-        flush_hist(hw, seg_hist(a, v.s, Lv::kHist), Lv::kNB);
+        block_flush<Lv::kNB>(a, lh, wseg, Lv::kHist);
     }
 }
 
@@ -263,11 +311,11 @@ __global__ __launch_bounds__(kBlock) void k_count(CandArgs a) {
         uint32_t key[kRows];
         load_keys(a, v, key);
         if (v.s != cached_s) {
-            const uint32_t p26 = a.seg[v.s].p26, r3 = a.seg[v.s].r3;
-            uint32_t d3, ab;
-            wave_pick<kNB3>(seg_hist(a, v.s, kHistH3), r3, d3, ab);
-            thr = (p26 << kD2Shift) | d3;
-            need = r3 - ab;
+            const uint32_t p20 = a.seg[v.s].p20, r2 = a.seg[v.s].r2;
+            uint32_t d2, ab;
+            wave_pick<kNB2>(seg_hist(a, v.s, kHistH2), r2, d2, ab);
+            thr = (p20 << kD1Shift) | d2;
+            need = r2 - ab;
             cached_s = v.s;
         }
         if (tile == v.first_tile && lane == 0) {
@@ -390,7 +438,6 @@ hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, u
     hipLaunchKernelGGL(k_gather, gt, b, 0, st, a);
     hipLaunchKernelGGL(k_radix<1>, gt, b, 0, st, a);
     hipLaunchKernelGGL(k_radix<2>, gt, b, 0, st, a);
-    hipLaunchKernelGGL(k_radix<3>, gt, b, 0, st, a);
     hipLaunchKernelGGL(k_count, gt, b, 0, st, a);
     if (quant) hipLaunchKernelGGL(k_emit<true>, gt, b, 0, st, a, o);
     else hipLaunchKernelGGL(k_emit<false>, gt, b, 0, st, a, o);

@@ -12,9 +12,12 @@
 //
 // A unit is the 1024 elements [1024u, 1024u + 1024) of the flat gradient,
 // one block of 256 threads with one 16-byte vector per thread, so every
-// load is aligned and issued before any table lookup.  A unit that holds a
-// tensor boundary also records, for each tensor starting inside it, how many
-// of its candidates precede that start (the candidate layout needs it).
+// load is aligned and issued before any table lookup.  Each wave compacts
+// the candidates of its quarter of the unit on its own, into slots
+// [1024u + 256w, ...), with no block barrier on the streaming path.  A unit
+// that holds a tensor boundary also records, for each tensor starting inside
+// it, how many of its candidates precede that start (the candidate layout
+// needs it).
 
 #include "gd_kernels.h"
 
@@ -44,7 +47,6 @@ __device__ __forceinline__ uint32_t tensor_of(const uint32_t* off, uint32_t T, u
 
 template <bool BASE>
 __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
-    __shared__ uint32_t wcnt[kWavesPerBlock];
     const uint32_t u = blockIdx.x;
     const int tid = threadIdx.x, w = tid >> 6, lane = lane_id();
     const uint32_t ustart = u * kUnitLen;
@@ -106,20 +108,12 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
         for (int q = 0; q < 4; ++q)
             if (e0 + q < uend) a.res[e0 + q] = ov[q];
     }
-    // ordered compaction over the block: waves in order, lanes in order,
-    // then the four elements of a lane
+    // ordered compaction over the wave's quarter: lanes in order, then the
+    // four elements of a lane
     const uint64_t m0 = ballot(cand[0]), m1 = ballot(cand[1]), m2 = ballot(cand[2]), m3 = ballot(cand[3]);
-    if (lane == 0) wcnt[w] = popc64(m0) + popc64(m1) + popc64(m2) + popc64(m3);
-    __syncthreads();
-    uint32_t base = 0, total = 0;
-#pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i) {
-        base += i < w ? wcnt[i] : 0u;
-        total += wcnt[i];
-    }
     if ((m0 | m1 | m2 | m3) != 0) {
-        uint32_t pos = base + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
-        uint2* out = a.slots + ustart;
+        uint32_t pos = lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
+        uint2* out = a.slots + ustart + w * kQuarter;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             if (cand[q]) {
@@ -128,7 +122,7 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
             }
         }
     }
-    if (tid == 0) a.cnt_lo[u] = total;
+    if (lane == 0) a.wcnt[4 * u + w] = popc64(m0) + popc64(m1) + popc64(m2) + popc64(m3);
     if (boundary) {
         // candidates before each tensor start strictly inside the unit
         __shared__ uint32_t red[kWavesPerBlock];

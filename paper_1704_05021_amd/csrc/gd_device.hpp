@@ -17,33 +17,46 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 // value and NaN above Inf).  Every key is below 2^31.
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;  // above every key: "nothing qualifies"
 
-// The 31 key bits are resolved in four radix digits, most significant first.
-// The second digit is narrow: the candidates that share the threshold's
-// first digit are many and spread out, and a narrow digit keeps their
-// histogram (and its global atomics) small.
+// The 31 key bits are resolved in three radix digits, most significant
+// first: 10, 10 and 11 bits.
 constexpr int kD0Shift = 21, kNB0 = 1024;  // key bits 30..21
-constexpr int kD1Shift = 15, kNB1 = 64;    // key bits 20..15
-constexpr int kD2Shift = 5, kNB2 = 1024;   // key bits 14..5
-constexpr int kNB3 = 32;                   // key bits  4..0
+constexpr int kD1Shift = 11, kNB1 = 1024;  // key bits 20..11
+constexpr int kNB2 = 2048;                 // key bits 10..0
 
 // Histogram words per threshold segment, one histogram per digit.
-constexpr int kHistH0 = 0, kHistH1 = kNB0, kHistH2 = kNB0 + kNB1, kHistH3 = kNB0 + kNB1 + kNB2;
-constexpr int kHistWords = kNB0 + kNB1 + kNB2 + kNB3;
+constexpr int kHistH0 = 0, kHistH1 = kNB0, kHistH2 = kNB0 + kNB1;
+constexpr int kHistWords = kNB0 + kNB1 + kNB2;
 
 // Sampling: units of 16 consecutive elements (one 64-byte line per array),
 // at most kMaxUnits units per segment.  A sample key is the top 16 bits of
 // the 31-bit key (relative resolution 2^-8), kNoKey16 marks a missing one.
 constexpr int kUnit = 16;
-constexpr int kMaxUnits = 1024;
+constexpr int kMaxUnits = 4096;
+constexpr int kMinSpreadUnits = 1024;
 constexpr int kSampleThreads = 128;    // gather blocks: one unit per thread
-constexpr int kBracketThreads = 1024;  // one block per segment: one unit per thread
+constexpr int kBracketThreads = 1024;  // one block per segment
+constexpr int kBracketUnits = kMaxUnits / kBracketThreads;  // units held per thread
 constexpr int kSampleBlocks = kMaxUnits / kSampleThreads;
+
+// Sample units of a segment with n16 16-element blocks: all of them when
+// there are at most kMaxUnits, else about one unit per 64 blocks (one
+// 16-byte group per 256 elements and input array), clamped to
+// [kMinSpreadUnits, kMaxUnits].
+__host__ __device__ constexpr uint32_t sample_unit_count(uint32_t n16) {
+    return n16 <= (uint32_t)kMaxUnits ? n16
+           : n16 / 64 < (uint32_t)kMinSpreadUnits ? (uint32_t)kMinSpreadUnits
+           : n16 / 64 > (uint32_t)kMaxUnits ? (uint32_t)kMaxUnits
+           : n16 / 64;
+}
 constexpr uint32_t kNoKey16 = 0xFFFFu;
 constexpr int kK16Shift = 15;           // key16 = key >> 15
-constexpr int kS0Shift = 6, kSNB1 = 64;  // key16 digits: bits 15..6 (= key digit 0), bits 5..0
+constexpr int kS0Shift = 6, kSNB1 = 64;
+constexpr int kSHistWords = 1024 + 2;  // per segment: digit histogram of the sample, valid and zero counts  // key16 digits: bits 15..6 (= key digit 0), bits 5..0
 
-// Elements per unit of the dense pass (one wave).
+// Elements per unit of the dense pass (one block), and per quarter (one
+// wave, which compacts its candidates on its own).
 constexpr uint32_t kUnitLen = 1024;
+constexpr uint32_t kQuarter = kUnitLen / 4;
 // Units per block of the candidate-count scan.
 constexpr uint32_t kScanUnits = 1024;
 constexpr int kScanThreads = 256;
@@ -56,13 +69,11 @@ struct SegState {
     uint32_t miss;  // 1 when fewer than k candidates: every element becomes one
     uint32_t d0;    // digit 0 of the threshold key (key >> 21)
     uint32_t r1;    // rank of the threshold among candidates with that digit 0
-    uint32_t p16;   // key >> 15 of the threshold key
+    uint32_t p20;   // key >> 11 of the threshold key
     uint32_t r2;    // rank among candidates with that prefix
-    uint32_t p26;   // key >> 5 of the threshold key
-    uint32_t r3;    // rank among candidates with that prefix
     uint32_t thr;   // the threshold key T (kNoKey when nothing is kept)
     uint32_t need;  // entries with key == T to keep, lowest index first
-    uint32_t pad[4];
+    uint32_t pad[6];
 };
 
 __device__ __forceinline__ uint32_t key_of(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }
@@ -158,6 +169,12 @@ __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uin
 // them first with cross-lane operations).
 __device__ __forceinline__ void lds_hist_add(uint32_t* h, uint32_t bin, bool active) {
     if (active) atomicAdd(&h[bin], 1u);
+}
+
+// The same for a histogram of 16-bit counters, two bins per word (bin 2i in
+// the low half of word i); each count must stay below 2^16.
+__device__ __forceinline__ void lds_hist_add16(uint32_t* h, uint32_t bin, bool active) {
+    if (active) atomicAdd(&h[bin >> 1], 1u << ((bin & 1u) << 4));
 }
 
 // Exclusive prefix over a block of NT threads; *total receives the block sum.

@@ -12,6 +12,7 @@ namespace gd {
 constexpr uint32_t kDebugLoTooHigh = 1;  // no candidates: every segment takes the fallback
 constexpr uint32_t kDebugHiAtLo = 2;     // zero every candidate in the dense pass
 constexpr uint32_t kDebugLoZero = 3;     // every element is a candidate
+constexpr uint32_t kDebugLoAtHi = 4;     // candidates only above the estimate, all zeroed: most segments miss
 
 struct SampleArgs {
     const float* grad;
@@ -24,6 +25,7 @@ struct SampleArgs {
     uint32_t keep_ppm;
     uint32_t debug_bracket;  // 0, or a kDebug* override of the sampled bracket
     uint16_t* skeys;
+    uint32_t* shist;  // [S * kSHistWords], zero on entry; k_bracket clears it again
     SegState* seg;
     uint32_t* hist;
     uint64_t* out_base;
@@ -41,8 +43,8 @@ struct DenseArgs {
     uint32_t T;
     uint32_t per_tensor;
     const SegState* seg;
-    uint2* slots;
-    uint32_t* cnt_lo;
+    uint2* slots;                // [C * 1024] candidates of unit u, quarter w at [1024u + 256w, ...)
+    uint32_t* wcnt;              // [4C] candidates of each quarter
     uint32_t* split;             // [T] candidates of a tensor's first unit that precede the tensor
 };
 
@@ -61,8 +63,8 @@ struct CandArgs {
     uint32_t keep_ppm;
     SegState* seg;
     uint32_t* hist;
-    uint2* slots;
-    uint32_t* cnt_lo;
+    const uint2* slots;
+    const uint32_t* wcnt;   // [4C]
     const uint32_t* split;  // [T]
     uint32_t* loc;        // [C] candidate offset of each unit inside its scan block
     uint32_t* neloc;      // [C] index of each non-empty unit inside its scan block
@@ -72,6 +74,7 @@ struct CandArgs {
     uint32_t* beoff;      // [scan blocks] first non-empty unit of each scan block
     uint32_t* ne_unit;    // [C] the non-empty units, in order
     uint32_t* ne_off;     // [C + 1] their first candidate (dense-pass order); [count] = total
+    uint32_t* ne_sub;     // [C] their quarter counts, running: c0 | (c0+c1) << 10 | (c0+c1+c2) << 20
     uint32_t* num_ne;     // [1] number of non-empty units
     uint32_t* raw_tbase;  // [T + 1] first candidate of each tensor (dense-pass order)
     uint32_t* cand_idx;   // [N] compact candidates, ascending flat index

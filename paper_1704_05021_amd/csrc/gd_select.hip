@@ -9,13 +9,26 @@
 // paper itself approximates the threshold by selecting on a 0.1% sample,
 // Section 4; here the sample only bounds an exact selection.)
 //
-//   k_sample  : many small blocks gather sample units (16 neighbours, one
-//               64-byte line per input array) and store 16-bit key prefixes;
-//               they also clear the per-call histograms and counters.
-//   k_bracket : one block per segment holds its sample keys in registers and
-//               picks lo and hi from sample ranks around the expected rank of
-//               the threshold, widened by the measured spread of per-unit
-//               counts (neighbouring elements can be strongly correlated).
+//   k_sample  : many small blocks gather sample units and store 16-bit key
+//               prefixes, with the digit histogram of each segment's sample
+//               (nonzero keys) and its valid and zero counts; they also clear
+//               the per-call histograms and counters.  A unit is 16 elements
+//               of one stratum: 16 neighbours when the whole segment is
+//               sampled, else four aligned groups of 4 neighbours spread over
+//               the stratum (one 16-byte load per group and input array).
+//               Neighbours are strongly correlated in sparse embedding
+//               gradients (a nonzero row), so spread groups carry far more
+//               information per sample than one run of 16.
+//   k_bracket : one block per segment holds its sample keys in registers,
+//               estimates the threshold's 16-bit key prefix P from the
+//               sample rank k * m / n, and measures the spread of the
+//               per-unit counts of keys >= P (neighbouring elements can be
+//               strongly correlated, so the spread is not assumed binomial).
+//               hi is just above P: the dense pass zeroes the residual of
+//               keys >= hi, and every key between hi and the exact threshold
+//               costs one fix-up write later, so hi is a point estimate.  lo
+//               lies 5 standard deviations (plus a constant) of that count
+//               below the estimate, so that fewer than k candidates is rare.
 
 #include "gd_kernels.h"
 
@@ -36,11 +49,11 @@ __device__ __forceinline__ uint32_t key16_of(uint32_t key) {
     return k < kNoKey16 ? k : kNoKey16 - 1;  // the top NaN keys share one value
 }
 
-// Units sampled from segment [seg_a, seg_b): 16-aligned blocks of 16
-// elements, at most kMaxUnits of them.
+// Units sampled from segment [seg_a, seg_b): n16 is the number of
+// 16-aligned blocks of 16 elements the segment touches.
 __device__ __forceinline__ void sample_units(uint32_t seg_a, uint32_t seg_b, uint32_t& n16, uint32_t& U) {
     n16 = seg_b > seg_a ? ((seg_b - 1) >> 4) - (seg_a >> 4) + 1 : 0u;
-    U = n16 < (uint32_t)kMaxUnits ? n16 : (uint32_t)kMaxUnits;
+    U = sample_unit_count(n16);
 }
 
 template <bool BASE>
@@ -75,193 +88,225 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
     uint32_t n16, U;
     sample_units(seg_a, seg_b, n16, U);
     const uint32_t j = blockIdx.x * kSampleThreads + tid;
-    if (j >= U) return;
-    // stratum j of the segment's 16-element blocks, one block chosen by a fixed hash
-    const uint32_t lo_j = (uint32_t)(((uint64_t)j * n16) / U);
-    const uint32_t hi_j = (uint32_t)(((uint64_t)(j + 1) * n16) / U);
-    uint32_t pick = 0;
-    if (U != n16) pick = mix32(j * 0x9E3779B9u ^ (s + 1u) * 0x85EBCA6Bu) % (hi_j - lo_j);
-    const uint32_t e0 = ((seg_a >> 4) + lo_j + pick) * kUnit;
+    if (blockIdx.x * kSampleThreads >= U) return;  // whole block idle (block-uniform)
+    __shared__ uint32_t hs[kNB0];
+    __shared__ uint32_t cnt[2];
+    for (int i = tid; i < kNB0; i += kSampleThreads) hs[i] = 0;
+    if (tid < 2) cnt[tid] = 0;
+    __syncthreads();
     uint32_t k16[kUnit];
-    if (e0 >= seg_a && e0 + kUnit <= seg_b) {
-        const f4* g4 = reinterpret_cast<const f4*>(a.grad + e0);
-        const f4* r4 = reinterpret_cast<const f4*>(a.res + e0);
-        const f4* b4 = reinterpret_cast<const f4*>(BASE ? a.base + e0 : a.grad + e0);
-        f4 g[4], r[4], b[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            g[q] = g4[q];
-            r[q] = r4[q];
-            b[q] = BASE ? b4[q] : g[q];
+    for (int q = 0; q < kUnit; ++q) k16[q] = kNoKey16;
+    if (j < U) {
+        // stratum j: 16-element blocks [lo_j, hi_j) of the segment's aligned grid
+        const uint32_t lo_j = (uint32_t)(((uint64_t)j * n16) / U);
+        const uint32_t hi_j = (uint32_t)(((uint64_t)(j + 1) * n16) / U);
+        const uint32_t s0 = ((seg_a >> 4) + lo_j) * kUnit;
+        if (U == n16) {
+            // every block sampled: its 16 neighbours
+            if (s0 >= seg_a && s0 + kUnit <= seg_b) {
+                const f4* g4 = reinterpret_cast<const f4*>(a.grad + s0);
+                const f4* r4 = reinterpret_cast<const f4*>(a.res + s0);
+                const f4* b4 = reinterpret_cast<const f4*>(BASE ? a.base + s0 : a.grad + s0);
+                f4 g[4], r[4], b[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    g[q] = g4[q];
+                    r[q] = r4[q];
+                    b[q] = BASE ? b4[q] : g[q];
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        k16[4 * q + c] = key16_of(key_of(acc_of<BASE>(g[q][c], b[q][c], r[q][c])));
+            } else {
+#pragma unroll
+                for (int q = 0; q < kUnit; ++q) {
+                    const uint32_t e = s0 + q;
+                    if (e >= seg_a && e < seg_b)
+                        k16[q] = key16_of(key_of(acc_of<BASE>(a.grad[e], BASE ? a.base[e] : 0.0f, a.res[e])));
+                }
+            }
+        } else {
+            // one aligned group of 4 from each quarter of the stratum, by a fixed hash
+            const uint32_t len = (hi_j - lo_j) * kUnit, sub = len / 4;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t h = mix32((j * 4u + q) * 0x9E3779B9u ^ (s + 1u) * 0x85EBCA6Bu);
+                const uint32_t e = s0 + q * sub + (h % (sub / 4)) * 4;
+                if (e >= seg_a && e + 4 <= seg_b) {
+                    const f4 g = *reinterpret_cast<const f4*>(a.grad + e);
+                    const f4 r = *reinterpret_cast<const f4*>(a.res + e);
+                    const f4 b = BASE ? *reinterpret_cast<const f4*>(a.base + e) : g;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) k16[4 * q + c] = key16_of(key_of(acc_of<BASE>(g[c], b[c], r[c])));
+                } else {
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const uint32_t x = e + c;
+                        if (x >= seg_a && x < seg_b)
+                            k16[4 * q + c] =
+                                key16_of(key_of(acc_of<BASE>(a.grad[x], BASE ? a.base[x] : 0.0f, a.res[x])));
+                    }
+                }
+            }
         }
+        uint4* dst = reinterpret_cast<uint4*>(a.skeys + a.skey_base[s] + (size_t)kUnit * j);
+        dst[0] = make_uint4(k16[0] | (k16[1] << 16), k16[2] | (k16[3] << 16), k16[4] | (k16[5] << 16),
+                            k16[6] | (k16[7] << 16));
+        dst[1] = make_uint4(k16[8] | (k16[9] << 16), k16[10] | (k16[11] << 16), k16[12] | (k16[13] << 16),
+                            k16[14] | (k16[15] << 16));
+    }
+    // digit histogram of the nonzero keys; valid and zero counts
+    uint32_t nvalid = 0, nzero = 0;
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-            for (int c = 0; c < 4; ++c) k16[4 * q + c] = key16_of(key_of(acc_of<BASE>(g[q][c], b[q][c], r[q][c])));
-    } else {
-#pragma unroll
-        for (int q = 0; q < kUnit; ++q) {
-            const uint32_t e = e0 + q;
-            k16[q] = kNoKey16;
-            if (e >= seg_a && e < seg_b)
-                k16[q] = key16_of(key_of(acc_of<BASE>(a.grad[e], BASE ? a.base[e] : 0.0f, a.res[e])));
+    for (int q = 0; q < kUnit; ++q) {
+        const bool valid = k16[q] != kNoKey16;
+        lds_hist_add(hs, valid ? k16[q] >> kS0Shift : 0u, valid && k16[q] != 0);
+        nvalid += valid;
+        nzero += valid && k16[q] == 0;
+    }
+    nvalid = wave_sum(nvalid);
+    nzero = wave_sum(nzero);
+    if (lane_id() == 0) {
+        atomicAdd(&cnt[0], nvalid);
+        atomicAdd(&cnt[1], nzero);
+    }
+    __syncthreads();
+    uint32_t* sh = a.shist + (size_t)s * kSHistWords;
+    for (int i = tid; i < kNB0; i += kSampleThreads)
+        if (hs[i]) atomicAdd(&sh[i], hs[i]);
+    if (tid < 2 && cnt[tid]) atomicAdd(&sh[kNB0 + tid], cnt[tid]);
+}
+
+// 16-bit prefix of the r-th largest nonzero sample key (r >= 1, at most the
+// number of nonzero keys), from the digit histogram hA: a digit pick, then a
+// histogram of the low 6 bits among keys with that digit.  Called by the
+// whole block; hB is cleared here.
+__device__ uint32_t pick16(const uint32_t* hA, uint32_t* hB, uint32_t* par, uint32_t r,
+                           const uint32_t (&kw)[kBracketUnits][kUnit / 2]) {
+    const int tid = threadIdx.x;
+    if (tid < kSNB1) hB[tid] = 0;
+    if (tid < kWave) {
+        uint32_t d, ab;
+        wave_pick<kNB0>(hA, r, d, ab);
+        if (tid == 0) {
+            par[0] = d;
+            par[1] = r - ab;
         }
     }
-    uint4* dst = reinterpret_cast<uint4*>(a.skeys + a.skey_base[s] + (size_t)kUnit * j);
-    dst[0] = make_uint4(k16[0] | (k16[1] << 16), k16[2] | (k16[3] << 16), k16[4] | (k16[5] << 16),
-                        k16[6] | (k16[7] << 16));
-    dst[1] = make_uint4(k16[8] | (k16[9] << 16), k16[10] | (k16[11] << 16), k16[12] | (k16[13] << 16),
-                        k16[14] | (k16[15] << 16));
+    __syncthreads();
+    const uint32_t dq = par[0];
+#pragma unroll
+    for (int j = 0; j < kBracketUnits; ++j)
+#pragma unroll
+        for (int i = 0; i < kUnit; ++i) {
+            const uint32_t key = (kw[j][i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
+            lds_hist_add(hB, key & (kSNB1 - 1), key != kNoKey16 && key != 0 && (key >> kS0Shift) == dq);
+        }
+    __syncthreads();
+    if (tid < kWave) {
+        uint32_t d, ab;
+        wave_pick<kSNB1>(hB, par[1], d, ab);
+        if (tid == 0) par[2] = (dq << kS0Shift) | d;
+    }
+    __syncthreads();
+    const uint32_t p = par[2];
+    __syncthreads();
+    return p;
 }
 
 __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
     const uint32_t s = blockIdx.x;
-    const int tid = threadIdx.x, w = tid >> 6;
+    const int tid = threadIdx.x;
     const uint32_t seg_a = a.seg_off[s], seg_b = a.seg_off[s + 1];
     const uint32_t n = seg_b - seg_a;
     const uint32_t k = keep_of(n, a.keep_ppm);
     __shared__ uint32_t hA[kNB0];
-    __shared__ uint32_t hB[2][kSNB1];
-    __shared__ uint32_t par[12];
+    __shared__ uint32_t hB[kSNB1];
+    __shared__ uint32_t par[4];
+    __shared__ uint32_t sums[4];
     uint32_t n16, U;
     sample_units(seg_a, seg_b, n16, U);
+    // the sample's digit histogram and counts, cleared for the next call
+    {
+        uint32_t* sh = a.shist + (size_t)s * kSHistWords;
+        for (int i = tid; i < kNB0; i += kBracketThreads) hA[i] = sh[i];
+        if (tid < 2) sums[tid] = sh[kNB0 + tid];
+        if (tid >= 2 && tid < 4) sums[tid] = 0;
+        __syncthreads();
+        for (int i = tid; i < kSHistWords; i += kBracketThreads) sh[i] = 0;
+    }
     uint32_t lo, hi;
     if (k == 0) {
         lo = hi = kNoKey;
     } else if (k >= n) {
         lo = hi = 0;
     } else {
-        // thread u holds the 16 keys of sample unit u
-        uint32_t kv[kUnit];
-        if ((uint32_t)tid < U) {
-            const uint4* src = reinterpret_cast<const uint4*>(a.skeys + a.skey_base[s] + (size_t)kUnit * tid);
-            const uint4 x0 = src[0], x1 = src[1];
-            const uint32_t wv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        // thread tid holds sample units tid + j * kBracketThreads, 16 keys each
+        uint32_t kw[kBracketUnits][kUnit / 2];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                kv[2 * i] = wv[i] & 0xFFFFu;
-                kv[2 * i + 1] = wv[i] >> 16;
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < kUnit; ++i) kv[i] = kNoKey16;
-        }
-        for (int i = tid; i < kNB0; i += kBracketThreads) hA[i] = 0;
-        if (tid < 2 * kSNB1) (&hB[0][0])[tid] = 0;
-        if (tid < 12) par[tid] = 0;
-        __syncthreads();
-        // Pass 1: digit-0 histogram of the nonzero sample keys; zero keys
-        // (most of a sparse embedding gradient) are only counted.
-        uint32_t nvalid = 0, nzero = 0;
-#pragma unroll
-        for (int i = 0; i < kUnit; ++i) {
-            const uint32_t key = kv[i];
-            const bool valid = key != kNoKey16;
-            lds_hist_add(hA, valid ? key >> kS0Shift : 0u, valid && key != 0);
-            nvalid += valid;
-            nzero += valid && key == 0;
-        }
-        nvalid = wave_sum(nvalid);
-        nzero = wave_sum(nzero);
-        if (lane_id() == 0) {
-            atomicAdd(&par[0], nvalid);
-            atomicAdd(&par[1], nzero);
-        }
-        __syncthreads();
-        const uint32_t m = par[0], mnz = par[0] - par[1];
-        const bool full = m >= n;  // every element sampled: exact ranks
-        const double q = (double)k * (double)m / (double)n;
-        if (!full && w == 0) {
-            // digit-0 bin of the estimated threshold (rank q in the sample)
-            const uint32_t rq = (uint32_t)fmax(1.0, floor(q + 0.5));
-            uint32_t d = 0, ab;
-            if (rq > mnz || !wave_pick<kNB0>(hA, rq, d, ab)) d = 0;
-            if (lane_id() == 0) par[2] = d;
-        }
-        __syncthreads();
-        if (!full) {
-            // Pass 2: spread of the per-unit counts at that bin.  Units are
-            // runs of 16 neighbours, which can be strongly correlated (a
-            // nonzero embedding row), so the rank uncertainty of the sample is
-            // measured rather than assumed binomial.
-            const uint32_t dq = par[2];
-            uint32_t c = 0;
-#pragma unroll
-            for (int i = 0; i < kUnit; ++i) c += (kv[i] != kNoKey16 && kv[i] != 0 && (kv[i] >> kS0Shift) >= dq);
-            uint32_t s1 = wave_sum(c), s2 = wave_sum(c * c);
-            if (lane_id() == 0) {
-                atomicAdd(&par[3], s1);
-                atomicAdd(&par[4], s2);
-            }
-        }
-        __syncthreads();
-        if (tid == 0) {
-            uint32_t r_hi, r_lo;
-            if (full) {
-                r_hi = r_lo = k;
+        for (int j = 0; j < kBracketUnits; ++j) {
+            const uint32_t u = tid + j * kBracketThreads;
+            if (u < U) {
+                const uint4* src = reinterpret_cast<const uint4*>(a.skeys + a.skey_base[s] + (size_t)kUnit * u);
+                const uint4 x0 = src[0], x1 = src[1];
+                kw[j][0] = x0.x;
+                kw[j][1] = x0.y;
+                kw[j][2] = x0.z;
+                kw[j][3] = x0.w;
+                kw[j][4] = x1.x;
+                kw[j][5] = x1.y;
+                kw[j][6] = x1.z;
+                kw[j][7] = x1.w;
             } else {
-                const double mean = (double)par[3] / U, var = (double)par[4] / U - mean * mean;
-                const double sd = sqrt(fmax(q, U * fmax(var, 0.0)));
-                const double fh = floor(q - 3.0 * sd - 2.0);
-                const double fl = ceil(q + 5.0 * sd + 4.0);
-                r_hi = fh < 1.0 ? 0u : (uint32_t)fh;
-                r_lo = fl > (double)m ? kNoKey : (uint32_t)fl;
-            }
-            // ranks that fall among the zero keys
-            if (r_hi > mnz) r_hi = 0;
-            if (r_lo != kNoKey && r_lo > mnz) r_lo = kNoKey;
-            par[5] = r_hi;
-            par[6] = r_lo;
-        }
-        __syncthreads();
-        const uint32_t r_hi = par[5], r_lo = par[6];
-        if (w == 0 && r_hi) {
-            uint32_t d, ab;
-            wave_pick<kNB0>(hA, r_hi, d, ab);
-            if (lane_id() == 0) {
-                par[7] = d;
-                par[8] = r_hi - ab;
-            }
-        }
-        if (w == 1 && r_lo != kNoKey) {
-            uint32_t d, ab;
-            wave_pick<kNB0>(hA, r_lo, d, ab);
-            if (lane_id() == 0) {
-                par[9] = d;
-                par[10] = r_lo - ab;
-            }
-        }
-        __syncthreads();
-        const uint32_t dh = r_hi ? par[7] : kNoKey, dl = r_lo != kNoKey ? par[9] : kNoKey;
 #pragma unroll
-        for (int i = 0; i < kUnit; ++i) {
-            const uint32_t key = kv[i];
-            const bool nz = key != kNoKey16 && key != 0;
-            const uint32_t d0 = key >> kS0Shift, d1 = key & (kSNB1 - 1);
-            lds_hist_add(hB[0], d1, nz && d0 == dh);
-            lds_hist_add(hB[1], d1, nz && d0 == dl);
+                for (int i = 0; i < kUnit / 2; ++i) kw[j][i] = 0xFFFFFFFFu;
+            }
         }
-        __syncthreads();
-        if (w == 0 && r_hi) {
-            uint32_t d, ab;
-            wave_pick<kSNB1>(hB[0], par[8], d, ab);
-            if (lane_id() == 0) par[8] = d;
-        }
-        if (w == 1 && r_lo != kNoKey) {
-            uint32_t d, ab;
-            wave_pick<kSNB1>(hB[1], par[10], d, ab);
-            if (lane_id() == 0) par[10] = d;
-        }
-        __syncthreads();
-        hi = r_hi ? ((((dh << kS0Shift) | par[8]) + 1u) << kK16Shift) : kNoKey;
-        if (r_lo != kNoKey) {
-            lo = ((dl << kS0Shift) | par[10]) << kK16Shift;
-            if (lo == 0) lo = 1;
-        } else {
-            // The rank falls among zero keys: candidates are the nonzero
-            // entries, unless every element was sampled and zeros are known
-            // to be needed.
+        const uint32_t m = sums[0], mnz = sums[0] - sums[1];
+        const bool full = m >= n;  // every element sampled: exact ranks
+        const double q = full ? (double)k : (double)k * (double)m / (double)n;
+        const uint32_t rq = (uint32_t)fmax(1.0, floor(q + 0.5));
+        if (rq > mnz) {
+            // the estimate falls among zero keys: candidates are the nonzero
+            // entries (or, when every element was sampled and zeros are
+            // known to be needed, all of them); nothing is zeroed early
+            hi = kNoKey;
             lo = (full && k > mnz) ? 0u : 1u;
+        } else {
+            const uint32_t P = pick16(hA, hB, par, rq, kw);
+            hi = (P + 1u) << kK16Shift;
+            if (full) {
+                lo = P << kK16Shift;
+            } else {
+                // Pass 2: spread of the per-unit counts of keys >= P
+#pragma unroll
+                for (int j = 0; j < kBracketUnits; ++j) {
+                    uint32_t c = 0;
+#pragma unroll
+                    for (int i = 0; i < kUnit; ++i) {
+                        const uint32_t key = (kw[j][i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
+                        c += key != kNoKey16 && key >= P;
+                    }
+                    const uint32_t s1 = wave_sum(c), s2 = wave_sum(c * c);
+                    if (lane_id() == 0) {
+                        atomicAdd(&sums[2], s1);
+                        atomicAdd(&sums[3], s2);
+                    }
+                }
+                __syncthreads();
+                const double mean = (double)sums[2] / U, var = (double)sums[3] / U - mean * mean;
+                const double sd = sqrt(fmax(q, U * fmax(var, 0.0)));
+                const double fl = ceil(q + 5.0 * sd + 4.0);
+                if (fl > (double)mnz) {
+                    lo = 1u;  // the margin reaches the zero keys
+                } else {
+                    lo = pick16(hA, hB, par, (uint32_t)fl, kw) << kK16Shift;
+                    if (lo == 0) lo = 1;
+                }
+            }
         }
     }
     if (a.debug_bracket == kDebugLoTooHigh && k > 0) {
@@ -271,6 +316,8 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
         hi = lo;
     } else if (a.debug_bracket == kDebugLoZero && k > 0) {
         lo = 0;
+    } else if (a.debug_bracket == kDebugLoAtHi && k > 0 && k < n) {
+        lo = hi;
     }
     if (tid == 0) {
         a.seg[s].lo = lo;

@@ -211,7 +211,7 @@ class Compressor:
         if st != 0:
             raise GDError(st, "gd_debug_force_bracket")
 
-    SEG_FIELDS = ("lo", "hi", "clo", "miss", "d0", "r1", "p21", "r2", "thr", "need")
+    SEG_FIELDS = ("lo", "hi", "clo", "miss", "d0", "r1", "p20", "r2", "thr", "need")
 
     def debug_state(self):
         """(per-segment state of the last call as a list of dicts, decomposition info dict)."""
@@ -223,7 +223,7 @@ class Compressor:
         if st != 0:
             raise GDError(st, "gd_debug_state")
         segs = [dict(zip(self.SEG_FIELDS, (int(x) for x in row[:10]))) for row in words]
-        keys = ("chunk_len", "chunks", "tile", "max_tiles")
+        keys = ("unit_len", "units", "tile", "max_tiles")
         return segs, dict(zip(keys, (int(x) for x in info)))
 
     def profile_enable(self, on: bool = True) -> None:

@@ -56,7 +56,7 @@ def _tie_heavy(rng, n):
     return v.astype(np.float32)
 
 
-@pytest.mark.parametrize("debug", [0, 1, 2, 3], ids=["sampled", "fallback", "zero_all_cands", "all_cands"])
+@pytest.mark.parametrize("debug", [0, 1, 2, 3, 4], ids=["sampled", "fallback", "zero_all_cands", "all_cands", "lo_at_hi"])
 @pytest.mark.parametrize("seed", range(6))
 def test_random_layouts(seed, debug):
     rng = np.random.default_rng(100 + seed)
@@ -102,7 +102,7 @@ def test_unaligned_tensor_offsets():
     comp = gd.Compressor(offsets)
     for per in (False, True):
         for quant in (False, True):
-            for debug in (0, 1, 2, 3):
+            for debug in (0, 1, 2, 3, 4):
                 check_case(g, r, offsets, 0.9, per, quant, comp=comp, debug_bracket=debug, what=f"per={per} q={quant}")
 
 
@@ -148,6 +148,7 @@ def test_mnist_mlp_full():
 def test_small_workloads(name):
     _run_workload(name)
     _run_workload(name, steps=2, debug=1)
+    _run_workload(name, steps=2, debug=4)
 
 
 @pytest.mark.parametrize("name,steps", [("mlp_784_4096_4096_10_t3", 3), ("nmt_85k_per_tensor", 2),
