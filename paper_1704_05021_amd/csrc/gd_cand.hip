@@ -3,27 +3,34 @@
 // Candidates (every element with key >= lo, or every element of a segment
 // whose bracket missed) are processed in tiles of kTile consecutive
 // candidates of one tensor, one wave per tile, so the work is balanced
-// however unevenly the candidates fall across the gradient.
+// however unevenly the candidates fall across the gradient.  Five phases:
 //
-//   k_gather     : compacts each tile's candidates from the per-quarter
-//                  slots (or, for a missed segment, straight from the
-//                  residual) into one array in ascending flat index, with
-//                  the digit-0 histogram.
-//   k_radix<L>   : digit L-1 of the k-th largest key from the previous
-//                  histogram; the histogram of digit L over the candidates
-//                  that share the prefix found so far (L = 1, 2).
-//   k_count      : the last digit, i.e. the exact threshold key T and the
-//                  number of candidates equal to T to keep (lowest index
-//                  first); per tile, the candidates above and equal to T.
-//   k_emit       : kept (index, value) pairs in ascending index order, the
-//                  residual of every candidate whose fate differs from what
-//                  the dense pass assumed, kept counts per tensor (and
-//                  per-tile sums for quantisation).
+//   gather   : compacts each tile's candidates from the per-quarter slots
+//              (or, for a missed segment, straight from the residual) into
+//              one array in ascending flat index, with the digit-0
+//              histogram.
+//   radix<L> : digit L-1 of the k-th largest key from the previous
+//              histogram; the histogram of digit L over the candidates that
+//              share the prefix found so far (L = 1, 2).
+//   count    : the last digit, i.e. the exact threshold key T and the number
+//              of candidates equal to T to keep (lowest index first); per
+//              tile, the candidates above and equal to T.
+//   emit     : kept (index, value) pairs in ascending index order, the
+//              residual of every candidate whose fate differs from what the
+//              dense pass assumed, kept counts per tensor (and per-tile sums
+//              for quantisation).
 //
 // Together they realise the exact-k rule: keep the k largest |acc| of each
 // segment, ties broken by lower flat index (Algorithm 1, Section 4).
 //
-// The histogram passes run in rounds of four consecutive tiles per block;
+// The phases run either as five kernels, or as one cooperative kernel
+// (k_select) whose co-resident blocks meet at grid barriers between phases.
+// A wave handles the same tiles in every phase, so the compact candidates it
+// wrote are its own; what crosses blocks inside k_select (histograms, digit
+// ranks, the threshold, per-tile counts) goes through agent-scope atomics,
+// which every XCD sees coherently without cache write-backs.
+//
+// The histogram phases run in rounds of four consecutive tiles per block;
 // each wave counts into its own LDS histogram and the block adds the four
 // to the segment histogram once per round (waves of one segment merged), so
 // the global atomics on the few hot bins are a quarter of one per tile.
@@ -56,22 +63,22 @@ __device__ __forceinline__ uint32_t* seg_hist(const CandArgs& a, uint32_t s, int
 
 // Adds the block's four per-wave histograms (16-bit counters, two bins per
 // word: a wave counts at most one tile of kTile candidates per round) to
-// their segments' histograms and clears them.  wseg[w] is wave w's segment
-// this round (kNoKey: no tile); waves of one segment are summed first.
-// Called by the whole block.
+// their segments' histograms and clears them.  lh holds the four histograms
+// of NB / 2 words each; wseg[w] is wave w's segment this round (kNoKey: no
+// tile); waves of one segment are summed first.  Called by the whole block.
 template <int NB>
-__device__ __forceinline__ void block_flush(const CandArgs& a, uint32_t (*lh)[NB / 2], const uint32_t* wseg,
-                                            int which) {
+__device__ __forceinline__ void block_flush(const CandArgs& a, uint32_t* lh, const uint32_t* wseg, int which) {
     static_assert(kWavesPerBlock * kTile < 65536, "16-bit histogram counters");
+    constexpr int W = NB / 2;
     __syncthreads();
     uint32_t sg[kWavesPerBlock];
-    for (int i = threadIdx.x; i < NB / 2; i += kBlock) {
+    for (int i = threadIdx.x; i < W; i += kBlock) {
         uint32_t h[kWavesPerBlock];
 #pragma unroll
         for (int w = 0; w < kWavesPerBlock; ++w) {
             sg[w] = wseg[w];
-            h[w] = lh[w][i];
-            lh[w][i] = 0;
+            h[w] = lh[w * W + i];
+            lh[w * W + i] = 0;
         }
 #pragma unroll
         for (int w = 0; w < kWavesPerBlock; ++w) {
@@ -98,19 +105,19 @@ constexpr uint32_t kWin = kTile;      // non-empty units held in the gather wind
 // A tile of kTile candidates lies in at most kTile consecutive non-empty
 // units, so a window of kTile non-empty units starting at the unit that
 // holds the tile's first candidate always covers the tile.
-__global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
-    __shared__ uint32_t lh[kWavesPerBlock][kNB0 / 2];
-    __shared__ uint32_t woff[kWavesPerBlock][kWin + 1];
-    __shared__ uint32_t wunit[kWavesPerBlock][kWin];
-    __shared__ uint32_t wsub[kWavesPerBlock][kWin];
-    __shared__ uint32_t srcmap[kWavesPerBlock][kTile];
-    __shared__ uint32_t wseg[kWavesPerBlock];
+// LDS words of the gather phase: four digit-0 histograms, then per wave the
+// window offsets, units and quarter counts and the tile's slot map.
+constexpr int kGatherLds = kWavesPerBlock * (kNB0 / 2 + (kWin + 1) + kWin + kWin + kTile) + kWavesPerBlock;
+
+__device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
     const int w = threadIdx.x >> 6, lane = lane_id();
-    uint32_t* hw = lh[w];
-    uint32_t* wo = woff[w];
-    uint32_t* wu = wunit[w];
-    uint32_t* ws = wsub[w];
-    uint32_t* sm = srcmap[w];
+    uint32_t* lh = lds;
+    uint32_t* hw = lh + w * (kNB0 / 2);
+    uint32_t* wo = lh + kWavesPerBlock * (kNB0 / 2) + w * (kWin + 1);
+    uint32_t* wu = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1) + w * kWin;
+    uint32_t* ws = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + kWin) + w * kWin;
+    uint32_t* sm = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + 2 * kWin) + w * kTile;
+    uint32_t* wseg = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + 2 * kWin + kTile);
     for (int i = lane; i < kNB0 / 2; i += kWave) hw[i] = 0;
     wave_lds_sync();
     const uint32_t ntiles = a.tile_base[a.T];
@@ -131,7 +138,8 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
             for (int r = 0; r < kRows; ++r) {
                 const uint32_t pl = v.p0 + r * kWave + lane;
                 ix[r] = e_base + pl;
-                vb[r] = pl < v.p1 ? __float_as_uint(a.res[e_base + pl]) : 0u;
+                const uint32_t x = __float_as_uint(a.res[e_base + (pl < v.p1 ? pl : v.p0)]);
+                vb[r] = pl < v.p1 ? x : 0u;
             }
         } else {
             // compact position p <-> dense-pass offset p + shift
@@ -145,9 +153,13 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
                 for (int i = 0; i < NW; ++i) {
                     const uint32_t j = i * kWave + lane;
                     const bool in = j < kWin && j0 + j < nne;
-                    xo[i] = (j <= kWin && j0 + j <= nne) ? a.ne_off[j0 + j] : kNoKey;
-                    xu[i] = in ? a.ne_unit[j0 + j] : 0u;
-                    xs[i] = in ? a.ne_sub[j0 + j] : 0u;
+                    // unconditional loads at clamped positions (j0 < nne here), so
+                    // that all of them are in flight together
+                    const uint32_t jo = j0 + j <= nne ? j0 + j : nne, ju = in ? j0 + j : j0;
+                    const uint32_t o = a.ne_off[jo], u = a.ne_unit[ju], sb = a.ne_sub[ju];
+                    xo[i] = (j <= kWin && j0 + j <= nne) ? o : kNoKey;
+                    xu[i] = in ? u : 0u;
+                    xs[i] = in ? sb : 0u;
                 }
 #pragma unroll
                 for (int i = 0; i < NW; ++i) {
@@ -194,7 +206,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
 #pragma unroll
             for (int r = 0; r < kRows; ++r) {
                 const uint32_t q = r * kWave + lane;
-                const uint2 e = q < cnt ? a.slots[sm[q]] : make_uint2(0u, 0u);
+                const uint2 e = a.slots[sm[q < cnt ? q : 0u]];  // cnt >= 1: sm[0] is a real slot
                 ix[r] = e.x;
                 vb[r] = e.y;
             }
@@ -219,7 +231,8 @@ __device__ __forceinline__ void load_keys(const CandArgs& a, const TileView& v, 
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
         const uint32_t pl = v.p0 + r * kWave + lane_id();
-        key[r] = pl < v.p1 ? (a.cand_val[pl] & 0x7FFFFFFFu) : 0u;
+        const uint32_t x = a.cand_val[pl < v.p1 ? pl : v.p0];  // unconditional: all rows in flight
+        key[r] = pl < v.p1 ? (x & 0x7FFFFFFFu) : 0u;
     }
 }
 
@@ -238,35 +251,40 @@ struct Level<2> {
     static constexpr int kPrefixShift = kD1Shift, kDigitShift = 0, kPrevBits = kD0Shift - kD1Shift;
 };
 
-template <int L>
+template <int L, bool CO>
 __device__ __forceinline__ void read_level(const SegState& g, uint32_t k, uint32_t& prefix, uint32_t& rank) {
     if (L == 1) {
         prefix = 0;
         rank = k;
     } else {
-        prefix = g.d0;
-        rank = g.r1;
+        prefix = ld_co<CO>(&g.d0);
+        rank = ld_co<CO>(&g.r1);
     }
 }
 
-template <int L>
+template <int L, bool CO>
 __device__ __forceinline__ void write_level(SegState& g, uint32_t prefix, uint32_t rank) {
     if (L == 1) {
-        g.d0 = prefix;
-        g.r1 = rank;
+        st_co<CO>(&g.d0, prefix);
+        st_co<CO>(&g.r1, rank);
     } else {
-        g.p20 = prefix;
-        g.r2 = rank;
+        st_co<CO>(&g.p20, prefix);
+        st_co<CO>(&g.r2, rank);
     }
 }
 
 template <int L>
-__global__ __launch_bounds__(kBlock) void k_radix(CandArgs a) {
+constexpr int radix_lds() {
+    return kWavesPerBlock * (Level<L>::kNB / 2) + kWavesPerBlock;
+}
+
+template <int L, bool CO>
+__device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
     using Lv = Level<L>;
-    __shared__ uint32_t lh[kWavesPerBlock][Lv::kNB / 2];
-    __shared__ uint32_t wseg[kWavesPerBlock];
     const int w = threadIdx.x >> 6, lane = lane_id();
-    uint32_t* hw = lh[w];
+    uint32_t* lh = lds;
+    uint32_t* hw = lh + w * (Lv::kNB / 2);
+    uint32_t* wseg = lh + kWavesPerBlock * (Lv::kNB / 2);
     for (int i = lane; i < Lv::kNB / 2; i += kWave) hw[i] = 0;
     wave_lds_sync();
     const uint32_t ntiles = a.tile_base[a.T];
@@ -280,13 +298,13 @@ __global__ __launch_bounds__(kBlock) void k_radix(CandArgs a) {
             load_keys(a, v, key);
             if (v.s != cached_s) {
                 uint32_t p0, r0, d, ab;
-                read_level<L>(a.seg[v.s], v.k, p0, r0);
-                wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
+                read_level<L, CO>(a.seg[v.s], v.k, p0, r0);
+                wave_pick<Lv::kPrevNB, CO>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
                 prefix = (p0 << Lv::kPrevBits) | d;
                 rank = r0 - ab;
                 cached_s = v.s;
             }
-            if (tile == v.first_tile && lane == 0) write_level<L>(a.seg[v.s], prefix, rank);
+            if (tile == v.first_tile && lane == 0) write_level<L, CO>(a.seg[v.s], prefix, rank);
 #pragma unroll
             for (int r = 0; r < kRows; ++r) {
                 const bool active = v.p0 + r * kWave + lane < v.p1;
@@ -301,7 +319,8 @@ __global__ __launch_bounds__(kBlock) void k_radix(CandArgs a) {
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_count(CandArgs a) {
+template <bool CO>
+__device__ __forceinline__ void phase_count(const CandArgs& a) {
     const int w = threadIdx.x >> 6, lane = lane_id();
     const uint32_t ntiles = a.tile_base[a.T];
     uint32_t cached_s = kNoKey, thr = kNoKey, need = 0;
@@ -311,16 +330,16 @@ __global__ __launch_bounds__(kBlock) void k_count(CandArgs a) {
         uint32_t key[kRows];
         load_keys(a, v, key);
         if (v.s != cached_s) {
-            const uint32_t p20 = a.seg[v.s].p20, r2 = a.seg[v.s].r2;
+            const uint32_t p20 = ld_co<CO>(&a.seg[v.s].p20), r2 = ld_co<CO>(&a.seg[v.s].r2);
             uint32_t d2, ab;
-            wave_pick<kNB2>(seg_hist(a, v.s, kHistH2), r2, d2, ab);
+            wave_pick<kNB2, CO>(seg_hist(a, v.s, kHistH2), r2, d2, ab);
             thr = (p20 << kD1Shift) | d2;
             need = r2 - ab;
             cached_s = v.s;
         }
         if (tile == v.first_tile && lane == 0) {
-            a.seg[v.s].thr = thr;
-            a.seg[v.s].need = need;
+            st_co<CO>(&a.seg[v.s].thr, thr);
+            st_co<CO>(&a.seg[v.s].need, need);
         }
         uint32_t gt = 0, eq = 0;
 #pragma unroll
@@ -332,14 +351,14 @@ __global__ __launch_bounds__(kBlock) void k_count(CandArgs a) {
         gt = wave_sum(gt);
         eq = wave_sum(eq);
         if (lane == 0) {
-            a.tile_gt[tile] = gt;
-            a.tile_eq[tile] = eq;
+            st_co<CO>(&a.tile_gt[tile], gt);
+            st_co<CO>(&a.tile_eq[tile], eq);
         }
     }
 }
 
-template <bool QUANT>
-__global__ __launch_bounds__(kBlock) void k_emit(CandArgs a, EmitArgs o) {
+template <bool QUANT, bool CO>
+__device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o) {
     const int w = threadIdx.x >> 6, lane = lane_id();
     const uint32_t ntiles = a.tile_base[a.T];
     for (uint32_t tile = blockIdx.x * kWavesPerBlock + w; tile < ntiles; tile += gridDim.x * kWavesPerBlock) {
@@ -349,10 +368,12 @@ __global__ __launch_bounds__(kBlock) void k_emit(CandArgs a, EmitArgs o) {
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
             const uint32_t pl = v.p0 + r * kWave + lane;
-            ix[r] = pl < v.p1 ? a.cand_idx[pl] : 0u;
-            vb[r] = pl < v.p1 ? a.cand_val[pl] : 0u;
+            const uint32_t pc = pl < v.p1 ? pl : v.p0;
+            const uint32_t x = a.cand_idx[pc], y = a.cand_val[pc];
+            ix[r] = pl < v.p1 ? x : 0u;
+            vb[r] = pl < v.p1 ? y : 0u;
         }
-        const uint32_t thr = a.seg[v.s].thr, need = a.seg[v.s].need;
+        const uint32_t thr = ld_co<CO>(&a.seg[v.s].thr), need = ld_co<CO>(&a.seg[v.s].need);
         const uint32_t hi = v.miss ? kNoKey : a.seg[v.s].hi;
         // candidates above / equal to the threshold in earlier tiles of the segment
         uint32_t bg = 0, be = 0;
@@ -361,8 +382,10 @@ __global__ __launch_bounds__(kBlock) void k_emit(CandArgs a, EmitArgs o) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const uint32_t q = b0 + j * kWave + lane;
-                g8[j] = q < tile ? a.tile_gt[q] : 0u;
-                e8[j] = q < tile ? a.tile_eq[q] : 0u;
+                const uint32_t qc = q < tile ? q : v.first_tile;
+                const uint32_t x = ld_co<CO>(&a.tile_gt[qc]), y = ld_co<CO>(&a.tile_eq[qc]);
+                g8[j] = q < tile ? x : 0u;
+                e8[j] = q < tile ? y : 0u;
             }
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
@@ -426,15 +449,115 @@ __global__ __launch_bounds__(kBlock) void k_emit(CandArgs a, EmitArgs o) {
     }
 }
 
+// ---- five kernels, one per phase ----
+
+__global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
+    __shared__ uint32_t lds[kGatherLds];
+    phase_gather(a, lds);
+}
+
+template <int L>
+__global__ __launch_bounds__(kBlock) void k_radix(CandArgs a) {
+    __shared__ uint32_t lds[radix_lds<L>()];
+    phase_radix<L, false>(a, lds);
+}
+
+__global__ __launch_bounds__(kBlock) void k_count(CandArgs a) { phase_count<false>(a); }
+
+template <bool QUANT>
+__global__ __launch_bounds__(kBlock) void k_emit(CandArgs a, EmitArgs o) {
+    phase_emit<QUANT, false>(a, o);
+}
+
+// ---- one cooperative kernel ----
+
+// Grid barrier for a cooperative launch (every block co-resident).  Blocks
+// arrive on one of kSyncGroups counters (one cache line each), the last
+// arrival of a group on the top counter, and every block waits for the top
+// counter to reach this barrier's epoch.  Counters only grow within a launch
+// and start at zero (the layout kernel clears them).  Each wave's earlier
+// global writes and atomics have completed before its block arrives.  The
+// wait is bounded: after kSyncTimeout ticks of the 100 MHz clock the block
+// records a timeout in sync[kSyncFlag] and goes on, so a launch always ends.
+__device__ __forceinline__ void grid_sync(const CandArgs& a, uint32_t& epoch) {
+    // every wave waits until its own global stores and atomics are done (a
+    // workgroup-scope fence does not wait for them on this target)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        ++epoch;
+        const uint32_t G = gridDim.x;
+        const uint32_t ng = G < (uint32_t)kSyncGroups ? G : (uint32_t)kSyncGroups;
+        const uint32_t g = blockIdx.x % kSyncGroups;
+        const uint32_t gsize = (G - g + kSyncGroups - 1) / kSyncGroups;
+        uint32_t* top = a.sync + kSyncGroups * kSyncStride;
+        const uint32_t old =
+            __hip_atomic_fetch_add(a.sync + g * kSyncStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old + 1 == epoch * gsize) __hip_atomic_fetch_add(top, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t t0 = wall_clock64();
+        while (ld_co<true>(top) < epoch * ng) {
+            __builtin_amdgcn_s_sleep(1);
+            if (wall_clock64() - t0 > kSyncTimeout) {
+                st_co<true>(a.sync + kSyncFlag * kSyncStride, 1u);
+                break;
+            }
+        }
+    }
+    __syncthreads();
+}
+
+template <bool QUANT>
+__global__ __launch_bounds__(kBlock) void k_select(CandArgs a, EmitArgs o) {
+    __shared__ uint32_t lds[kGatherLds];
+    uint32_t epoch = 0;
+    phase_gather(a, lds);
+    grid_sync(a, epoch);
+    phase_radix<1, true>(a, lds);
+    grid_sync(a, epoch);
+    phase_radix<2, true>(a, lds);
+    grid_sync(a, epoch);
+    phase_count<true>(a);
+    grid_sync(a, epoch);
+    phase_emit<QUANT, true>(a, o);
+}
+
+static_assert(radix_lds<1>() <= kGatherLds && radix_lds<2>() <= kGatherLds, "phases share the gather LDS");
+
 static inline uint32_t blocks_for_waves(uint32_t waves) { return (waves + kWavesPerBlock - 1) / kWavesPerBlock; }
 
-hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles, hipStream_t st) {
+hipError_t select_grid_limit(uint32_t* blocks) {
+    *blocks = 0;
+    int dev = 0, coop = 0, cus = 0, per_cu_q = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(&k_select<false>),
+                                                         kBlock, 0);
+    if (e == hipSuccess)
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_q, reinterpret_cast<const void*>(&k_select<true>),
+                                                         kBlock, 0);
+    if (e != hipSuccess) return e;
+    const int m = per_cu < per_cu_q ? per_cu : per_cu_q;
+    if (coop && m > 0 && cus > 0) *blocks = (uint32_t)(m * cus);
+    return hipSuccess;
+}
+
+hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles,
+                             uint32_t coop_blocks, hipStream_t st) {
     if (a.num_units == 0) return hipSuccess;
     const dim3 b(kBlock);
-    uint32_t tb = blocks_for_waves(max_tiles);
-    if (tb > kTileBlocks) tb = kTileBlocks;
-    if (tb == 0) tb = 1;
-    const dim3 gt(tb);
+    const uint32_t need = blocks_for_waves(max_tiles) ? blocks_for_waves(max_tiles) : 1u;
+    if (coop_blocks > 0) {
+        const dim3 g(need < coop_blocks ? need : coop_blocks);
+        CandArgs ca = a;
+        EmitArgs oa = o;
+        void* args[] = {&ca, &oa};
+        const void* f = quant ? reinterpret_cast<const void*>(&k_select<true>)
+                              : reinterpret_cast<const void*>(&k_select<false>);
+        return hipLaunchCooperativeKernel(f, g, b, args, 0, st);
+    }
+    const dim3 gt(need < kTileBlocks ? need : kTileBlocks);
     hipLaunchKernelGGL(k_gather, gt, b, 0, st, a);
     hipLaunchKernelGGL(k_radix<1>, gt, b, 0, st, a);
     hipLaunchKernelGGL(k_radix<2>, gt, b, 0, st, a);

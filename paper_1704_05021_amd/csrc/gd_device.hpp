@@ -123,7 +123,22 @@ __device__ __forceinline__ double wave_sum(double v) {
 // holding the r-th largest element (r >= 1) and the number of elements in
 // higher digits.  Returns false when the histogram holds fewer than r
 // elements.  Called by a whole wave; hist may be global or LDS memory.
-template <int NB>
+// Loads and stores of words that other blocks of the same kernel read or
+// write between grid barriers: relaxed atomics at agent scope, which every
+// XCD sees coherently (no cache write-back or invalidate is needed).  With
+// CO false they are plain accesses, for data that crosses a kernel boundary.
+template <bool CO>
+__device__ __forceinline__ uint32_t ld_co(const uint32_t* p) {
+    if (CO) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return *p;
+}
+template <bool CO>
+__device__ __forceinline__ void st_co(uint32_t* p, uint32_t v) {
+    if (CO) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else *p = v;
+}
+
+template <int NB, bool CO = false>
 __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uint32_t& above) {
     constexpr int B = NB >= kWave ? NB / kWave : 1;
     const int lane = lane_id();
@@ -132,7 +147,7 @@ __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uin
     uint32_t sum = 0;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-        c[i] = top - 1 - i >= 0 ? hist[top - 1 - i] : 0u;
+        c[i] = top - 1 - i >= 0 ? ld_co<CO>(hist + (top - 1 - i)) : 0u;
         sum += c[i];
     }
     const uint32_t incl = wave_incl_scan(sum);
