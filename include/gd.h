@@ -161,23 +161,13 @@ gd_status gd_profile_read(gd_ctx* ctx, double* dense_ms, uint64_t* dense_launche
 gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode);
 
 /*
- * Test hook: choose how later gd_compress calls on this ctx run the passes
- * after the dense pass.  mode 0: one cooperative kernel with grid barriers
- * where the device supports cooperative launches (else five kernels); 1:
- * always five kernels.  Results are identical; GD_ERR_ARG for other modes.
- */
-gd_status gd_debug_force_path(gd_ctx* ctx, int mode);
-
-/*
  * Test hook: waits for the device, then copies the per-segment state of the
  * last gd_compress call (16 uint32 words per threshold segment: candidate
  * bracket lo and hi, candidate count, bracket-miss flag, radix digits and
  * ranks, threshold key, ties kept) for up to max_segments segments into
- * seg_words (host), and the decomposition into info (host, 6 entries:
- * elements per dense-pass unit, units, candidates per tile, most tiles,
- * blocks of the cooperative select kernel (0 when five kernels run), and 1
- * if a grid barrier of the last call timed out, else 0).  Synchronises the
- * host.
+ * seg_words (host), and the decomposition into info (host, 4 entries:
+ * elements per dense-pass unit, units, candidates per tile, most tiles).
+ * Synchronises the host.
  */
 gd_status gd_debug_state(gd_ctx* ctx, uint32_t* seg_words, uint32_t max_segments, uint64_t* info);
 

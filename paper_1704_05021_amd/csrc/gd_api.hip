@@ -166,15 +166,13 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
          dev_alloc(ctx, &ctx->scr.flags, 4) && dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) &&
          dev_alloc(ctx, &ctx->scr.seg, S_max) && dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
          dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&
-         dev_alloc(ctx, &ctx->scr.qbase, T + 1) && dev_alloc(ctx, &ctx->scr.shist, (size_t)S_max * gd::kSHistWords) &&
-         dev_alloc(ctx, &ctx->scr.sync, gd::kSyncWords);
+         dev_alloc(ctx, &ctx->scr.qbase, T + 1) && dev_alloc(ctx, &ctx->scr.shist, (size_t)S_max * gd::kSHistWords);
     if (!ok) {
         free_all(ctx);
         delete ctx;
         return GD_ERR_OOM;
     }
-    if (gd::select_grid_limit(&ctx->coop_blocks) != hipSuccess ||
-        hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
+    if (hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
         hipMemset(ctx->scr.shist, 0, (size_t)S_max * gd::kSHistWords * sizeof(uint32_t)) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
         free_all(ctx);
@@ -290,7 +288,6 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ca.tile_eq = ctx->scr.tile_eq;
     ca.tile_q = ctx->scr.tile_q;
     ca.out_base = ctx->scr.out_base;
-    ca.sync = ctx->scr.sync;
     gd::EmitArgs ea{};
     ea.idx = out->idx;
     ea.val = out->val;
@@ -298,8 +295,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ea.capacity = out->capacity;
     const bool q = quant == GD_QUANT_SIGN_MEAN;
     if (gd::launch_layout(ca, st) != hipSuccess) return GD_ERR_HIP;
-    const uint32_t coop = ctx->debug_path == 1 ? 0u : ctx->coop_blocks;
-    if (gd::launch_candidates(ca, ea, q, ctx->max_tiles, coop, st) != hipSuccess) return GD_ERR_HIP;
+    if (gd::launch_candidates(ca, ea, q, ctx->max_tiles, st) != hipSuccess) return GD_ERR_HIP;
 
     if (q) {
         gd::QuantArgs qa{};
@@ -350,12 +346,6 @@ gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode) {
     return GD_OK;
 }
 
-gd_status gd_debug_force_path(gd_ctx* ctx, int mode) {
-    if (!ctx || mode < 0 || mode > 1) return GD_ERR_ARG;
-    ctx->debug_path = (uint32_t)mode;
-    return GD_OK;
-}
-
 gd_status gd_debug_state(gd_ctx* ctx, uint32_t* seg_words, uint32_t max_segments, uint64_t* info) {
     if (!ctx || !info || (max_segments && !seg_words)) return GD_ERR_ARG;
     DeviceGuard guard(ctx->device);
@@ -363,18 +353,9 @@ gd_status gd_debug_state(gd_ctx* ctx, uint32_t* seg_words, uint32_t max_segments
     info[1] = ctx->num_units;
     info[2] = gd::kTile;
     info[3] = ctx->max_tiles;
-    info[4] = ctx->debug_path == 1 ? 0u : ctx->coop_blocks;
-    info[5] = 0;
-    if (hipDeviceSynchronize() != hipSuccess) return GD_ERR_HIP;
-    if (ctx->num_units > 0) {
-        uint32_t flag = 0;
-        if (hipMemcpy(&flag, ctx->scr.sync + gd::kSyncFlag * gd::kSyncStride, sizeof flag, hipMemcpyDeviceToHost) !=
-            hipSuccess)
-            return GD_ERR_HIP;
-        info[5] = flag;
-    }
     const uint32_t n = std::min(max_segments, ctx->T);
     if (n == 0) return GD_OK;
+    if (hipDeviceSynchronize() != hipSuccess) return GD_ERR_HIP;
     if (hipMemcpy(seg_words, ctx->scr.seg, n * sizeof(gd::SegState), hipMemcpyDeviceToHost) != hipSuccess)
         return GD_ERR_HIP;
     return GD_OK;

@@ -11,7 +11,10 @@
 //              histogram.
 //   radix<L> : digit L-1 of the k-th largest key from the previous
 //              histogram; the histogram of digit L over the candidates that
-//              share the prefix found so far (L = 1, 2).
+//              share the prefix found so far (L = 1, 2; digits of 10, 8 and
+//              13 key bits).  Few candidates share the first 18 bits, so
+//              digit 2 is counted with direct global atomics (fine and
+//              coarse bins) instead of block histograms.
 //   count    : the last digit, i.e. the exact threshold key T and the number
 //              of candidates equal to T to keep (lowest index first); per
 //              tile, the candidates above and equal to T.
@@ -21,15 +24,11 @@
 //              for quantisation).
 //
 // Together they realise the exact-k rule: keep the k largest |acc| of each
-// segment, ties broken by lower flat index (Algorithm 1, Section 4).
-//
-// The phases run either as five kernels, or as one cooperative kernel
-// (k_select) whose co-resident blocks meet at grid barriers between phases.
-// A wave handles the same tiles in every phase, so the compact candidates it
-// wrote are its own; what crosses blocks inside k_select (histograms, digit
-// ranks, the threshold, per-tile counts) goes through agent-scope atomics,
-// which every XCD sees coherently without cache write-backs.
-//
+// segment, ties broken by lower flat index (Algorithm 1, Section 4).  Each
+// phase is one kernel: on this part a kernel boundary (about 1.5 us) is
+// cheaper than the coherent reads a grid barrier needs for every wave to
+// see the shared histograms.
+
 // The histogram phases run in rounds of four consecutive tiles per block;
 // each wave counts into its own LDS histogram and the block adds the four
 // to the segment histogram once per round (waves of one segment merged), so
@@ -251,42 +250,45 @@ struct Level<2> {
     static constexpr int kPrefixShift = kD1Shift, kDigitShift = 0, kPrevBits = kD0Shift - kD1Shift;
 };
 
-template <int L, bool CO>
+template <int L>
 __device__ __forceinline__ void read_level(const SegState& g, uint32_t k, uint32_t& prefix, uint32_t& rank) {
     if (L == 1) {
         prefix = 0;
         rank = k;
     } else {
-        prefix = ld_co<CO>(&g.d0);
-        rank = ld_co<CO>(&g.r1);
+        prefix = g.d0;
+        rank = g.r1;
     }
 }
 
-template <int L, bool CO>
+template <int L>
 __device__ __forceinline__ void write_level(SegState& g, uint32_t prefix, uint32_t rank) {
     if (L == 1) {
-        st_co<CO>(&g.d0, prefix);
-        st_co<CO>(&g.r1, rank);
+        g.d0 = prefix;
+        g.r1 = rank;
     } else {
-        st_co<CO>(&g.p20, prefix);
-        st_co<CO>(&g.r2, rank);
+        g.p18 = prefix;
+        g.r2 = rank;
     }
 }
 
 template <int L>
 constexpr int radix_lds() {
-    return kWavesPerBlock * (Level<L>::kNB / 2) + kWavesPerBlock;
+    return L == 1 ? kWavesPerBlock * (Level<L>::kNB / 2) + kWavesPerBlock : 1;
 }
 
-template <int L, bool CO>
+template <int L>
 __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
     using Lv = Level<L>;
+    constexpr bool kBlockHist = L == 1;
     const int w = threadIdx.x >> 6, lane = lane_id();
     uint32_t* lh = lds;
     uint32_t* hw = lh + w * (Lv::kNB / 2);
     uint32_t* wseg = lh + kWavesPerBlock * (Lv::kNB / 2);
-    for (int i = lane; i < Lv::kNB / 2; i += kWave) hw[i] = 0;
-    wave_lds_sync();
+    if (kBlockHist) {
+        for (int i = lane; i < Lv::kNB / 2; i += kWave) hw[i] = 0;
+        wave_lds_sync();
+    }
     const uint32_t ntiles = a.tile_base[a.T];
     uint32_t cached_s = kNoKey, prefix = 0, rank = 0;
     for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += gridDim.x * kWavesPerBlock) {
@@ -298,28 +300,41 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
             load_keys(a, v, key);
             if (v.s != cached_s) {
                 uint32_t p0, r0, d, ab;
-                read_level<L, CO>(a.seg[v.s], v.k, p0, r0);
-                wave_pick<Lv::kPrevNB, CO>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
+                read_level<L>(a.seg[v.s], v.k, p0, r0);
+                wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
                 prefix = (p0 << Lv::kPrevBits) | d;
                 rank = r0 - ab;
                 cached_s = v.s;
             }
-            if (tile == v.first_tile && lane == 0) write_level<L, CO>(a.seg[v.s], prefix, rank);
+            if (tile == v.first_tile && lane == 0) write_level<L>(a.seg[v.s], prefix, rank);
+            if (kBlockHist) {
 #pragma unroll
-            for (int r = 0; r < kRows; ++r) {
-                const bool active = v.p0 + r * kWave + lane < v.p1;
-                lds_hist_add16(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
-                               active && (key[r] >> Lv::kPrefixShift) == prefix);
+                for (int r = 0; r < kRows; ++r) {
+                    const bool active = v.p0 + r * kWave + lane < v.p1;
+                    lds_hist_add16(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
+                                   active && (key[r] >> Lv::kPrefixShift) == prefix);
+                }
+                if (lane == 0) wseg[w] = v.s;
+            } else {
+                uint32_t* hf = seg_hist(a, v.s, kHistH2);
+                uint32_t* hc = seg_hist(a, v.s, kHistH2c);
+#pragma unroll
+                for (int r = 0; r < kRows; ++r) {
+                    const bool active = v.p0 + r * kWave + lane < v.p1;
+                    if (active && (key[r] >> Lv::kPrefixShift) == prefix) {
+                        const uint32_t d = key[r] & (Lv::kNB - 1);
+                        atomicAdd(hf + d, 1u);
+                        atomicAdd(hc + (d >> kD2cShift), 1u);
+                    }
+                }
             }
-            if (lane == 0) wseg[w] = v.s;
-        } else if (lane == 0) {
+        } else if (kBlockHist && lane == 0) {
             wseg[w] = kNoKey;
         }
-        block_flush<Lv::kNB>(a, lh, wseg, Lv::kHist);
+        if (kBlockHist) block_flush<Lv::kNB>(a, lh, wseg, Lv::kHist);
     }
 }
 
-template <bool CO>
 __device__ __forceinline__ void phase_count(const CandArgs& a) {
     const int w = threadIdx.x >> 6, lane = lane_id();
     const uint32_t ntiles = a.tile_base[a.T];
@@ -330,16 +345,18 @@ __device__ __forceinline__ void phase_count(const CandArgs& a) {
         uint32_t key[kRows];
         load_keys(a, v, key);
         if (v.s != cached_s) {
-            const uint32_t p20 = ld_co<CO>(&a.seg[v.s].p20), r2 = ld_co<CO>(&a.seg[v.s].r2);
-            uint32_t d2, ab;
-            wave_pick<kNB2, CO>(seg_hist(a, v.s, kHistH2), r2, d2, ab);
-            thr = (p20 << kD1Shift) | d2;
-            need = r2 - ab;
+            // digit 2 in two steps: its coarse bin, then the bin among 32
+            const uint32_t p18 = a.seg[v.s].p18, r2 = a.seg[v.s].r2;
+            uint32_t dc, abc, df, abf;
+            wave_pick<kNB2c>(seg_hist(a, v.s, kHistH2c), r2, dc, abc);
+            wave_pick<kNB2 / kNB2c>(seg_hist(a, v.s, kHistH2) + (dc << kD2cShift), r2 - abc, df, abf);
+            thr = (p18 << kD1Shift) | (dc << kD2cShift) | df;
+            need = r2 - abc - abf;
             cached_s = v.s;
         }
         if (tile == v.first_tile && lane == 0) {
-            st_co<CO>(&a.seg[v.s].thr, thr);
-            st_co<CO>(&a.seg[v.s].need, need);
+            a.seg[v.s].thr = thr;
+            a.seg[v.s].need = need;
         }
         uint32_t gt = 0, eq = 0;
 #pragma unroll
@@ -351,13 +368,13 @@ __device__ __forceinline__ void phase_count(const CandArgs& a) {
         gt = wave_sum(gt);
         eq = wave_sum(eq);
         if (lane == 0) {
-            st_co<CO>(&a.tile_gt[tile], gt);
-            st_co<CO>(&a.tile_eq[tile], eq);
+            a.tile_gt[tile] = gt;
+            a.tile_eq[tile] = eq;
         }
     }
 }
 
-template <bool QUANT, bool CO>
+template <bool QUANT>
 __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o) {
     const int w = threadIdx.x >> 6, lane = lane_id();
     const uint32_t ntiles = a.tile_base[a.T];
@@ -373,8 +390,8 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             ix[r] = pl < v.p1 ? x : 0u;
             vb[r] = pl < v.p1 ? y : 0u;
         }
-        const uint32_t thr = ld_co<CO>(&a.seg[v.s].thr), need = ld_co<CO>(&a.seg[v.s].need);
         const uint32_t hi = v.miss ? kNoKey : a.seg[v.s].hi;
+        const uint32_t thr = a.seg[v.s].thr, need = a.seg[v.s].need;
         // candidates above / equal to the threshold in earlier tiles of the segment
         uint32_t bg = 0, be = 0;
         for (uint32_t b0 = v.first_tile; b0 < tile; b0 += 8 * kWave) {
@@ -382,8 +399,8 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const uint32_t q = b0 + j * kWave + lane;
-                const uint32_t qc = q < tile ? q : v.first_tile;
-                const uint32_t x = ld_co<CO>(&a.tile_gt[qc]), y = ld_co<CO>(&a.tile_eq[qc]);
+                const uint32_t qc = q < tile ? q : v.first_tile;  // unconditional loads, all in flight
+                const uint32_t x = a.tile_gt[qc], y = a.tile_eq[qc];
                 g8[j] = q < tile ? x : 0u;
                 e8[j] = q < tile ? y : 0u;
             }
@@ -449,8 +466,6 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
     }
 }
 
-// ---- five kernels, one per phase ----
-
 __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
     __shared__ uint32_t lds[kGatherLds];
     phase_gather(a, lds);
@@ -459,104 +474,22 @@ __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
 template <int L>
 __global__ __launch_bounds__(kBlock) void k_radix(CandArgs a) {
     __shared__ uint32_t lds[radix_lds<L>()];
-    phase_radix<L, false>(a, lds);
+    phase_radix<L>(a, lds);
 }
 
-__global__ __launch_bounds__(kBlock) void k_count(CandArgs a) { phase_count<false>(a); }
+__global__ __launch_bounds__(kBlock) void k_count(CandArgs a) { phase_count(a); }
 
 template <bool QUANT>
 __global__ __launch_bounds__(kBlock) void k_emit(CandArgs a, EmitArgs o) {
-    phase_emit<QUANT, false>(a, o);
+    phase_emit<QUANT>(a, o);
 }
-
-// ---- one cooperative kernel ----
-
-// Grid barrier for a cooperative launch (every block co-resident).  Blocks
-// arrive on one of kSyncGroups counters (one cache line each), the last
-// arrival of a group on the top counter, and every block waits for the top
-// counter to reach this barrier's epoch.  Counters only grow within a launch
-// and start at zero (the layout kernel clears them).  Each wave's earlier
-// global writes and atomics have completed before its block arrives.  The
-// wait is bounded: after kSyncTimeout ticks of the 100 MHz clock the block
-// records a timeout in sync[kSyncFlag] and goes on, so a launch always ends.
-__device__ __forceinline__ void grid_sync(const CandArgs& a, uint32_t& epoch) {
-    // every wave waits until its own global stores and atomics are done (a
-    // workgroup-scope fence does not wait for them on this target)
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        ++epoch;
-        const uint32_t G = gridDim.x;
-        const uint32_t ng = G < (uint32_t)kSyncGroups ? G : (uint32_t)kSyncGroups;
-        const uint32_t g = blockIdx.x % kSyncGroups;
-        const uint32_t gsize = (G - g + kSyncGroups - 1) / kSyncGroups;
-        uint32_t* top = a.sync + kSyncGroups * kSyncStride;
-        const uint32_t old =
-            __hip_atomic_fetch_add(a.sync + g * kSyncStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (old + 1 == epoch * gsize) __hip_atomic_fetch_add(top, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const uint64_t t0 = wall_clock64();
-        while (ld_co<true>(top) < epoch * ng) {
-            __builtin_amdgcn_s_sleep(1);
-            if (wall_clock64() - t0 > kSyncTimeout) {
-                st_co<true>(a.sync + kSyncFlag * kSyncStride, 1u);
-                break;
-            }
-        }
-    }
-    __syncthreads();
-}
-
-template <bool QUANT>
-__global__ __launch_bounds__(kBlock) void k_select(CandArgs a, EmitArgs o) {
-    __shared__ uint32_t lds[kGatherLds];
-    uint32_t epoch = 0;
-    phase_gather(a, lds);
-    grid_sync(a, epoch);
-    phase_radix<1, true>(a, lds);
-    grid_sync(a, epoch);
-    phase_radix<2, true>(a, lds);
-    grid_sync(a, epoch);
-    phase_count<true>(a);
-    grid_sync(a, epoch);
-    phase_emit<QUANT, true>(a, o);
-}
-
-static_assert(radix_lds<1>() <= kGatherLds && radix_lds<2>() <= kGatherLds, "phases share the gather LDS");
 
 static inline uint32_t blocks_for_waves(uint32_t waves) { return (waves + kWavesPerBlock - 1) / kWavesPerBlock; }
 
-hipError_t select_grid_limit(uint32_t* blocks) {
-    *blocks = 0;
-    int dev = 0, coop = 0, cus = 0, per_cu_q = 0, per_cu = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess)
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(&k_select<false>),
-                                                         kBlock, 0);
-    if (e == hipSuccess)
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_q, reinterpret_cast<const void*>(&k_select<true>),
-                                                         kBlock, 0);
-    if (e != hipSuccess) return e;
-    const int m = per_cu < per_cu_q ? per_cu : per_cu_q;
-    if (coop && m > 0 && cus > 0) *blocks = (uint32_t)(m * cus);
-    return hipSuccess;
-}
-
-hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles,
-                             uint32_t coop_blocks, hipStream_t st) {
+hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles, hipStream_t st) {
     if (a.num_units == 0) return hipSuccess;
     const dim3 b(kBlock);
     const uint32_t need = blocks_for_waves(max_tiles) ? blocks_for_waves(max_tiles) : 1u;
-    if (coop_blocks > 0) {
-        const dim3 g(need < coop_blocks ? need : coop_blocks);
-        CandArgs ca = a;
-        EmitArgs oa = o;
-        void* args[] = {&ca, &oa};
-        const void* f = quant ? reinterpret_cast<const void*>(&k_select<true>)
-                              : reinterpret_cast<const void*>(&k_select<false>);
-        return hipLaunchCooperativeKernel(f, g, b, args, 0, st);
-    }
     const dim3 gt(need < kTileBlocks ? need : kTileBlocks);
     hipLaunchKernelGGL(k_gather, gt, b, 0, st, a);
     hipLaunchKernelGGL(k_radix<1>, gt, b, 0, st, a);

@@ -18,14 +18,19 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;  // above every key: "nothing qualifies"
 
 // The 31 key bits are resolved in three radix digits, most significant
-// first: 10, 10 and 11 bits.
+// first: 10, 8 and 13 bits.  Digit 1 is narrow because the candidates that
+// share the threshold's digit 0 are many and every bin a block touches costs
+// one global atomic; digit 2 is wide because few candidates share the first
+// 18 bits, so its histogram stays sparse.
 constexpr int kD0Shift = 21, kNB0 = 1024;  // key bits 30..21
-constexpr int kD1Shift = 11, kNB1 = 1024;  // key bits 20..11
-constexpr int kNB2 = 2048;                 // key bits 10..0
+constexpr int kD1Shift = 13, kNB1 = 256;   // key bits 20..13
+constexpr int kNB2 = 8192;                 // key bits 12..0
 
-// Histogram words per threshold segment, one histogram per digit.
-constexpr int kHistH0 = 0, kHistH1 = kNB0, kHistH2 = kNB0 + kNB1;
-constexpr int kHistWords = kNB0 + kNB1 + kNB2;
+// Histogram words per threshold segment: one histogram per digit, and digit
+// 2 also in 256 coarse bins of 32 (its top 8 bits) for a two-step pick.
+constexpr int kNB2c = 256, kD2cShift = 5;
+constexpr int kHistH0 = 0, kHistH1 = kNB0, kHistH2 = kNB0 + kNB1, kHistH2c = kNB0 + kNB1 + kNB2;
+constexpr int kHistWords = kNB0 + kNB1 + kNB2 + kNB2c;
 
 // Sampling: units of 16 consecutive elements (one 64-byte line per array),
 // at most kMaxUnits units per segment.  A sample key is the top 16 bits of
@@ -69,7 +74,7 @@ struct SegState {
     uint32_t miss;  // 1 when fewer than k candidates: every element becomes one
     uint32_t d0;    // digit 0 of the threshold key (key >> 21)
     uint32_t r1;    // rank of the threshold among candidates with that digit 0
-    uint32_t p20;   // key >> 11 of the threshold key
+    uint32_t p18;   // key >> 13 of the threshold key
     uint32_t r2;    // rank among candidates with that prefix
     uint32_t thr;   // the threshold key T (kNoKey when nothing is kept)
     uint32_t need;  // entries with key == T to keep, lowest index first
@@ -123,22 +128,7 @@ __device__ __forceinline__ double wave_sum(double v) {
 // holding the r-th largest element (r >= 1) and the number of elements in
 // higher digits.  Returns false when the histogram holds fewer than r
 // elements.  Called by a whole wave; hist may be global or LDS memory.
-// Loads and stores of words that other blocks of the same kernel read or
-// write between grid barriers: relaxed atomics at agent scope, which every
-// XCD sees coherently (no cache write-back or invalidate is needed).  With
-// CO false they are plain accesses, for data that crosses a kernel boundary.
-template <bool CO>
-__device__ __forceinline__ uint32_t ld_co(const uint32_t* p) {
-    if (CO) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return *p;
-}
-template <bool CO>
-__device__ __forceinline__ void st_co(uint32_t* p, uint32_t v) {
-    if (CO) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else *p = v;
-}
-
-template <int NB, bool CO = false>
+template <int NB>
 __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uint32_t& above) {
     constexpr int B = NB >= kWave ? NB / kWave : 1;
     const int lane = lane_id();
@@ -147,7 +137,7 @@ __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uin
     uint32_t sum = 0;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-        c[i] = top - 1 - i >= 0 ? ld_co<CO>(hist + (top - 1 - i)) : 0u;
+        c[i] = top - 1 - i >= 0 ? hist[top - 1 - i] : 0u;
         sum += c[i];
     }
     const uint32_t incl = wave_incl_scan(sum);

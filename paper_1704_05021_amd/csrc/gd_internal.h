@@ -53,7 +53,6 @@ struct Scratch {
     SegState* seg = nullptr;         // [S_max]
     uint64_t* out_base = nullptr;    // [S_max] first output slot of each segment
     uint16_t* skeys = nullptr;       // 16-bit sample keys
-    uint32_t* sync = nullptr;        // [kSyncWords] grid barrier of the select kernel
     uint32_t* shist = nullptr;       // [S_max * kSHistWords] sample histograms, kept zero between calls
     uint32_t* qbase = nullptr;       // [T + 1] first output slot of each tensor
 };
@@ -73,8 +72,6 @@ struct gd_ctx {
     gd::Scratch scr;
     std::vector<void*> allocations;
     uint32_t debug_bracket = 0;
-    uint32_t debug_path = 0;    // 1: five candidate kernels even where the cooperative one can run
-    uint32_t coop_blocks = 0;   // most co-resident blocks of the cooperative select kernel (0: none)
     bool profile = false;
     std::vector<hipEvent_t> events;  // pairs
     size_t events_used = 0;

@@ -51,14 +51,6 @@ struct DenseArgs {
 constexpr uint32_t kTile = 1024;        // candidates per tile of the candidate passes
 constexpr uint32_t kTileBlocks = 512;   // most blocks a candidate pass launches (4 waves each)
 
-// Grid barrier words of the cooperative select kernel: kSyncGroups arrival
-// counters, the top counter and a timeout flag, one 128-byte line each.
-constexpr int kSyncGroups = 8;
-constexpr int kSyncStride = 32;
-constexpr int kSyncFlag = kSyncGroups + 1;
-constexpr int kSyncWords = (kSyncGroups + 2) * kSyncStride;
-constexpr uint64_t kSyncTimeout = 20000000;  // 200 ms of the 100 MHz wall clock
-
 struct CandArgs {
     float* res;
     const uint32_t* unit_info;      // [C]
@@ -96,7 +88,6 @@ struct CandArgs {
     double* tile_q;       // [max tiles * 4]
     const uint64_t* out_base;
     uint32_t* flags;      // [0]: some segment missed its bracket
-    uint32_t* sync;       // [kSyncWords] grid barrier of the cooperative select kernel
 };
 
 struct EmitArgs {
@@ -136,13 +127,7 @@ struct ApplyArgs {
 hipError_t launch_sample(const SampleArgs& a, bool has_base, hipStream_t st);
 hipError_t launch_layout(const CandArgs& a, hipStream_t st);
 hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st);
-// Most co-resident blocks of the cooperative select kernel on the current
-// device (0 when the device cannot launch cooperatively).
-hipError_t select_grid_limit(uint32_t* blocks);
-// The candidate passes: one cooperative kernel when coop_blocks > 0 (at most
-// that many blocks), else five kernels.
-hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles,
-                             uint32_t coop_blocks, hipStream_t st);
+hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles, hipStream_t st);
 hipError_t launch_quant(const QuantArgs& q, hipStream_t st);
 hipError_t launch_apply(const ApplyArgs& a, uint32_t max_nnz, hipStream_t st);
 

@@ -73,8 +73,6 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
     __shared__ uint32_t any_miss;
     const int tid = threadIdx.x;
     if (tid == 0) any_miss = 0;
-    // the select kernel's barrier counters and timeout flag start at zero
-    if (tid < kSyncGroups + 2) a.sync[tid * kSyncStride] = 0;
     uint32_t carry = 0, necarry = 0;
     for (uint32_t b0 = 0; b0 < nblocks; b0 += kScanThreads) {
         const uint32_t b = b0 + tid;

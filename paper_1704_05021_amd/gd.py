@@ -40,7 +40,6 @@ EXPORTS = [
     "gd_profile_enable",
     "gd_profile_read",
     "gd_debug_force_bracket",
-    "gd_debug_force_path",
     "gd_debug_state",
 ]
 
@@ -94,8 +93,6 @@ def _lib() -> ctypes.CDLL:
     lib.gd_profile_read.restype = i32
     lib.gd_debug_force_bracket.argtypes = [vp, i32]
     lib.gd_debug_force_bracket.restype = i32
-    lib.gd_debug_force_path.argtypes = [vp, i32]
-    lib.gd_debug_force_path.restype = i32
     lib.gd_debug_state.argtypes = [vp, vp, u32, vp]
     lib.gd_debug_state.restype = i32
     _LIB = lib
@@ -214,25 +211,19 @@ class Compressor:
         if st != 0:
             raise GDError(st, "gd_debug_force_bracket")
 
-    SEG_FIELDS = ("lo", "hi", "clo", "miss", "d0", "r1", "p20", "r2", "thr", "need")
-
-    def debug_force_path(self, mode: int) -> None:
-        """0: cooperative select kernel where available; 1: five kernels."""
-        st = _lib().gd_debug_force_path(self._h, int(mode))
-        if st != 0:
-            raise GDError(st, "gd_debug_force_path")
+    SEG_FIELDS = ("lo", "hi", "clo", "miss", "d0", "r1", "p18", "r2", "thr", "need")
 
     def debug_state(self):
         """(per-segment state of the last call as a list of dicts, decomposition info dict)."""
         import numpy as np
 
         words = np.zeros((max(self.T, 1), 16), dtype=np.uint32)
-        info = np.zeros(6, dtype=np.uint64)
+        info = np.zeros(4, dtype=np.uint64)
         st = _lib().gd_debug_state(self._h, words.ctypes.data, self.T, info.ctypes.data)
         if st != 0:
             raise GDError(st, "gd_debug_state")
         segs = [dict(zip(self.SEG_FIELDS, (int(x) for x in row[:10]))) for row in words]
-        keys = ("unit_len", "units", "tile", "max_tiles", "select_blocks", "barrier_timeout")
+        keys = ("unit_len", "units", "tile", "max_tiles")
         return segs, dict(zip(keys, (int(x) for x in info)))
 
     def profile_enable(self, on: bool = True) -> None:

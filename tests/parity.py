@@ -88,26 +88,15 @@ def assert_parity(g: Result, o: Result, quant: bool, what: str = "") -> None:
         assert np.array_equal(bits(g.residual), bits(o.residual)), f"{what}: equal centres but residuals differ"
 
 
-def assert_no_barrier_timeout(comp: gd.Compressor, what: str = "") -> None:
-    """The cooperative select kernel's grid barriers all completed in time."""
-    _, info = comp.debug_state()
-    assert info["barrier_timeout"] == 0, f"{what}: a grid barrier timed out"
-
-
 def check_case(grad, residual, offsets: Sequence[int], drop: float, per_tensor: bool, quant: bool,
-               base=None, comp: Optional[gd.Compressor] = None, debug_bracket: int = 0, path: int = 0,
+               base=None, comp: Optional[gd.Compressor] = None, debug_bracket: int = 0,
                what: str = "") -> Result:
-    """One GPU call against the oracle.  path 0: the cooperative select kernel
-    where the device has it; path 1: the five-kernel form of the same passes."""
     comp = comp or gd.Compressor(offsets)
     comp.debug_force_bracket(debug_bracket)
-    comp.debug_force_path(path)
     try:
         g = gpu_compress(comp, grad, residual, drop, per_tensor, quant, base)
-        assert_no_barrier_timeout(comp, what)
     finally:
         comp.debug_force_bracket(0)
-        comp.debug_force_path(0)
     o = oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base)
     assert_parity(g, o, quant, what)
     return o
