@@ -412,8 +412,8 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         }
         bg = wave_sum(bg);
         be = wave_sum(be);
+        const uint32_t be0 = be;
         const uint64_t ob = a.out_base[v.s];
-        uint32_t kept_n = 0;
         double sp = 0.0, sn = 0.0;
         uint32_t np = 0, nn = 0;
 #pragma unroll
@@ -431,7 +431,6 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
                     o.idx[pos] = ix[r];
                     o.val[pos] = __uint_as_float(vb[r]);
                 }
-                ++kept_n;
                 if (QUANT) {
                     const float x = __uint_as_float(vb[r]);
                     if (x < 0.0f) {
@@ -449,8 +448,34 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             bg += popc64(mg);
             be += popc64(me);
         }
-        kept_n = wave_sum(kept_n);
-        if (lane == 0 && kept_n) atomicAdd(&o.tensor_counts[v.t], kept_n);
+        if (tile == a.tile_base[v.t]) {
+            // The first tile of a tensor writes the tensor's kept count: per
+            // tile, every candidate above T plus the ties still needed (in
+            // ascending tile order within the segment).  No atomics: a few
+            // hundred tiles adding to one counter serialise badly.
+            const uint32_t tend = a.tile_base[v.t + 1];
+            uint32_t cnt = 0, run_e = be0;
+            for (uint32_t b0 = tile; b0 < tend; b0 += 8 * kWave) {
+                uint32_t g8[8], e8[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const uint32_t q = b0 + j * kWave + lane;
+                    const uint32_t qc = q < tend ? q : tile;
+                    const uint32_t x = a.tile_gt[qc], y = a.tile_eq[qc];
+                    g8[j] = q < tend ? x : 0u;
+                    e8[j] = q < tend ? y : 0u;
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const uint32_t ie = wave_incl_scan(e8[j]);
+                    const uint32_t before = run_e + ie - e8[j];
+                    const uint32_t ties = need > before ? (need - before < e8[j] ? need - before : e8[j]) : 0u;
+                    cnt += wave_sum(g8[j] + ties);
+                    run_e += __shfl(ie, kWave - 1, kWave);
+                }
+            }
+            if (lane == 0) o.tensor_counts[v.t] = cnt;
+        }
         if (QUANT) {
             sp = wave_sum(sp);
             sn = wave_sum(sn);
