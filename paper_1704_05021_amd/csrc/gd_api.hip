@@ -152,12 +152,12 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
               dev_upload(ctx, &ctx->tab.global_off, goff) && dev_upload(ctx, &ctx->tab.skey_base_tensor, sk_t) &&
               dev_upload(ctx, &ctx->tab.skey_base_global, sk_g);
     const uint32_t MT = ctx->max_tiles;
-    ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.wcnt, 4 * (size_t)C) &&
+    ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.cnt, C) &&
          dev_alloc(ctx, &ctx->scr.split, T) && dev_alloc(ctx, &ctx->scr.loc, C) &&
          dev_alloc(ctx, &ctx->scr.neloc, C) && dev_alloc(ctx, &ctx->scr.btot, scan_blocks) &&
          dev_alloc(ctx, &ctx->scr.betot, scan_blocks) && dev_alloc(ctx, &ctx->scr.boff, scan_blocks) &&
          dev_alloc(ctx, &ctx->scr.beoff, scan_blocks) && dev_alloc(ctx, &ctx->scr.ne_unit, C) &&
-         dev_alloc(ctx, &ctx->scr.ne_off, C + 1) && dev_alloc(ctx, &ctx->scr.ne_sub, C) && dev_alloc(ctx, &ctx->scr.num_ne, 1) &&
+         dev_alloc(ctx, &ctx->scr.ne_off, C + 1) && dev_alloc(ctx, &ctx->scr.num_ne, 1) &&
          dev_alloc(ctx, &ctx->scr.raw_tbase, T + 1) && dev_alloc(ctx, &ctx->scr.cand_idx, N) &&
          dev_alloc(ctx, &ctx->scr.cand_val, N) && dev_alloc(ctx, &ctx->scr.ten_cbase, T + 1) &&
          dev_alloc(ctx, &ctx->scr.tile_base, T + 1) && dev_alloc(ctx, &ctx->scr.tile_ne0, MT) &&
@@ -241,7 +241,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     da.per_tensor = per;
     da.seg = ctx->scr.seg;
     da.slots = ctx->scr.slots;
-    da.wcnt = ctx->scr.wcnt;
+    da.cnt = ctx->scr.cnt;
     const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_units > 0;
     if (timed && hipEventRecord(ctx->events[ctx->events_used], st) != hipSuccess) return GD_ERR_HIP;
     if (gd::launch_dense(da, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
@@ -264,7 +264,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ca.seg = ctx->scr.seg;
     ca.hist = ctx->scr.hist;
     ca.slots = ctx->scr.slots;
-    ca.wcnt = ctx->scr.wcnt;
+    ca.cnt = ctx->scr.cnt;
     ca.split = ctx->scr.split;
     ca.loc = ctx->scr.loc;
     ca.neloc = ctx->scr.neloc;
@@ -274,7 +274,6 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     ca.beoff = ctx->scr.beoff;
     ca.ne_unit = ctx->scr.ne_unit;
     ca.ne_off = ctx->scr.ne_off;
-    ca.ne_sub = ctx->scr.ne_sub;
     ca.num_ne = ctx->scr.num_ne;
     ca.raw_tbase = ctx->scr.raw_tbase;
     ca.cand_idx = ctx->scr.cand_idx;

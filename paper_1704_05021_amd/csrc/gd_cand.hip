@@ -5,7 +5,7 @@
 // candidates of one tensor, one wave per tile, so the work is balanced
 // however unevenly the candidates fall across the gradient.  Five phases:
 //
-//   gather   : compacts each tile's candidates from the per-quarter slots
+//   gather   : compacts each tile's candidates from the per-unit slots
 //              (or, for a missed segment, straight from the residual) into
 //              one array in ascending flat index, with the digit-0
 //              histogram.
@@ -105,8 +105,8 @@ constexpr uint32_t kWin = kTile;      // non-empty units held in the gather wind
 // units, so a window of kTile non-empty units starting at the unit that
 // holds the tile's first candidate always covers the tile.
 // LDS words of the gather phase: four digit-0 histograms, then per wave the
-// window offsets, units and quarter counts and the tile's slot map.
-constexpr int kGatherLds = kWavesPerBlock * (kNB0 / 2 + (kWin + 1) + kWin + kWin + kTile) + kWavesPerBlock;
+// window offsets and units and the tile's slot map.
+constexpr int kGatherLds = kWavesPerBlock * (kNB0 / 2 + (kWin + 1) + kWin + kTile) + kWavesPerBlock;
 
 __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
     const int w = threadIdx.x >> 6, lane = lane_id();
@@ -114,9 +114,8 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
     uint32_t* hw = lh + w * (kNB0 / 2);
     uint32_t* wo = lh + kWavesPerBlock * (kNB0 / 2) + w * (kWin + 1);
     uint32_t* wu = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1) + w * kWin;
-    uint32_t* ws = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + kWin) + w * kWin;
-    uint32_t* sm = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + 2 * kWin) + w * kTile;
-    uint32_t* wseg = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + 2 * kWin + kTile);
+    uint32_t* sm = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + kWin) + w * kTile;
+    uint32_t* wseg = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + kWin + kTile);
     for (int i = lane; i < kNB0 / 2; i += kWave) hw[i] = 0;
     wave_lds_sync();
     const uint32_t ntiles = a.tile_base[a.T];
@@ -147,7 +146,7 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
             const uint32_t nne = a.num_ne[0];
             {
                 constexpr int NW = (kWin + kWave) / kWave;
-                uint32_t xo[NW], xu[NW], xs[NW];
+                uint32_t xo[NW], xu[NW];
 #pragma unroll
                 for (int i = 0; i < NW; ++i) {
                     const uint32_t j = i * kWave + lane;
@@ -155,25 +154,20 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
                     // unconditional loads at clamped positions (j0 < nne here), so
                     // that all of them are in flight together
                     const uint32_t jo = j0 + j <= nne ? j0 + j : nne, ju = in ? j0 + j : j0;
-                    const uint32_t o = a.ne_off[jo], u = a.ne_unit[ju], sb = a.ne_sub[ju];
+                    const uint32_t o = a.ne_off[jo], u = a.ne_unit[ju];
                     xo[i] = (j <= kWin && j0 + j <= nne) ? o : kNoKey;
                     xu[i] = in ? u : 0u;
-                    xs[i] = in ? sb : 0u;
                 }
 #pragma unroll
                 for (int i = 0; i < NW; ++i) {
                     const uint32_t j = i * kWave + lane;
                     if (j <= kWin) wo[j] = xo[i];
-                    if (j < kWin) {
-                        wu[j] = xu[i];
-                        ws[j] = xs[i];
-                    }
+                    if (j < kWin) wu[j] = xu[i];
                 }
                 wave_lds_sync();
             }
             // merge path: lane L maps the kRows consecutive candidates starting
-            // at kRows * L to slot indices (one search, then a forward walk);
-            // rank x inside a unit lies in quarter q = #{running counts <= x}
+            // at kRows * L to slot indices (one search, then a forward walk)
             const uint32_t q0 = kRows * lane, cnt = v.p1 - v.p0, r0 = v.p0 + shift;
             if (q0 < cnt) {
                 uint32_t lo = 0, hi = kWin;
@@ -183,7 +177,7 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
                     if (wo[mid] <= rp0) lo = mid;
                     else hi = mid;
                 }
-                uint32_t j = lo, cur = wo[j], nxt = wo[j + 1], ub = wu[j] * kUnitLen, sub = ws[j];
+                uint32_t j = lo, cur = wo[j], nxt = wo[j + 1], ub = wu[j] * kUnitLen;
                 for (int i = 0; i < kRows && q0 + i < cnt; ++i) {
                     const uint32_t rp = rp0 + i;
                     while (rp >= nxt) {
@@ -191,13 +185,8 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
                         cur = nxt;
                         nxt = wo[j + 1];
                         ub = wu[j] * kUnitLen;
-                        sub = ws[j];
                     }
-                    const uint32_t x = rp - cur;
-                    const uint32_t c1 = sub & 0x3FFu, c2 = (sub >> 10) & 0x3FFu, c3 = sub >> 20;
-                    const uint32_t q = (x >= c1) + (x >= c2) + (x >= c3);
-                    const uint32_t before = q == 0 ? 0u : q == 1 ? c1 : q == 2 ? c2 : c3;
-                    sm[q0 + i] = ub + q * kQuarter + (x - before);
+                    sm[q0 + i] = ub + (rp - cur);
                 }
             }
             wave_lds_sync();

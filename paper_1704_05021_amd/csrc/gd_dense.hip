@@ -12,9 +12,8 @@
 //
 // A unit is the 1024 elements [1024u, 1024u + 1024) of the flat gradient,
 // one block of 256 threads with one 16-byte vector per thread, so every
-// load is aligned and issued before any table lookup.  Each wave compacts
-// the candidates of its quarter of the unit on its own, into slots
-// [1024u + 256w, ...), with no block barrier on the streaming path.  A unit
+// load is aligned and issued before any table lookup.  The block compacts
+// the unit's candidates into slots [1024u, ...) and stores their count.  A unit
 // that holds a tensor boundary also records, for each tensor starting inside
 // it, how many of its candidates precede that start (the candidate layout
 // needs it).
@@ -108,12 +107,22 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
         for (int q = 0; q < 4; ++q)
             if (e0 + q < uend) a.res[e0 + q] = ov[q];
     }
-    // ordered compaction over the wave's quarter: lanes in order, then the
-    // four elements of a lane
+    // ordered compaction over the unit: waves in order, lanes in order, then
+    // the four elements of a lane, into one contiguous list per unit (fewer
+    // partially written cache lines than a list per wave)
     const uint64_t m0 = ballot(cand[0]), m1 = ballot(cand[1]), m2 = ballot(cand[2]), m3 = ballot(cand[3]);
+    __shared__ uint32_t qc[kWavesPerBlock];
+    if (lane == 0) qc[w] = popc64(m0) + popc64(m1) + popc64(m2) + popc64(m3);
+    __syncthreads();
+    uint32_t base = 0, total = 0;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+        base += i < w ? qc[i] : 0u;
+        total += qc[i];
+    }
     if ((m0 | m1 | m2 | m3) != 0) {
-        uint32_t pos = lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
-        uint2* out = a.slots + ustart + w * kQuarter;
+        uint32_t pos = base + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
+        uint2* out = a.slots + ustart;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             if (cand[q]) {
@@ -122,7 +131,7 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
             }
         }
     }
-    if (lane == 0) a.wcnt[4 * u + w] = popc64(m0) + popc64(m1) + popc64(m2) + popc64(m3);
+    if (tid == 0) a.cnt[u] = total;
     if (boundary) {
         // candidates before each tensor start strictly inside the unit
         __shared__ uint32_t red[kWavesPerBlock];

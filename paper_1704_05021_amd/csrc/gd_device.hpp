@@ -58,10 +58,8 @@ constexpr int kK16Shift = 15;           // key16 = key >> 15
 constexpr int kS0Shift = 6, kSNB1 = 64;
 constexpr int kSHistWords = 1024 + 2;  // per segment: digit histogram of the sample, valid and zero counts  // key16 digits: bits 15..6 (= key digit 0), bits 5..0
 
-// Elements per unit of the dense pass (one block), and per quarter (one
-// wave, which compacts its candidates on its own).
+// Elements per unit of the dense pass (one block).
 constexpr uint32_t kUnitLen = 1024;
-constexpr uint32_t kQuarter = kUnitLen / 4;
 // Units per block of the candidate-count scan.
 constexpr uint32_t kScanUnits = 1024;
 constexpr int kScanThreads = 256;

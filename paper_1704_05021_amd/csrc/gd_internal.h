@@ -12,8 +12,7 @@ namespace gd {
 
 // Decomposition of the flat gradient, fixed at gd_create:
 //  * unit u: elements [1024u, 1024u + 1024) (the last one may be shorter),
-//    one block of the dense pass; the candidates of its quarter w (one wave)
-//    go to slots[1024u + 256w ...].
+//    one block of the dense pass; its candidates go to slots[1024u ...].
 //  * tile: up to kTile consecutive candidates of one tensor, one wave of the
 //    candidate passes (at most `max_tiles` of them).
 struct Tables {
@@ -26,7 +25,7 @@ struct Tables {
 
 struct Scratch {
     uint2* slots = nullptr;          // [max(N,1)] candidate (index, value bits) per unit
-    uint32_t* wcnt = nullptr;        // [4C] candidates per unit quarter
+    uint32_t* cnt = nullptr;         // [C] candidates per unit
     uint32_t* split = nullptr;       // [T] candidates of a tensor's first unit before the tensor
     uint32_t* loc = nullptr;         // [C] candidate offset of each unit inside its scan block
     uint32_t* neloc = nullptr;       // [C] non-empty unit index inside its scan block
@@ -36,7 +35,6 @@ struct Scratch {
     uint32_t* beoff = nullptr;       // [scan blocks]
     uint32_t* ne_unit = nullptr;     // [C] non-empty units in order
     uint32_t* ne_off = nullptr;      // [C + 1] their first candidate (dense-pass order)
-    uint32_t* ne_sub = nullptr;      // [C] their running quarter counts, packed
     uint32_t* num_ne = nullptr;      // [1]
     uint32_t* raw_tbase = nullptr;   // [T + 1]
     uint32_t* cand_idx = nullptr;    // [max(N,1)] candidates in ascending index order

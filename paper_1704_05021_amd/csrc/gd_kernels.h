@@ -43,8 +43,8 @@ struct DenseArgs {
     uint32_t T;
     uint32_t per_tensor;
     const SegState* seg;
-    uint2* slots;                // [C * 1024] candidates of unit u, quarter w at [1024u + 256w, ...)
-    uint32_t* wcnt;              // [4C] candidates of each quarter
+    uint2* slots;                // [C * 1024] candidates of unit u at [1024u, ...), ascending index
+    uint32_t* cnt;               // [C] candidates of each unit
     uint32_t* split;             // [T] candidates of a tensor's first unit that precede the tensor
 };
 
@@ -64,7 +64,7 @@ struct CandArgs {
     SegState* seg;
     uint32_t* hist;
     const uint2* slots;
-    const uint32_t* wcnt;   // [4C]
+    const uint32_t* cnt;    // [C]
     const uint32_t* split;  // [T]
     uint32_t* loc;        // [C] candidate offset of each unit inside its scan block
     uint32_t* neloc;      // [C] index of each non-empty unit inside its scan block
@@ -74,7 +74,6 @@ struct CandArgs {
     uint32_t* beoff;      // [scan blocks] first non-empty unit of each scan block
     uint32_t* ne_unit;    // [C] the non-empty units, in order
     uint32_t* ne_off;     // [C + 1] their first candidate (dense-pass order); [count] = total
-    uint32_t* ne_sub;     // [C] their quarter counts, running: c0 | (c0+c1) << 10 | (c0+c1+c2) << 20
     uint32_t* num_ne;     // [1] number of non-empty units
     uint32_t* raw_tbase;  // [T + 1] first candidate of each tensor (dense-pass order)
     uint32_t* cand_idx;   // [N] compact candidates, ascending flat index

@@ -34,15 +34,18 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(CandArgs a) {
     const int tid = threadIdx.x;
     const uint32_t C = a.num_units;
 
-    // 1. local scan of this block's 1024 units (4 per thread, 4 quarters each)
+    // 1. local scan of this block's 1024 units (4 per thread)
     const uint32_t x = blockIdx.x * kScanUnits + 4 * tid;
     uint32_t c[4] = {0, 0, 0, 0};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        if (x + q < C) {
-            const uint4 v = reinterpret_cast<const uint4*>(a.wcnt)[x + q];
-            c[q] = v.x + v.y + v.z + v.w;
-        }
+    if (x + 4 <= C) {
+        const uint4 v = *reinterpret_cast<const uint4*>(a.cnt + x);
+        c[0] = v.x;
+        c[1] = v.y;
+        c[2] = v.z;
+        c[3] = v.w;
+    } else {
+        for (int q = 0; q < 4; ++q)
+            if (x + q < C) c[q] = a.cnt[x + q];
     }
     uint32_t total, ne_total;
     const uint32_t excl = block_excl_scan<kScanThreads>(c[0] + c[1] + c[2] + c[3], lds, &total);
@@ -153,17 +156,14 @@ __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
     const uint32_t u = blockIdx.x * kBlock + threadIdx.x;
     const bool have = u < a.num_units;
     uint32_t raw = 0, cnt = 0, info = 0;
-    uint4 wc = make_uint4(0u, 0u, 0u, 0u);
     bool restore = false;
     if (have) {
         raw = a.loc[u] + a.boff[u / kScanUnits];
-        wc = reinterpret_cast<const uint4*>(a.wcnt)[u];
-        cnt = wc.x + wc.y + wc.z + wc.w;
+        cnt = a.cnt[u];
         const uint32_t ne = a.neloc[u] + a.beoff[u / kScanUnits];
         if (cnt) {
             a.ne_unit[ne] = u;
             a.ne_off[ne] = raw;
-            a.ne_sub[ne] = wc.x | (wc.x + wc.y) << 10 | (wc.x + wc.y + wc.z) << 20;
         }
         info = a.unit_info[u];
         const uint32_t ustart = u * kUnitLen, uend = ustart + kUnitLen < a.N ? ustart + kUnitLen : a.N;
@@ -185,29 +185,25 @@ __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
         }
     }
     // Missed segments: the dense pass wrote +0 where key >= hi; put acc back
-    // from the unit's candidate lists (one unit at a time, the whole wave).
+    // from the unit's candidate list (one unit at a time, the whole wave).
     uint64_t todo = ballot(restore);
     while (todo) {
         const int src = __ffsll((unsigned long long)todo) - 1;
         todo &= todo - 1;
-        const uint32_t uu = __shfl(u, src, kWave);
-        const uint32_t qc[4] = {__shfl(wc.x, src, kWave), __shfl(wc.y, src, kWave), __shfl(wc.z, src, kWave),
-                                __shfl(wc.w, src, kWave)};
-        for (int q = 0; q < 4; ++q) {
-            for (uint32_t i = lane_id(); i < qc[q]; i += kWave) {
-                const uint2 e = a.slots[(size_t)uu * kUnitLen + q * kQuarter + i];
-                uint32_t s = 0;
-                if (a.per_tensor) {
-                    uint32_t lo = 0, hi = a.T;
-                    while (hi - lo > 1) {
-                        const uint32_t mid = (lo + hi) >> 1;
-                        if (a.tensor_off[mid] <= e.x) lo = mid;
-                        else hi = mid;
-                    }
-                    s = lo;
+        const uint32_t uu = __shfl(u, src, kWave), nn = __shfl(cnt, src, kWave);
+        for (uint32_t i = lane_id(); i < nn; i += kWave) {
+            const uint2 e = a.slots[(size_t)uu * kUnitLen + i];
+            uint32_t s = 0;
+            if (a.per_tensor) {
+                uint32_t lo = 0, hi = a.T;
+                while (hi - lo > 1) {
+                    const uint32_t mid = (lo + hi) >> 1;
+                    if (a.tensor_off[mid] <= e.x) lo = mid;
+                    else hi = mid;
                 }
-                if (a.seg[s].miss && (e.y & 0x7FFFFFFFu) >= a.seg[s].hi) a.res[e.x] = __uint_as_float(e.y);
+                s = lo;
             }
+            if (a.seg[s].miss && (e.y & 0x7FFFFFFFu) >= a.seg[s].hi) a.res[e.x] = __uint_as_float(e.y);
         }
     }
 }
