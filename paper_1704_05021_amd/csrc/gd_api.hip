@@ -152,7 +152,7 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
               dev_upload(ctx, &ctx->tab.global_off, goff) && dev_upload(ctx, &ctx->tab.skey_base_tensor, sk_t) &&
               dev_upload(ctx, &ctx->tab.skey_base_global, sk_g);
     const uint32_t MT = ctx->max_tiles;
-    ok = ok && dev_alloc(ctx, &ctx->scr.slots, N) && dev_alloc(ctx, &ctx->scr.cnt, C) &&
+    ok = ok && dev_alloc(ctx, &ctx->scr.slots, (size_t)C * gd::kUnitLen) && dev_alloc(ctx, &ctx->scr.cnt, C) &&
          dev_alloc(ctx, &ctx->scr.split, T) && dev_alloc(ctx, &ctx->scr.loc, C) &&
          dev_alloc(ctx, &ctx->scr.neloc, C) && dev_alloc(ctx, &ctx->scr.btot, scan_blocks) &&
          dev_alloc(ctx, &ctx->scr.betot, scan_blocks) && dev_alloc(ctx, &ctx->scr.boff, scan_blocks) &&

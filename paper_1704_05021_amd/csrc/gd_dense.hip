@@ -131,6 +131,12 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
             }
         }
     }
+    {
+        // pad the list to whole 128-byte lines, so that no partially written
+        // line is left for HBM to merge
+        const uint32_t padded = (total + 15u) & ~15u;
+        if ((uint32_t)tid < padded - total) a.slots[ustart + total + tid] = make_uint2(kNoKey, 0u);
+    }
     if (tid == 0) a.cnt[u] = total;
     if (boundary) {
         // candidates before each tensor start strictly inside the unit
