@@ -49,6 +49,13 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.gdo_compress.restype = i32
     lib.gdo_apply_sparse.argtypes = [vp, u64, u32, vp, vp, vp, f32]
     lib.gdo_apply_sparse.restype = i32
+    lib.gdo_splitmix64.argtypes = [u64, u64]
+    lib.gdo_splitmix64.restype = u64
+    lib.gdo_sample_position.argtypes = [u64, u32, u64, u64, u64, u64]
+    lib.gdo_sample_position.restype = u64
+    lib.gdo_compress_sampled.argtypes = [vp, vp, vp, vp, u32, dbl, i32, u32, u64, vp, vp, vp, u64,
+                                         ctypes.POINTER(u64)]
+    lib.gdo_compress_sampled.restype = i32
     return lib
 
 
@@ -126,6 +133,50 @@ def compress(
     k = int(k.value)
     return Compressed(idx[:k].copy(), val[:k].copy(), r, counts,
                       None if bits is None else bits[:(k + 31) // 32].copy(), means)
+
+
+def splitmix64(seed: int, i: int, lib: Optional[ctypes.CDLL] = None) -> int:
+    """Output number i of SplitMix64 seeded with ``seed`` (the sample-position generator)."""
+    return int((lib or load()).gdo_splitmix64(seed, i))
+
+
+def sample_position(seed: int, s: int, a: int, n: int, m: int, j: int, lib: Optional[ctypes.CDLL] = None) -> int:
+    """Flat position of sample j of m drawn from segment s = [a, a + n)."""
+    return int((lib or load()).gdo_sample_position(seed, s, a, n, m, j))
+
+
+def compress_sampled(
+    grad: np.ndarray,
+    residual: np.ndarray,
+    offsets: Sequence[int],
+    drop_ratio: float = 0.99,
+    per_tensor: bool = False,
+    sample_ppm: int = 1000,
+    seed: int = 0,
+    base: Optional[np.ndarray] = None,
+    capacity: Optional[int] = None,
+    lib: Optional[ctypes.CDLL] = None,
+) -> Compressed:
+    """Algorithm 1 with the threshold selected on a sample (Section 4); inputs are not modified."""
+    lib = lib or load()
+    g = np.ascontiguousarray(grad, dtype=np.float32)
+    r = np.array(residual, dtype=np.float32, copy=True)
+    b = None if base is None else np.ascontiguousarray(base, dtype=np.float32)
+    off = np.ascontiguousarray(offsets, dtype=np.uint64)
+    T = off.size - 1
+    assert off[-1] == g.size == r.size
+    cap = int(g.size) if capacity is None else int(capacity)
+    idx = np.zeros(max(cap, 1), np.uint32)
+    val = np.zeros(max(cap, 1), np.float32)
+    counts = np.zeros(T, np.uint32)
+    k = ctypes.c_uint64(0)
+    rc = lib.gdo_compress_sampled(_ptr(g), _ptr(b), _ptr(r), _ptr(off), T, float(drop_ratio), int(per_tensor),
+                                  int(sample_ppm), int(seed), _ptr(idx), _ptr(val), _ptr(counts), cap,
+                                  ctypes.byref(k))
+    if rc != 0:
+        raise ValueError(f"gdo_compress_sampled failed with status {rc}")
+    k = int(k.value)
+    return Compressed(idx[:k].copy(), val[:k].copy(), r, counts, None, None)
 
 
 def apply_sparse(params: np.ndarray, idx: List[np.ndarray], val: List[np.ndarray], lr: float = 1.0,

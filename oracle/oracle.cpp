@@ -38,6 +38,19 @@
 //   R6  server apply: s[i] = sum of the pushed values at i in client order
 //       (float adds starting from +0.0f), then p[i] = p[i] - lr * s[i].
 //   R7  pull delta: acc = (p_new - p_last) + residual, two float roundings.
+//   R9  sampled threshold (Section 4: select on a 0.1% sample of the
+//       gradient, then keep what lies strictly above the threshold):
+//       segment s of n entries draws m = ceil(n * sample_ppm / 1e6)
+//       positions, one per stratum [floor(j n / m), floor((j+1) n / m)), at
+//       offset u mod (stratum length), where u is output number
+//       2^32 * s + j of SplitMix64 seeded with `seed` (Steele, Lea and Flood,
+//       OOPSLA 2014).  With k_m = floor(m * keep_ppm / 1e6) the threshold T
+//       is the (k_m + 1)-th largest sample key (the exact mode's relation to
+//       Algorithm 1, R2; for k_m = 0 the largest) and entries with key > T
+//       are kept; k_m >= m keeps everything and R = 1 (keep_ppm = 0) keeps
+//       nothing.  The count is data dependent; kept entries past the output
+//       capacity (in ascending index) are not sent and keep acc in the
+//       residual.
 //
 // Build: g++ -O2 -ffp-contract=off -fPIC -shared (no fast-math).
 
@@ -227,6 +240,119 @@ int gdo_compress(const float* grad, const float* base, float* residual, const ui
             first = last;
         }
     }
+    return 0;
+}
+
+// R9: output number i of SplitMix64 seeded with seed: the state advances by
+// the golden-ratio increment once per output and is then mixed.
+uint64_t gdo_splitmix64(uint64_t seed, uint64_t i) {
+    uint64_t z = seed + (i + 1) * 0x9E3779B97F4A7C15ull;
+#ifdef GDO_MUTANT_SPLITMIX_SHIFT
+    z = (z ^ (z >> 31)) * 0xBF58476D1CE4E5B9ull;  // mutant: wrong first shift
+#else
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+#endif
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// Position of sample j of segment s ([a, a+n)) among m samples (R9).
+uint64_t gdo_sample_position(uint64_t seed, uint32_t s, uint64_t a, uint64_t n, uint64_t m, uint64_t j) {
+    const uint64_t lo = j * n / m, hi = (j + 1) * n / m;
+#ifdef GDO_MUTANT_SAMPLE_WHOLE_SEGMENT
+    (void)lo;
+    (void)hi;
+    return a + gdo_splitmix64(seed, ((uint64_t)s << 32) | j) % n;  // mutant: ignores the strata
+#else
+    return a + lo + gdo_splitmix64(seed, ((uint64_t)s << 32) | j) % (hi - lo);
+#endif
+}
+
+// Algorithm 1 with the threshold selected on a sample (Section 4, R9).
+// Arguments as gdo_compress, without quantisation, plus sample_ppm (1..1e6)
+// and seed.  idx/val may be null when capacity is 0.  *out_k receives the
+// number of entries sent.  Returns 0 on success, 1 on bad arguments.
+int gdo_compress_sampled(const float* grad, const float* base, float* residual, const uint64_t* offsets,
+                         uint32_t T, double drop_ratio, int per_tensor, uint32_t sample_ppm, uint64_t seed,
+                         uint32_t* idx, float* val, uint32_t* tensor_counts, uint64_t capacity, uint64_t* out_k) {
+    if (!grad || !residual || !offsets || T == 0 || !tensor_counts) return 1;
+    if (capacity && (!idx || !val)) return 1;
+    if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return 1;
+    if (sample_ppm == 0 || sample_ppm > 1000000u) return 1;
+    const uint64_t N = offsets[T];
+    if (offsets[0] != 0 || N > 0xFFFFFFFFull) return 1;
+    for (uint32_t t = 0; t < T; ++t)
+        if (offsets[t + 1] < offsets[t]) return 1;
+    const uint64_t keep_ppm = gdo_keep_ppm(drop_ratio);
+
+    // Algorithm 1, first line: add the carried residual (pulls: delta first, R7).
+    std::vector<float> acc(N);
+    for (uint64_t i = 0; i < N; ++i) {
+        float g = grad[i];
+        if (base) g = g - base[i];
+        acc[i] = g + residual[i];
+    }
+
+    std::vector<std::pair<uint64_t, uint64_t>> seg;
+    if (per_tensor) {
+        for (uint32_t t = 0; t < T; ++t) seg.push_back({offsets[t], offsets[t + 1]});
+    } else {
+        seg.push_back({0, N});
+    }
+
+    // Section 4: the threshold from a selection on the sample; keep above it.
+    std::vector<uint8_t> keep(N, 0);
+    for (uint32_t s = 0; s < seg.size(); ++s) {
+        const uint64_t a = seg[s].first, n = seg[s].second - seg[s].first;
+        if (n == 0) continue;
+        const uint64_t m = (n * sample_ppm + 999999u) / 1000000u;
+        std::vector<uint32_t> skeys(m);
+        for (uint64_t j = 0; j < m; ++j) skeys[j] = key_of(acc[gdo_sample_position(seed, s, a, n, m, j)]);
+        const uint64_t km = m * keep_ppm / 1000000u;
+        if (keep_ppm == 0) continue;
+        if (km >= m) {
+            for (uint64_t i = a; i < a + n; ++i) keep[i] = 1;
+            continue;
+        }
+#ifdef GDO_MUTANT_SAMPLED_KTH
+        const uint64_t r = km ? km - 1 : 0;  // mutant: threshold at the k_m-th sample key
+#else
+        const uint64_t r = km;  // 0-based rank of the (k_m + 1)-th largest
+#endif
+        std::nth_element(skeys.begin(), skeys.begin() + r, skeys.end(), std::greater<uint32_t>());
+        const uint32_t thr = skeys[r];
+        for (uint64_t i = a; i < a + n; ++i) {
+#ifdef GDO_MUTANT_SAMPLED_GE
+            keep[i] = key_of(acc[i]) >= thr;  // mutant: keeps the threshold key too
+#else
+            keep[i] = key_of(acc[i]) > thr;
+#endif
+        }
+    }
+
+    // sparse(dropped) in ascending index, up to the capacity; the rest stays
+    // in the residual.
+    uint64_t j = 0;
+    for (uint32_t t = 0; t < T; ++t) tensor_counts[t] = 0;
+    for (uint32_t t = 0; t < T; ++t) {
+        for (uint64_t i = offsets[t]; i < offsets[t + 1]; ++i) {
+            if (!keep[i]) continue;
+#ifndef GDO_MUTANT_SAMPLED_NO_CAPACITY
+            if (j >= capacity) {
+                keep[i] = 0;
+                continue;
+            }
+#endif
+            if (j < capacity) {
+                idx[j] = (uint32_t)i;
+                val[j] = acc[i];
+            }
+            ++j;
+            ++tensor_counts[t];
+        }
+    }
+    if (out_k) *out_k = j;
+    for (uint64_t i = 0; i < N; ++i) residual[i] = keep[i] ? 0.0f : acc[i];
     return 0;
 }
 

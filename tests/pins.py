@@ -365,6 +365,146 @@ def pin_pull_delta(lib):
     check_invariants(acc, [0, 3000], 10_000, False, a.idx, a.val, a.residual, a.tensor_counts)
 
 
+# ---------------------------------------------------------------------------
+# sampled threshold (Section 4: selection on a 0.1% sample, keep above it)
+# ---------------------------------------------------------------------------
+
+SPLITMIX = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "splitmix64.json")
+
+
+def segments_of(offsets, per_tensor, N):
+    return [(offsets[t], offsets[t + 1]) for t in range(len(offsets) - 1)] if per_tensor else [(0, N)]
+
+
+def sampled_keep_brute(acc, offsets, keep_ppm, per_tensor, sample_ppm, seed, lib):
+    """Keep mask of the sampled mode: the sample's threshold by a full numpy sort.
+
+    Positions come from the oracle's generator (pinned separately against the
+    published SplitMix64 outputs and the stratum property); the selection on
+    the sample and the strict keep rule are recomputed here by brute force.
+    """
+    N = acc.size
+    kk = keys(acc)
+    keep = np.zeros(N, dtype=bool)
+    for s, (a, b) in enumerate(segments_of(offsets, per_tensor, N)):
+        n = b - a
+        if n == 0 or keep_ppm == 0:
+            continue
+        m = -(-n * sample_ppm // 1_000_000)
+        sk = np.sort(np.array([kk[oracle.sample_position(0 if seed is None else seed, s, a, n, m, j, lib=lib)]
+                               for j in range(m)], dtype=np.int64))[::-1]
+        km = m * keep_ppm // 1_000_000
+        if km >= m:
+            keep[a:b] = True
+        else:
+            keep[a:b] = kk[a:b] > sk[km]
+    return keep
+
+
+def pin_splitmix64_reference(lib):
+    """The position generator reproduces SplitMix64's published outputs."""
+    with open(SPLITMIX) as f:
+        gold = json.load(f)
+    for case in gold["cases"]:
+        got = [oracle.splitmix64(case["seed"], i, lib=lib) for i in range(len(case["outputs"]))]
+        assert got == [int(x) for x in case["outputs"]], (case["seed"], got)
+
+
+def pin_sample_positions(lib):
+    """One position per stratum [floor(j n/m), floor((j+1) n/m)); a full sample is every entry once."""
+    for (a, n, m, seed) in [(0, 1000, 10, 1), (17, 12345, 13, 2), (5, 7, 7, 3), (0, 100, 3, 4), (9, 2 ** 31, 4, 5)]:
+        pos = [oracle.sample_position(seed, 3, a, n, m, j, lib=lib) for j in range(m)]
+        for j, p in enumerate(pos):
+            assert a + j * n // m <= p < a + (j + 1) * n // m, (a, n, m, j, p)
+    pos = [oracle.sample_position(9, 0, 4, 50, 50, j, lib=lib) for j in range(50)]
+    assert pos == list(range(4, 54))
+    # the offsets within strata are spread, not a fixed column
+    pos = [oracle.sample_position(11, 0, 0, 100_000, 100, j, lib=lib) - j * 1000 for j in range(100)]
+    assert len(set(pos)) > 80
+
+
+def pin_sampled_full_sample_is_exact(lib):
+    """Every entry sampled and distinct magnitudes: the sampled mode keeps exactly the k largest."""
+    rng = np.random.default_rng(21)
+    offsets = [0, 3000, 3001, 7000, 7000, 10_000]
+    g = rng.permutation(np.arange(1, 10_001, dtype=np.float32)) * np.where(rng.random(10_000) < 0.5, -1, 1)
+    g = g.astype(np.float32)
+    r = np.zeros(10_000, np.float32)
+    for per in (False, True):
+        for drop in (0.99, 0.9, 0.5, 0.0, 1.0):
+            a = oracle.compress_sampled(g, r, offsets, drop, per_tensor=per, sample_ppm=1_000_000, seed=5, lib=lib)
+            keep = brute_keep(g, offsets, oracle.keep_ppm(drop, lib=lib), per)
+            assert np.array_equal(a.idx, np.nonzero(keep)[0].astype(np.uint32)), (per, drop)
+            assert np.array_equal(bits(a.residual), bits(np.where(keep, np.float32(0), g)))
+
+
+def pin_sampled_brute(lib):
+    """Partial samples with heavy ties: selection on the sample and the strict rule by full sort."""
+    rng = np.random.default_rng(22)
+    for trial in range(12):
+        T = int(rng.integers(1, 5))
+        sizes = rng.integers(0, 4000, T)
+        offsets = [0] + np.cumsum(sizes).tolist()
+        N = offsets[-1]
+        if N == 0:
+            continue
+        g = (rng.integers(-6, 7, N) * 0.25).astype(np.float32)
+        r = (rng.integers(-2, 3, N) * 0.125).astype(np.float32)
+        acc = g + r
+        per = bool(trial % 2)
+        ppm = int(rng.choice([2_000, 50_000, 300_000]))
+        drop = float(rng.choice([0.99, 0.9, 0.7]))
+        seed = int(rng.integers(0, 2 ** 63))
+        out = oracle.compress_sampled(g, r, offsets, drop, per_tensor=per, sample_ppm=ppm, seed=seed, lib=lib)
+        keep = sampled_keep_brute(acc, offsets, oracle.keep_ppm(drop, lib=lib), per, ppm, seed, lib)
+        assert np.array_equal(out.idx, np.nonzero(keep)[0].astype(np.uint32)), trial
+        assert np.array_equal(bits(out.val), bits(acc[keep]))
+        assert np.array_equal(bits(out.residual), bits(np.where(keep, np.float32(0), acc)))
+        assert list(out.tensor_counts) == [int(keep[offsets[t]:offsets[t + 1]].sum()) for t in range(T)]
+
+
+def pin_sampled_capacity(lib):
+    """A short output buffer sends the first entries; the rest stay in the residual."""
+    rng = np.random.default_rng(23)
+    offsets = [0, 40_000, 41_000, 100_000]
+    g = rng.normal(0, 1, 100_000).astype(np.float32)
+    r = rng.normal(0, 1, 100_000).astype(np.float32)
+    acc = g + r
+    full = oracle.compress_sampled(g, r, offsets, 0.99, per_tensor=False, sample_ppm=20_000, seed=3, lib=lib)
+    K = full.idx.size
+    assert K > 100
+    for cap in (0, 1, K // 3, K - 1, K, K + 5):
+        out = oracle.compress_sampled(g, r, offsets, 0.99, per_tensor=False, sample_ppm=20_000, seed=3,
+                                      capacity=cap, lib=lib)
+        c = min(cap, K)
+        assert np.array_equal(out.idx, full.idx[:c])
+        assert int(np.asarray(out.tensor_counts, np.int64).sum()) == c
+        sent = np.zeros(acc.size, bool)
+        sent[full.idx[:c]] = True
+        assert np.array_equal(bits(out.residual), bits(np.where(sent, np.float32(0), acc)))
+
+
+def pin_sampled_statistics(lib):
+    """On iid data the kept fraction tracks 1 - R; entries above the sample maximum when k_m = 0."""
+    rng = np.random.default_rng(24)
+    N = 2_000_000
+    g = rng.standard_t(3, N).astype(np.float32)
+    r = np.zeros(N, np.float32)
+    out = oracle.compress_sampled(g, r, [0, N], 0.99, sample_ppm=1000, seed=77, lib=lib)
+    # m = 2000 samples, k_m = 20: the kept fraction is Beta(m - 20, 21)-like, mean ~1.05%
+    assert 0.004 * N < out.idx.size < 0.02 * N, out.idx.size
+    kk = keys(g + r)
+    assert kk[out.idx].min() > kk[np.setdiff1d(np.arange(N), out.idx)].max()
+    # 50 samples at 1% keep: k_m = 0, the threshold is the largest sample key
+    n = 50_000
+    out = oracle.compress_sampled(g[:n], r[:n], [0, n], 0.99, sample_ppm=1000, seed=4, lib=lib)
+    smax = max(int(kk[oracle.sample_position(4, 0, 0, n, 50, j, lib=lib)]) for j in range(50))
+    assert np.array_equal(out.idx, np.nonzero(kk[:n] > smax)[0].astype(np.uint32))
+    # R = 1 keeps nothing, R = 0 keeps everything
+    assert oracle.compress_sampled(g[:n], r[:n], [0, n], 1.0, sample_ppm=1000, lib=lib).idx.size == 0
+    assert oracle.compress_sampled(g[:n], r[:n], [0, n], 0.0, sample_ppm=1000, lib=lib).idx.size == n
+
+
 ALL_PINS = [
     pin_keep_count,
     pin_golden_compress,
@@ -376,4 +516,10 @@ ALL_PINS = [
     pin_quant_exact,
     pin_apply_exact,
     pin_pull_delta,
+    pin_splitmix64_reference,
+    pin_sample_positions,
+    pin_sampled_full_sample_is_exact,
+    pin_sampled_brute,
+    pin_sampled_capacity,
+    pin_sampled_statistics,
 ]

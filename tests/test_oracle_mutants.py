@@ -24,6 +24,11 @@ MUTANTS = [
     "GDO_MUTANT_APPLY_REVERSE_CLIENTS",
     "GDO_MUTANT_APPLY_ADD",
     "GDO_MUTANT_DELTA_REVERSED",
+    "GDO_MUTANT_SAMPLED_KTH",
+    "GDO_MUTANT_SAMPLED_GE",
+    "GDO_MUTANT_SAMPLED_NO_CAPACITY",
+    "GDO_MUTANT_SPLITMIX_SHIFT",
+    "GDO_MUTANT_SAMPLE_WHOLE_SEGMENT",
 ]
 
 
