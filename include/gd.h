@@ -121,6 +121,37 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
                       void* stream);
 
 /*
+ * gd_compress_sampled - Algorithm 1 with the threshold selected on a sample,
+ * the paper's own selection (Section 4: sample 0.1% of the gradient and run
+ * the selection on the sample; Algorithm 1 keeps entries strictly above the
+ * threshold).  The number kept depends on the data.
+ *   grad, base, residual, drop_ratio, mode: as gd_compress.
+ *   sample_ppm (1..1000000): sample size per million entries of each threshold
+ *     segment (1000 = the paper's 0.1%).  A segment of n entries draws
+ *     m = ceil(n * sample_ppm / 1e6) positions, one in each stratum
+ *     [a + floor(j n / m), a + floor((j+1) n / m)) at the offset
+ *     u mod (stratum length), where u is output number 2^32 * s + j of
+ *     SplitMix64 (Steele, Lea and Flood, OOPSLA 2014) seeded with `seed`, s the
+ *     segment number and a its first index.
+ *   The threshold T is the (k_m + 1)-th largest |acc| of the m sampled entries,
+ *   k_m = floor(m * keep_ppm / 1e6) (the largest when k_m = 0); every entry
+ *   with |acc| > T is kept (as IEEE bit patterns with the sign cleared, the
+ *   order of gd_compress).  k_m >= m keeps every entry; drop_ratio 1 keeps none.
+ *   out: idx/val receive the kept entries in ascending index, at most
+ *     out->capacity of them (idx and val may be NULL when capacity is 0);
+ *     kept entries past the capacity are not sent and keep acc in the
+ *     residual.  tensor_counts[t] receives the entries of tensor t actually
+ *     sent; their sum is the output length.  sign_bits and means are ignored:
+ *     no quantisation in this mode.
+ *   residual (in/out): +0.0 at sent entries, acc elsewhere.
+ *   Returns GD_ERR_ARG for a bad sample_ppm or drop ratio, a NULL pointer or
+ *   a bad mode, GD_ERR_ALIGN as gd_compress; never GD_ERR_CAPACITY.
+ */
+gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base, float* residual,
+                              double drop_ratio, gd_threshold mode, uint32_t sample_ppm, uint64_t seed,
+                              const gd_sparse* out, void* stream);
+
+/*
  * gd_apply_sparse - server-side apply of sparse pushes to a parameter shard
  * (Section 3: servers own a shard and receive the clients' pieces).
  *   params (device, n floats, in/out).

@@ -65,6 +65,101 @@ void free_all(gd_ctx* ctx) {
     ctx->events.clear();
 }
 
+// The passes after the threshold bracket is set: the dense stream, the
+// candidate layout, exact selection or plain compaction, and quantisation.
+// k_total is the host-known output size (exact threshold) or 0 (sampled).
+gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, float* residual, bool per,
+                            uint32_t ppm, bool sampled, gd_quant quant, uint64_t k_total, const gd_sparse* out,
+                            hipStream_t st) {
+    const uint32_t* seg_off = per ? ctx->tab.tensor_off : ctx->tab.global_off;
+    gd::DenseArgs da{};
+    da.grad = grad;
+    da.base = base;
+    da.res = residual;
+    da.unit_info = ctx->tab.unit_info;
+    da.tensor_off = ctx->tab.tensor_off;
+    da.num_units = ctx->num_units;
+    da.N = (uint32_t)ctx->N;
+    da.T = ctx->T;
+    da.split = ctx->scr.split;
+    da.per_tensor = per;
+    da.seg = ctx->scr.seg;
+    da.slots = ctx->scr.slots;
+    da.cnt = ctx->scr.cnt;
+    const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_units > 0;
+    if (timed && hipEventRecord(ctx->events[ctx->events_used], st) != hipSuccess) return GD_ERR_HIP;
+    if (gd::launch_dense(da, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
+    if (timed) {
+        if (hipEventRecord(ctx->events[ctx->events_used + 1], st) != hipSuccess) return GD_ERR_HIP;
+        ctx->events_used += 2;
+    }
+    if (ctx->num_units > 0) ++ctx->dense_launches;
+
+    gd::CandArgs ca{};
+    ca.res = residual;
+    ca.unit_info = ctx->tab.unit_info;
+    ca.tensor_off = ctx->tab.tensor_off;
+    ca.seg_off = seg_off;
+    ca.num_units = ctx->num_units;
+    ca.N = (uint32_t)ctx->N;
+    ca.T = ctx->T;
+    ca.per_tensor = per;
+    ca.keep_ppm = ppm;
+    ca.seg = ctx->scr.seg;
+    ca.hist = ctx->scr.hist;
+    ca.slots = ctx->scr.slots;
+    ca.cnt = ctx->scr.cnt;
+    ca.split = ctx->scr.split;
+    ca.loc = ctx->scr.loc;
+    ca.neloc = ctx->scr.neloc;
+    ca.btot = ctx->scr.btot;
+    ca.betot = ctx->scr.betot;
+    ca.boff = ctx->scr.boff;
+    ca.beoff = ctx->scr.beoff;
+    ca.ne_unit = ctx->scr.ne_unit;
+    ca.ne_off = ctx->scr.ne_off;
+    ca.num_ne = ctx->scr.num_ne;
+    ca.raw_tbase = ctx->scr.raw_tbase;
+    ca.cand_idx = ctx->scr.cand_idx;
+    ca.cand_val = ctx->scr.cand_val;
+    ca.ten_cbase = ctx->scr.ten_cbase;
+    ca.tile_base = ctx->scr.tile_base;
+    ca.tile_ne0 = ctx->scr.tile_ne0;
+    ca.tile_tensor = ctx->scr.tile_tensor;
+    ca.flags = ctx->scr.flags;
+    ca.tile_gt = ctx->scr.tile_gt;
+    ca.tile_eq = ctx->scr.tile_eq;
+    ca.tile_q = ctx->scr.tile_q;
+    ca.out_base = ctx->scr.out_base;
+    ca.sampled = sampled ? 1u : 0u;
+    gd::EmitArgs ea{};
+    ea.idx = out->idx;
+    ea.val = out->val;
+    ea.tensor_counts = out->tensor_counts;
+    ea.capacity = out->capacity;
+    const bool q = quant == GD_QUANT_SIGN_MEAN;
+    if (gd::launch_layout(ca, st) != hipSuccess) return GD_ERR_HIP;
+    if (gd::launch_candidates(ca, ea, q, ctx->max_tiles, st) != hipSuccess) return GD_ERR_HIP;
+
+    if (q) {
+        gd::QuantArgs qa{};
+        qa.res = residual;
+        qa.idx = out->idx;
+        qa.val = out->val;
+        qa.sign_bits = out->sign_bits;
+        qa.means = out->means;
+        qa.tensor_counts = out->tensor_counts;
+        qa.tile_base = ctx->scr.tile_base;
+        qa.tile_q = ctx->scr.tile_q;
+        qa.qbase = ctx->scr.qbase;
+        qa.T = ctx->T;
+        qa.N = (uint32_t)ctx->N;
+        qa.k_total = k_total;
+        if (gd::launch_quant(qa, st) != hipSuccess) return GD_ERR_HIP;
+    }
+    return GD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -166,7 +261,8 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
          dev_alloc(ctx, &ctx->scr.flags, 4) && dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) &&
          dev_alloc(ctx, &ctx->scr.seg, S_max) && dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
          dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&
-         dev_alloc(ctx, &ctx->scr.qbase, T + 1) && dev_alloc(ctx, &ctx->scr.shist, (size_t)S_max * gd::kSHistWords);
+         dev_alloc(ctx, &ctx->scr.qbase, T + 1) && dev_alloc(ctx, &ctx->scr.shist, (size_t)S_max * gd::kSHistWords) &&
+         dev_alloc(ctx, &ctx->scr.sshist, (size_t)S_max * gd::kSsNB0);
     if (!ok) {
         free_all(ctx);
         delete ctx;
@@ -174,6 +270,7 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
     }
     if (hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
         hipMemset(ctx->scr.shist, 0, (size_t)S_max * gd::kSHistWords * sizeof(uint32_t)) != hipSuccess ||
+        hipMemset(ctx->scr.sshist, 0, (size_t)S_max * gd::kSsNB0 * sizeof(uint32_t)) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
         free_all(ctx);
         delete ctx;
@@ -228,91 +325,50 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     sa.tensor_counts = out->tensor_counts;
     if (gd::launch_sample(sa, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
 
-    gd::DenseArgs da{};
-    da.grad = grad;
-    da.base = base;
-    da.res = residual;
-    da.unit_info = ctx->tab.unit_info;
-    da.tensor_off = ctx->tab.tensor_off;
-    da.num_units = ctx->num_units;
-    da.N = (uint32_t)ctx->N;
-    da.T = ctx->T;
-    da.split = ctx->scr.split;
-    da.per_tensor = per;
-    da.seg = ctx->scr.seg;
-    da.slots = ctx->scr.slots;
-    da.cnt = ctx->scr.cnt;
-    const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_units > 0;
-    if (timed && hipEventRecord(ctx->events[ctx->events_used], st) != hipSuccess) return GD_ERR_HIP;
-    if (gd::launch_dense(da, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
-    if (timed) {
-        if (hipEventRecord(ctx->events[ctx->events_used + 1], st) != hipSuccess) return GD_ERR_HIP;
-        ctx->events_used += 2;
-    }
-    if (ctx->num_units > 0) ++ctx->dense_launches;
+    return run_after_bracket(ctx, grad, base, residual, per, ppm, false, quant, k_total, out, st);
+}
 
-    gd::CandArgs ca{};
-    ca.res = residual;
-    ca.unit_info = ctx->tab.unit_info;
-    ca.tensor_off = ctx->tab.tensor_off;
-    ca.seg_off = seg_off;
-    ca.num_units = ctx->num_units;
-    ca.N = (uint32_t)ctx->N;
-    ca.T = ctx->T;
-    ca.per_tensor = per;
-    ca.keep_ppm = ppm;
-    ca.seg = ctx->scr.seg;
-    ca.hist = ctx->scr.hist;
-    ca.slots = ctx->scr.slots;
-    ca.cnt = ctx->scr.cnt;
-    ca.split = ctx->scr.split;
-    ca.loc = ctx->scr.loc;
-    ca.neloc = ctx->scr.neloc;
-    ca.btot = ctx->scr.btot;
-    ca.betot = ctx->scr.betot;
-    ca.boff = ctx->scr.boff;
-    ca.beoff = ctx->scr.beoff;
-    ca.ne_unit = ctx->scr.ne_unit;
-    ca.ne_off = ctx->scr.ne_off;
-    ca.num_ne = ctx->scr.num_ne;
-    ca.raw_tbase = ctx->scr.raw_tbase;
-    ca.cand_idx = ctx->scr.cand_idx;
-    ca.cand_val = ctx->scr.cand_val;
-    ca.ten_cbase = ctx->scr.ten_cbase;
-    ca.tile_base = ctx->scr.tile_base;
-    ca.tile_ne0 = ctx->scr.tile_ne0;
-    ca.tile_tensor = ctx->scr.tile_tensor;
-    ca.flags = ctx->scr.flags;
-    ca.tile_gt = ctx->scr.tile_gt;
-    ca.tile_eq = ctx->scr.tile_eq;
-    ca.tile_q = ctx->scr.tile_q;
-    ca.out_base = ctx->scr.out_base;
-    gd::EmitArgs ea{};
-    ea.idx = out->idx;
-    ea.val = out->val;
-    ea.tensor_counts = out->tensor_counts;
-    ea.capacity = out->capacity;
-    const bool q = quant == GD_QUANT_SIGN_MEAN;
-    if (gd::launch_layout(ca, st) != hipSuccess) return GD_ERR_HIP;
-    if (gd::launch_candidates(ca, ea, q, ctx->max_tiles, st) != hipSuccess) return GD_ERR_HIP;
+gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base, float* residual,
+                              double drop_ratio, gd_threshold mode, uint32_t sample_ppm, uint64_t seed,
+                              const gd_sparse* out, void* stream) {
+    if (!ctx || !grad || !residual || !out) return GD_ERR_ARG;
+    if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
+    if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
+    if (sample_ppm == 0 || sample_ppm > 1000000u) return GD_ERR_ARG;
+    if (!out->tensor_counts || (out->capacity && (!out->idx || !out->val))) return GD_ERR_ARG;
+    if (!aligned16(grad) || !aligned16(residual) || (base && !aligned16(base))) return GD_ERR_ALIGN;
 
-    if (q) {
-        gd::QuantArgs qa{};
-        qa.res = residual;
-        qa.idx = out->idx;
-        qa.val = out->val;
-        qa.sign_bits = out->sign_bits;
-        qa.means = out->means;
-        qa.tensor_counts = out->tensor_counts;
-        qa.tile_base = ctx->scr.tile_base;
-        qa.tile_q = ctx->scr.tile_q;
-        qa.qbase = ctx->scr.qbase;
-        qa.T = ctx->T;
-        qa.N = (uint32_t)ctx->N;
-        qa.k_total = k_total;
-        if (gd::launch_quant(qa, st) != hipSuccess) return GD_ERR_HIP;
+    DeviceGuard guard(ctx->device);
+    if (!guard.ok) return GD_ERR_HIP;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool per = mode == GD_PER_TENSOR;
+    const uint32_t ppm = (uint32_t)keep_ppm_of(drop_ratio);
+    uint64_t max_n = 0;
+    if (per) {
+        for (uint32_t t = 0; t < ctx->T; ++t) max_n = std::max(max_n, ctx->offsets[t + 1] - ctx->offsets[t]);
+    } else {
+        max_n = ctx->N;
     }
-    return GD_OK;
+    const uint64_t max_samples = (max_n * sample_ppm + 999999u) / 1000000u;
+
+    gd::SampledArgs sa{};
+    sa.grad = grad;
+    sa.base = base;
+    sa.res = residual;
+    sa.seg_off = per ? ctx->tab.tensor_off : ctx->tab.global_off;
+    sa.S = per ? ctx->T : 1u;
+    sa.T = ctx->T;
+    sa.per_tensor = per;
+    sa.keep_ppm = ppm;
+    sa.sample_ppm = sample_ppm;
+    sa.seed = seed;
+    sa.skeys = ctx->scr.cand_idx;  // free until the candidate passes
+    sa.sshist = ctx->scr.sshist;
+    sa.seg = ctx->scr.seg;
+    sa.tensor_counts = out->tensor_counts;
+    if (gd::launch_sampled(sa, base != nullptr, (uint32_t)max_samples, st) != hipSuccess) return GD_ERR_HIP;
+
+    return run_after_bracket(ctx, grad, base, residual, per, ppm, true, GD_QUANT_NONE, 0, out, st);
 }
 
 gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const uint32_t* const* idx,

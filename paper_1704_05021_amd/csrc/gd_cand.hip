@@ -90,6 +90,7 @@ __device__ __forceinline__ void block_flush(const CandArgs& a, uint32_t* lh, con
                     sg[v] = kNoKey;
                 }
             }
+            if (a.sampled) continue;  // the threshold is already known
             uint32_t* g = seg_hist(a, sg[w], which) + 2 * i;
             if (sum & 0xFFFFu) atomicAdd(g, sum & 0xFFFFu);
             if (sum >> 16) atomicAdd(g + 1, sum >> 16);
@@ -333,6 +334,18 @@ __device__ __forceinline__ void phase_count(const CandArgs& a) {
         tile_setup(a, tile, v);
         uint32_t key[kRows];
         load_keys(a, v, key);
+        if (a.sampled) {
+            // the sampled threshold keeps every candidate
+            uint32_t c = 0;
+#pragma unroll
+            for (int r = 0; r < kRows; ++r) c += v.p0 + r * kWave + lane < v.p1;
+            c = wave_sum(c);
+            if (lane == 0) {
+                a.tile_gt[tile] = c;
+                a.tile_eq[tile] = 0;
+            }
+            continue;
+        }
         if (v.s != cached_s) {
             // digit 2 in two steps: its coarse bin, then the bin among 32
             const uint32_t p18 = a.seg[v.s].p18, r2 = a.seg[v.s].r2;
@@ -415,7 +428,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         }
         bg = wave_sum(bg);
         be = wave_sum(be);
-        const uint32_t be0 = be;
+        const uint32_t bg0 = bg, be0 = be;
         const uint64_t ob = a.out_base[v.s];
         double sp = 0.0, sn = 0.0;
         uint32_t np = 0, nn = 0;
@@ -423,17 +436,17 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         for (int r = 0; r < kRows; ++r) {
             const bool valid = v.p0 + r * kWave + lane < v.p1;
             const uint32_t key = vb[r] & 0x7FFFFFFFu;
-            const bool isgt = valid && key > thr;
-            const bool iseq = valid && key == thr;
+            const bool isgt = valid && (a.sampled || key > thr);
+            const bool iseq = valid && !a.sampled && key == thr;
             const uint64_t mg = ballot(isgt), me = ballot(iseq);
             const uint32_t G = bg + lanes_below(mg), E = be + lanes_below(me);
-            const bool kept = isgt || (iseq && E < need);
+            const uint64_t pos = ob + G + (E < need ? E : need);
+            // past the capacity (only possible under a sampled threshold) an
+            // entry is not sent and keeps acc in the residual
+            const bool kept = (isgt || (iseq && E < need)) && pos < o.capacity;
             if (kept) {
-                const uint64_t pos = ob + G + (E < need ? E : need);
-                if (pos < o.capacity) {
-                    o.idx[pos] = ix[r];
-                    o.val[pos] = __uint_as_float(vb[r]);
-                }
+                o.idx[pos] = ix[r];
+                o.val[pos] = __uint_as_float(vb[r]);
                 if (QUANT) {
                     const float x = __uint_as_float(vb[r]);
                     if (x < 0.0f) {
@@ -479,7 +492,10 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
                     run_e += __shfl(ie, kWave - 1, kWave);
                 }
             }
-            if (lane == 0) o.tensor_counts[v.t] = cnt;
+            // entries past the capacity are not sent
+            const uint64_t start = ob + bg0 + (be0 < need ? be0 : need);
+            const uint64_t room = o.capacity > start ? o.capacity - start : 0u;
+            if (lane == 0) o.tensor_counts[v.t] = (uint64_t)cnt < room ? cnt : (uint32_t)room;
         }
         if (QUANT) {
             sp = wave_sum(sp);
@@ -522,8 +538,10 @@ hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, u
     const uint32_t need = blocks_for_waves(max_tiles) ? blocks_for_waves(max_tiles) : 1u;
     const dim3 gt(need < kTileBlocks ? need : kTileBlocks);
     hipLaunchKernelGGL(k_gather, gt, b, 0, st, a);
-    hipLaunchKernelGGL(k_radix<1>, gt, b, 0, st, a);
-    hipLaunchKernelGGL(k_radix<2>, gt, b, 0, st, a);
+    if (!a.sampled) {  // a sampled threshold is already exact
+        hipLaunchKernelGGL(k_radix<1>, gt, b, 0, st, a);
+        hipLaunchKernelGGL(k_radix<2>, gt, b, 0, st, a);
+    }
     hipLaunchKernelGGL(k_count, gt, b, 0, st, a);
     if (quant) hipLaunchKernelGGL(k_emit<true>, gt, b, 0, st, a, o);
     else hipLaunchKernelGGL(k_emit<false>, gt, b, 0, st, a, o);

@@ -58,6 +58,18 @@ constexpr int kK16Shift = 15;           // key16 = key >> 15
 constexpr int kS0Shift = 6, kSNB1 = 64;
 constexpr int kSHistWords = 1024 + 2;  // per segment: digit histogram of the sample, valid and zero counts  // key16 digits: bits 15..6 (= key digit 0), bits 5..0
 
+// Sampled-threshold mode: sampler blocks of 1024 threads with 4 sample
+// positions each; a top digit of 11 key bits (2048 bins); the selection block
+// gathers up to 8192 keys sharing it into LDS, loading 8 keys per thread at a
+// time.
+constexpr int kSsThreads = 1024;
+constexpr int kSsPerThread = 4;
+constexpr int kSsNB0 = 2048;
+constexpr int kSsD0Shift = 20;
+constexpr int kSsSelThreads = 1024;
+constexpr int kSsList = 8192;
+constexpr int kSsBatch = 8;
+
 // Elements per unit of the dense pass (one block).
 constexpr uint32_t kUnitLen = 1024;
 // Units per block of the candidate-count scan.

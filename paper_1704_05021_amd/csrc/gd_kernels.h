@@ -32,6 +32,24 @@ struct SampleArgs {
     uint32_t* tensor_counts;
 };
 
+// Sampled-threshold mode (Section 4: selection on a sample of the gradient).
+struct SampledArgs {
+    const float* grad;
+    const float* base;  // nullable
+    const float* res;
+    const uint32_t* seg_off;  // [S + 1]
+    uint32_t S;
+    uint32_t T;
+    uint32_t per_tensor;
+    uint32_t keep_ppm;
+    uint32_t sample_ppm;  // 1 .. 1e6
+    uint64_t seed;
+    uint32_t* skeys;   // [N] sample keys of segment s at [seg_off[s], ...)
+    uint32_t* sshist;  // [S * kSsNB0] top-digit histogram, zero on entry; k_sselect clears it again
+    SegState* seg;
+    uint32_t* tensor_counts;
+};
+
 struct DenseArgs {
     const float* grad;
     const float* base;  // nullable
@@ -85,8 +103,9 @@ struct CandArgs {
     uint32_t* tile_gt;    // [max tiles]
     uint32_t* tile_eq;
     double* tile_q;       // [max tiles * 4]
-    const uint64_t* out_base;
+    uint64_t* out_base;   // [S] first output slot of each segment (the sampled mode writes it here)
     uint32_t* flags;      // [0]: some segment missed its bracket
+    uint32_t sampled;     // sampled threshold: every candidate is kept, no bracket can miss
 };
 
 struct EmitArgs {
@@ -124,6 +143,7 @@ struct ApplyArgs {
 };
 
 hipError_t launch_sample(const SampleArgs& a, bool has_base, hipStream_t st);
+hipError_t launch_sampled(const SampledArgs& a, bool has_base, uint32_t max_samples, hipStream_t st);
 hipError_t launch_layout(const CandArgs& a, hipStream_t st);
 hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st);
 hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles, hipStream_t st);

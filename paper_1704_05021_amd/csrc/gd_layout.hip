@@ -4,7 +4,9 @@
 //              counts.
 //   k_scan_final : one block scans the block totals and derives, per
 //              threshold segment, the candidate total and
-//              whether the bracket missed (fewer than k candidates), and per
+//              whether the bracket missed (fewer than k candidates; under a
+//              sampled threshold, where every candidate is sent, the first
+//              output slot instead), and per
 //              tensor the first candidate in dense-pass order, the first
 //              compact candidate and the first tile (tiles of kTile
 //              candidates never cross a tensor).  A tensor of a missed
@@ -107,13 +109,26 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
         const uint32_t n = a.seg_off[s + 1] - a.seg_off[s];
         const uint32_t k = keep_of(n, a.keep_ppm);
         const uint32_t cnt = a.per_tensor ? a.raw_tbase[s + 1] - a.raw_tbase[s] : grand;
-        const uint32_t miss = (k > 0 && cnt < k) ? 1u : 0u;
+        const uint32_t miss = (!a.sampled && k > 0 && cnt < k) ? 1u : 0u;
         a.seg[s].clo = cnt;
         a.seg[s].miss = miss;
         if (miss) atomicOr(&any_miss, 1u);
     }
     __threadfence_block();
     __syncthreads();
+    if (a.sampled) {
+        // every candidate is sent: segment s starts after the candidates of
+        // the segments before it
+        uint64_t carry = 0;
+        for (uint32_t b0 = 0; b0 < S; b0 += kScanThreads) {
+            const uint32_t s = b0 + tid;
+            const uint32_t c = s < S ? (a.per_tensor ? a.raw_tbase[s + 1] - a.raw_tbase[s] : grand) : 0u;
+            uint32_t tot;
+            const uint32_t e = block_excl_scan<kScanThreads>(c, lds, &tot);
+            if (s < S) a.out_base[s] = carry + e;
+            carry += tot;
+        }
+    }
     uint32_t ccarry = 0, tcarry = 0;
     for (uint32_t b0 = 0; b0 < a.T; b0 += kScanThreads) {
         const uint32_t t = b0 + tid;
