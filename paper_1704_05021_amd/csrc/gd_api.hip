@@ -262,7 +262,7 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
          dev_alloc(ctx, &ctx->scr.seg, S_max) && dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
          dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&
          dev_alloc(ctx, &ctx->scr.qbase, T + 1) && dev_alloc(ctx, &ctx->scr.shist, (size_t)S_max * gd::kSHistWords) &&
-         dev_alloc(ctx, &ctx->scr.sshist, (size_t)S_max * gd::kSsNB0);
+         dev_alloc(ctx, &ctx->scr.sshist, (size_t)S_max * gd::kSsCopies * gd::kSsNB0);
     if (!ok) {
         free_all(ctx);
         delete ctx;
@@ -270,7 +270,7 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
     }
     if (hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
         hipMemset(ctx->scr.shist, 0, (size_t)S_max * gd::kSHistWords * sizeof(uint32_t)) != hipSuccess ||
-        hipMemset(ctx->scr.sshist, 0, (size_t)S_max * gd::kSsNB0 * sizeof(uint32_t)) != hipSuccess ||
+        hipMemset(ctx->scr.sshist, 0, (size_t)S_max * gd::kSsCopies * gd::kSsNB0 * sizeof(uint32_t)) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
         free_all(ctx);
         delete ctx;

@@ -58,11 +58,13 @@ constexpr int kK16Shift = 15;           // key16 = key >> 15
 constexpr int kS0Shift = 6, kSNB1 = 64;
 constexpr int kSHistWords = 1024 + 2;  // per segment: digit histogram of the sample, valid and zero counts  // key16 digits: bits 15..6 (= key digit 0), bits 5..0
 
-// Sampled-threshold mode: sampler blocks of 1024 threads with 4 sample
-// positions each; a top digit of 11 key bits (2048 bins); the selection block
-// gathers up to 8192 keys sharing it into LDS, loading 8 keys per thread at a
-// time.
-constexpr int kSsThreads = 1024;
+// Sampled-threshold mode: sampler blocks of 256 threads with 4 sample
+// positions each; a top digit of 11 key bits (2048 bins), counted into one of
+// 8 copies of the segment histogram by block number, so that blocks adding to
+// the same hot bin rarely meet; the selection block gathers up to 8192 keys
+// sharing the digit into LDS, loading 8 keys per thread at a time.
+constexpr int kSsThreads = 256;
+constexpr int kSsCopies = 8;
 constexpr int kSsPerThread = 4;
 constexpr int kSsNB0 = 2048;
 constexpr int kSsD0Shift = 20;

@@ -53,7 +53,7 @@ struct Scratch {
     uint16_t* skeys = nullptr;       // 16-bit sample keys
     uint32_t* shist = nullptr;       // [S_max * kSHistWords] sample histograms, kept zero between calls
     uint32_t* qbase = nullptr;       // [T + 1] first output slot of each tensor
-    uint32_t* sshist = nullptr;      // [S_max * kSsNB0] sampled mode: top-digit histogram of the sample keys
+    uint32_t* sshist = nullptr;      // [S_max * kSsCopies * kSsNB0] sampled mode: top-digit histograms
 };
 
 }  // namespace gd

@@ -45,7 +45,7 @@ struct SampledArgs {
     uint32_t sample_ppm;  // 1 .. 1e6
     uint64_t seed;
     uint32_t* skeys;   // [N] sample keys of segment s at [seg_off[s], ...)
-    uint32_t* sshist;  // [S * kSsNB0] top-digit histogram, zero on entry; k_sselect clears it again
+    uint32_t* sshist;  // [S * kSsCopies * kSsNB0] top-digit histograms, zero on entry; k_sselect clears them
     SegState* seg;
     uint32_t* tensor_counts;
 };

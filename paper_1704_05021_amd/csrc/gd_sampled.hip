@@ -9,8 +9,8 @@
 //               at the offset given by output 2^32 s + j of SplitMix64 seeded
 //               by the caller (Steele, Lea and Flood, OOPSLA 2014), stores the
 //               key of acc at each position and adds the keys' top 11 bits to
-//               the segment's histogram (large blocks, so few global adds per
-//               bin).  It also clears the per-tensor counts and the segment's
+//               the segment's histogram (one of several copies by block
+//               number, so few global adds meet on a bin).  It also clears the per-tensor counts and the segment's
 //               candidate state.
 //   k_sselect : one block per segment takes the (k_m + 1)-th largest sample key
 //               T (k_m = floor(m * keep_ppm / 1e6); the largest when k_m = 0):
@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kSsThreads) void k_ssample(SampledArgs a) {
         lds_hist_add(h, key[q] >> kSsD0Shift, ok[q]);
     }
     __syncthreads();
-    uint32_t* gh = a.sshist + (size_t)s * kSsNB0;
+    uint32_t* gh = a.sshist + ((size_t)s * kSsCopies + blockIdx.x % kSsCopies) * kSsNB0;
     for (int i = tid; i < kSsNB0; i += kSsThreads)
         if (h[i]) atomicAdd(&gh[i], h[i]);
 }
@@ -139,10 +139,17 @@ __global__ __launch_bounds__(kSsSelThreads) void k_sselect(SampledArgs a) {
     __shared__ uint32_t list[kSsList];
     __shared__ uint32_t scan_lds[kSsSelThreads / kWave + 1];
     __shared__ uint32_t par[3];
-    uint32_t* gh = a.sshist + (size_t)s * kSsNB0;
+    uint32_t* gh = a.sshist + (size_t)s * kSsCopies * kSsNB0;
     for (int i = tid; i < kSsNB0; i += kSsSelThreads) {
-        h[i] = gh[i];
-        gh[i] = 0;  // ready for the next call
+        uint32_t c[kSsCopies], sum = 0;
+#pragma unroll
+        for (int q = 0; q < kSsCopies; ++q) c[q] = gh[q * kSsNB0 + i];
+#pragma unroll
+        for (int q = 0; q < kSsCopies; ++q) {
+            sum += c[q];
+            gh[q * kSsNB0 + i] = 0;  // ready for the next call
+        }
+        h[i] = sum;
     }
     if (tid == 0) par[0] = par[1] = par[2] = 0;
     __syncthreads();
