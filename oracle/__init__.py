@@ -45,7 +45,8 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.gdo_keep_ppm.restype = u64
     lib.gdo_keep_count.argtypes = [u64, dbl]
     lib.gdo_keep_count.restype = u64
-    lib.gdo_compress.argtypes = [vp, vp, vp, vp, u32, dbl, i32, i32, vp, vp, vp, vp, vp, u64, ctypes.POINTER(u64)]
+    lib.gdo_compress.argtypes = [vp, vp, vp, vp, u32, dbl, i32, i32, vp, vp, vp, vp, vp, u64, ctypes.POINTER(u64),
+                                 vp]
     lib.gdo_compress.restype = i32
     lib.gdo_apply_sparse.argtypes = [vp, u64, u32, vp, vp, vp, f32]
     lib.gdo_apply_sparse.restype = i32
@@ -107,11 +108,16 @@ def compress(
     offsets: Sequence[int],
     drop_ratio: float = 0.99,
     per_tensor: bool = False,
-    quant: bool = False,
+    quant=False,
     base: Optional[np.ndarray] = None,
     lib: Optional[ctypes.CDLL] = None,
+    columns: Optional[Sequence[int]] = None,
 ) -> Compressed:
-    """One call of Algorithm 1 over the layout ``offsets``; inputs are not modified."""
+    """One call of Algorithm 1 over the layout ``offsets``; inputs are not modified.
+
+    quant: False/0 none, True/1 per-tensor sign mean, 2 threshold, 3 global
+    average, 4 column-wise average over the matrices ``columns`` describes.
+    """
     lib = lib or load()
     g = np.ascontiguousarray(grad, dtype=np.float32)
     r = np.array(residual, dtype=np.float32, copy=True)
@@ -123,11 +129,15 @@ def compress(
     idx = np.zeros(max(cap, 1), np.uint32)
     val = np.zeros(max(cap, 1), np.float32)
     counts = np.zeros(T, np.uint32)
+    quant = int(quant)
+    cols = None if columns is None else np.ascontiguousarray(columns, dtype=np.uint32)
+    groups = int(cols.astype(np.int64).sum()) if (quant == 4 and cols is not None) else T
     bits = np.zeros(max((cap + 31) // 32, 1), np.uint32) if quant else None
-    means = np.zeros(2 * T, np.float32) if quant else None
+    means = np.zeros(2 * groups, np.float32) if quant else None
     k = ctypes.c_uint64(0)
-    rc = lib.gdo_compress(_ptr(g), _ptr(b), _ptr(r), _ptr(off), T, float(drop_ratio), int(per_tensor), int(quant),
-                          _ptr(idx), _ptr(val), _ptr(bits), _ptr(means), _ptr(counts), cap, ctypes.byref(k))
+    rc = lib.gdo_compress(_ptr(g), _ptr(b), _ptr(r), _ptr(off), T, float(drop_ratio), int(per_tensor), quant,
+                          _ptr(idx), _ptr(val), _ptr(bits), _ptr(means), _ptr(counts), cap, ctypes.byref(k),
+                          _ptr(cols))
     if rc != 0:
         raise ValueError(f"gdo_compress failed with status {rc}")
     k = int(k.value)

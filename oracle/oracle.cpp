@@ -38,6 +38,17 @@
 //   R6  server apply: s[i] = sum of the pushed values at i in client order
 //       (float adds starting from +0.0f), then p[i] = p[i] - lr * s[i].
 //   R7  pull delta: acc = (p_new - p_last) + residual, two float roundings.
+//   R10 the other centres Section 5.4 tests, over the same kept set and with
+//       the same sign bits and error feedback as R5:
+//       threshold (quant 2): every survivor maps to +-T_s, T_s the smallest
+//         kept |acc| of its threshold segment (0 when the segment keeps none);
+//       global average (quant 3): one positive and one negative average over
+//         every kept entry of the call, the same pair for every tensor;
+//       column-wise average (quant 4): tensor t is a row-major matrix of
+//         columns[t] columns (columns[t] divides its size); each column's kept
+//         positives and negatives are averaged separately, pairs stored for
+//         the columns of tensor 0, then tensor 1, ... (columns NULL: one
+//         column per tensor, which is R5).
 //   R9  sampled threshold (Section 4: select on a 0.1% sample of the
 //       gradient, then keep what lies strictly above the threshold):
 //       segment s of n entries draws m = ceil(n * sample_ppm / 1e6)
@@ -95,19 +106,27 @@ uint64_t gdo_keep_count(uint64_t n, double drop_ratio) {
 // Algorithm 1 over the tensors described by offsets[0..T] (offsets[T] = N).
 // grad, base (nullable), residual: length N.  residual is read and rewritten.
 // Outputs (caller-allocated, capacity entries): idx, val; sign_bits
-// (ceil(capacity/32) words) and means (2*T) when quant != 0; tensor_counts (T).
+// (ceil(capacity/32) words) and means (2*T, or 2 * sum of columns for quant 4)
+// when quant != 0; tensor_counts (T).  quant: 0 none, 1 per-tensor sign mean
+// (R5), 2 threshold, 3 global average, 4 column-wise average (R10); columns
+// (T entries, nullable) describes the matrices for quant 4.
 // Returns 0 on success, 1 on bad arguments, 3 when capacity is too small.
 int gdo_compress(const float* grad, const float* base, float* residual, const uint64_t* offsets,
                  uint32_t T, double drop_ratio, int per_tensor, int quant, uint32_t* idx, float* val,
                  uint32_t* sign_bits, float* means, uint32_t* tensor_counts, uint64_t capacity,
-                 uint64_t* out_k) {
+                 uint64_t* out_k, const uint32_t* columns) {
     if (!grad || !residual || !offsets || T == 0 || !idx || !val || !tensor_counts) return 1;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return 1;
+    if (quant < 0 || quant > 4) return 1;
     if (quant && (!sign_bits || !means)) return 1;
     const uint64_t N = offsets[T];
     if (offsets[0] != 0 || N > 0xFFFFFFFFull) return 1;
     for (uint32_t t = 0; t < T; ++t)
         if (offsets[t + 1] < offsets[t]) return 1;
+    if (quant == 4 && columns) {
+        for (uint32_t t = 0; t < T; ++t)
+            if (columns[t] == 0 || (offsets[t + 1] - offsets[t]) % columns[t] != 0) return 1;
+    }
 
     // Segments over which one threshold is chosen (Section 4: global or local).
     std::vector<std::pair<uint64_t, uint64_t>> seg;
@@ -200,44 +219,133 @@ int gdo_compress(const float* grad, const float* base, float* residual, const ui
 #endif
     }
 
-    // Section 5.4, sign-mean 1-bit quantisation with error feedback (R5).
+    // Section 5.4, 1-bit quantisation with error feedback (R5, R10): each
+    // kept entry is sent as the centre of its group and sign, and acc minus
+    // that centre goes back into the residual.
     if (quant) {
         const uint64_t words = (k_total + 31) / 32;
         for (uint64_t w = 0; w < words; ++w) sign_bits[w] = 0;
-        uint64_t first = 0;  // first output slot of tensor t
-        for (uint32_t t = 0; t < T; ++t) {
-            const uint64_t last = first + tensor_counts[t];
-            double pos_sum = 0.0, neg_sum = 0.0;
-            uint64_t pos_n = 0, neg_n = 0;
-            for (uint64_t q = first; q < last; ++q) {
-                if (val[q] < 0.0f) {
-                    neg_sum += (double)val[q];
-                    ++neg_n;
-                } else {
-                    pos_sum += (double)val[q];
-                    ++pos_n;
+        // group of every output slot: its tensor, or its column for quant 4
+        std::vector<uint64_t> colbase(T + 1, 0);
+        for (uint32_t t = 0; t < T; ++t) colbase[t + 1] = colbase[t] + (quant == 4 && columns ? columns[t] : 1);
+        std::vector<uint64_t> group(k_total);
+        {
+            uint64_t q = 0;
+            for (uint32_t t = 0; t < T; ++t) {
+                for (uint32_t c = 0; c < tensor_counts[t]; ++c, ++q) {
+                    uint64_t g = t;
+                    if (quant == 4) {
+                        const uint64_t cols = columns ? columns[t] : 1;
+#ifdef GDO_MUTANT_COLUMN_IS_ROW
+                        g = colbase[t] + ((idx[q] - offsets[t]) / cols) % cols;  // mutant: rows, not columns
+#else
+                        g = colbase[t] + (idx[q] - offsets[t]) % cols;
+#endif
+                    }
+                    group[q] = g;
                 }
             }
-            const float pos_c = pos_n ? (float)(pos_sum / (double)pos_n) : 0.0f;
-            const float neg_c = neg_n ? (float)(neg_sum / (double)neg_n) : 0.0f;
-#ifdef GDO_MUTANT_SWAP_CENTRES
-            means[2 * t + 0] = neg_c;
-            means[2 * t + 1] = pos_c;
-#else
-            means[2 * t + 0] = pos_c;
-            means[2 * t + 1] = neg_c;
-#endif
-            for (uint64_t q = first; q < last; ++q) {
-                const bool neg = val[q] < 0.0f;
-#ifdef GDO_MUTANT_BITS_MSB_FIRST
-                if (neg) sign_bits[q >> 5] |= 1u << (31 - (q & 31));
-#else
-                if (neg) sign_bits[q >> 5] |= 1u << (q & 31);
-#endif
-                const float sent = neg ? means[2 * t + 1] : means[2 * t + 0];
-                residual[idx[q]] = val[q] - sent;
+        }
+        const uint64_t G = quant == 4 ? colbase[T] : T;
+        std::vector<float> pos_c(G, 0.0f), neg_c(G, 0.0f);
+        if (quant == 1 || quant == 4) {
+            // averages per group, summed in double in ascending index
+            std::vector<double> ps(G, 0.0), ns(G, 0.0);
+            std::vector<uint64_t> pn(G, 0), nn(G, 0);
+            for (uint64_t q = 0; q < k_total; ++q) {
+                if (val[q] < 0.0f) {
+                    ns[group[q]] += (double)val[q];
+                    ++nn[group[q]];
+                } else {
+                    ps[group[q]] += (double)val[q];
+                    ++pn[group[q]];
+                }
             }
-            first = last;
+            for (uint64_t g = 0; g < G; ++g) {
+                pos_c[g] = pn[g] ? (float)(ps[g] / (double)pn[g]) : 0.0f;
+                neg_c[g] = nn[g] ? (float)(ns[g] / (double)nn[g]) : 0.0f;
+            }
+        } else if (quant == 3) {
+            // one average of each sign over the whole call
+            double ps = 0.0, ns = 0.0;
+            uint64_t pn = 0, nn = 0;
+            for (uint64_t q = 0; q < k_total; ++q) {
+                if (val[q] < 0.0f) {
+                    ns += (double)val[q];
+                    ++nn;
+                } else {
+                    ps += (double)val[q];
+                    ++pn;
+                }
+            }
+            const float pc = pn ? (float)(ps / (double)pn) : 0.0f;
+            const float nc = nn ? (float)(ns / (double)nn) : 0.0f;
+            for (uint64_t g = 0; g < G; ++g) {
+#ifdef GDO_MUTANT_GLOBAL_MEAN_PER_TENSOR
+                (void)pc;
+                (void)nc;
+#else
+                pos_c[g] = pc;
+                neg_c[g] = nc;
+#endif
+            }
+#ifdef GDO_MUTANT_GLOBAL_MEAN_PER_TENSOR
+            // mutant: per-tensor averages instead of one over the call
+            std::vector<double> ps2(G, 0.0), ns2(G, 0.0);
+            std::vector<uint64_t> pn2(G, 0), nn2(G, 0);
+            for (uint64_t q = 0; q < k_total; ++q) {
+                if (val[q] < 0.0f) { ns2[group[q]] += val[q]; ++nn2[group[q]]; }
+                else { ps2[group[q]] += val[q]; ++pn2[group[q]]; }
+            }
+            for (uint64_t g = 0; g < G; ++g) {
+                pos_c[g] = pn2[g] ? (float)(ps2[g] / (double)pn2[g]) : 0.0f;
+                neg_c[g] = nn2[g] ? (float)(ns2[g] / (double)nn2[g]) : 0.0f;
+            }
+#endif
+        } else {
+            // quant 2: the smallest kept magnitude of each threshold segment
+            std::vector<uint32_t> seg_min(seg.size(), 0xFFFFFFFFu);
+            std::vector<uint8_t> seg_any(seg.size(), 0);
+            uint64_t q = 0;
+            for (uint32_t t = 0; t < T; ++t) {
+                const uint32_t sg = per_tensor ? t : 0u;
+                for (uint32_t c = 0; c < tensor_counts[t]; ++c, ++q) {
+                    const uint32_t kk = key_of(val[q]);
+#ifdef GDO_MUTANT_THRESHOLD_MAX
+                    if (!seg_any[sg] || kk > seg_min[sg]) seg_min[sg] = kk;  // mutant: the largest instead
+#else
+                    if (!seg_any[sg] || kk < seg_min[sg]) seg_min[sg] = kk;
+#endif
+                    seg_any[sg] = 1;
+                }
+            }
+            for (uint32_t t = 0; t < T; ++t) {
+                const uint32_t sg = per_tensor ? t : 0u;
+                if (!seg_any[sg]) continue;
+                float mag;
+                std::memcpy(&mag, &seg_min[sg], sizeof mag);
+                pos_c[t] = mag;
+                neg_c[t] = -mag;
+            }
+        }
+        for (uint64_t g = 0; g < G; ++g) {
+#ifdef GDO_MUTANT_SWAP_CENTRES
+            means[2 * g + 0] = neg_c[g];
+            means[2 * g + 1] = pos_c[g];
+#else
+            means[2 * g + 0] = pos_c[g];
+            means[2 * g + 1] = neg_c[g];
+#endif
+        }
+        for (uint64_t q = 0; q < k_total; ++q) {
+            const bool neg = val[q] < 0.0f;
+#ifdef GDO_MUTANT_BITS_MSB_FIRST
+            if (neg) sign_bits[q >> 5] |= 1u << (31 - (q & 31));
+#else
+            if (neg) sign_bits[q >> 5] |= 1u << (q & 31);
+#endif
+            const float sent = neg ? means[2 * group[q] + 1] : means[2 * group[q] + 0];
+            residual[idx[q]] = val[q] - sent;
         }
     }
     return 0;

@@ -315,6 +315,97 @@ def pin_quant_exact(lib):
         assert np.array_equal(bits(out.residual[dropped]), bits(acc[dropped]))
 
 
+def _check_sign_bits(out, k):
+    for q in range(k):
+        bit = (int(out.sign_bits[q >> 5]) >> (q & 31)) & 1
+        assert bit == int(bool(out.val[q] < 0))
+    if k % 32:
+        assert int(out.sign_bits[-1]) >> (k % 32) == 0
+
+
+def _exact_avg(vals):
+    return sum(Fraction(float(x)) for x in vals) / len(vals)
+
+
+def pin_quant_other_centres(lib):
+    """Threshold, global-average and column-wise centres (Section 5.4) against exact arithmetic."""
+    rng = np.random.default_rng(12)
+    offsets = [0, 700, 701, 1500, 1500, 2600]
+    columns = [7, 1, 17, 3, 11]  # each divides its tensor's size (799 = 17 * 47)
+    T, N = len(offsets) - 1, offsets[-1]
+    tensor_of = np.searchsorted(np.array(offsets[1:]), np.arange(N), side="right")
+    for trial in range(6):
+        g = (rng.standard_t(3, N) * 10.0 ** rng.uniform(-4, 0)).astype(np.float32)
+        r = rng.normal(0, 1e-3, N).astype(np.float32)
+        acc = g + r
+        per = bool(trial % 2)
+        # threshold: +-(smallest kept magnitude of the segment)
+        out = oracle.compress(g, r, offsets, 0.9, per_tensor=per, quant=2, lib=lib)
+        k = out.idx.size
+        _check_sign_bits(out, k)
+        kt = tensor_of[out.idx]
+        for t in range(T):
+            seg = (kt == t) if per else np.ones(k, bool)
+            if seg.any():
+                tmag = np.min(np.abs(out.val[seg]))
+                assert bits([out.means[2 * t]])[0] == bits([tmag])[0]
+                assert bits([out.means[2 * t + 1]])[0] == bits([-tmag])[0]
+            else:
+                assert bits(out.means[2 * t:2 * t + 2]).tolist() == [0, 0]
+        for q in range(k):
+            c = out.means[2 * kt[q] + int(out.val[q] < 0)]
+            assert within_half_ulp(out.residual[out.idx[q]], Fraction(float(out.val[q])) - Fraction(float(c)))
+        # global average: one pair over every kept entry
+        out = oracle.compress(g, r, offsets, 0.9, per_tensor=per, quant=3, lib=lib)
+        k = out.idx.size
+        _check_sign_bits(out, k)
+        pos = [x for x in out.val if not (x < 0)]
+        neg = [x for x in out.val if x < 0]
+        for t in range(T):
+            mp, mn = out.means[2 * t], out.means[2 * t + 1]
+            assert within_half_ulp(mp, _exact_avg(pos)) if pos else bits([mp])[0] == 0
+            assert within_half_ulp(mn, _exact_avg(neg)) if neg else bits([mn])[0] == 0
+        assert np.all(bits(out.means[0::2]) == bits(out.means[0])) and np.all(bits(out.means[1::2]) == bits(out.means[1]))
+        # column-wise average
+        out = oracle.compress(g, r, offsets, 0.9, per_tensor=per, quant=4, columns=columns, lib=lib)
+        k = out.idx.size
+        _check_sign_bits(out, k)
+        colbase = np.concatenate([[0], np.cumsum(columns)])
+        assert out.means.size == 2 * colbase[-1]
+        col = np.array([colbase[t] + (int(i) - offsets[t]) % columns[t] for i, t in zip(out.idx, tensor_of[out.idx])],
+                       dtype=np.int64)
+        for c in range(colbase[-1]):
+            v = out.val[col == c]
+            pos = [x for x in v if not (x < 0)]
+            neg = [x for x in v if x < 0]
+            mp, mn = out.means[2 * c], out.means[2 * c + 1]
+            assert within_half_ulp(mp, _exact_avg(pos)) if pos else bits([mp])[0] == 0
+            assert within_half_ulp(mn, _exact_avg(neg)) if neg else bits([mn])[0] == 0
+        for q in range(k):
+            cq = out.means[2 * col[q] + int(out.val[q] < 0)]
+            assert within_half_ulp(out.residual[out.idx[q]], Fraction(float(out.val[q])) - Fraction(float(cq)))
+        dropped = np.ones(N, bool)
+        dropped[out.idx] = False
+        assert np.array_equal(bits(out.residual[dropped]), bits(acc[dropped]))
+
+
+def pin_quant_column_limits(lib):
+    """One column per tensor is the per-tensor sign mean; one column per entry sends every value exactly."""
+    rng = np.random.default_rng(13)
+    offsets = [0, 900, 960, 2000]
+    N = offsets[-1]
+    g = rng.normal(0, 1, N).astype(np.float32)
+    r = rng.normal(0, 0.1, N).astype(np.float32)
+    for per in (False, True):
+        a = oracle.compress(g, r, offsets, 0.95, per_tensor=per, quant=1, lib=lib)
+        b = oracle.compress(g, r, offsets, 0.95, per_tensor=per, quant=4, columns=[1, 1, 1], lib=lib)
+        assert np.array_equal(bits(a.means), bits(b.means)) and np.array_equal(bits(a.residual), bits(b.residual))
+        sizes = [offsets[t + 1] - offsets[t] for t in range(3)]
+        c = oracle.compress(g, r, offsets, 0.95, per_tensor=per, quant=4, columns=sizes, lib=lib)
+        assert np.all(bits(c.residual[c.idx]) == 0), "a column of one kept value sends it exactly"
+        assert np.array_equal(bits(c.val), bits((g + r)[c.idx]))
+
+
 def pin_apply_exact(lib):
     rng = np.random.default_rng(5)
     n = 5000
@@ -514,6 +605,8 @@ ALL_PINS = [
     pin_invariants_large,
     pin_special_cases,
     pin_quant_exact,
+    pin_quant_other_centres,
+    pin_quant_column_limits,
     pin_apply_exact,
     pin_pull_delta,
     pin_splitmix64_reference,

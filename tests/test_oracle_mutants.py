@@ -29,6 +29,9 @@ MUTANTS = [
     "GDO_MUTANT_SAMPLED_NO_CAPACITY",
     "GDO_MUTANT_SPLITMIX_SHIFT",
     "GDO_MUTANT_SAMPLE_WHOLE_SEGMENT",
+    "GDO_MUTANT_THRESHOLD_MAX",
+    "GDO_MUTANT_GLOBAL_MEAN_PER_TENSOR",
+    "GDO_MUTANT_COLUMN_IS_ROW",
 ]
 
 
