@@ -49,10 +49,21 @@ typedef enum {
     GD_PER_TENSOR = 1 /* one threshold per tensor ("per parameter matrix") */
 } gd_threshold;
 
-/* What is sent for the survivors (Section 5.4). */
+/* What is sent for the survivors (Section 5.4: 1-bit quantisation after
+ * dropping).  Every quantised form sends the indices, one sign bit per kept
+ * entry (set when acc < 0) and centre pairs (positive centre, negative
+ * centre); the kept entry's residual becomes acc minus the centre it is sent
+ * as. */
 typedef enum {
-    GD_QUANT_NONE = 0,     /* (index, value) pairs */
-    GD_QUANT_SIGN_MEAN = 1 /* indices + one sign bit each + two centres per tensor */
+    GD_QUANT_NONE = 0,        /* (index, value) pairs */
+    GD_QUANT_SIGN_MEAN = 1,   /* per tensor: average of its kept positives, of its kept negatives */
+    GD_QUANT_THRESHOLD = 2,   /* +-T, T the dropping threshold (the smallest kept |acc| of the
+                                 threshold segment), stored per tensor; (0, 0) when the segment
+                                 keeps nothing */
+    GD_QUANT_GLOBAL_MEAN = 3, /* one average of all kept positives and one of all kept negatives,
+                                 stored for every tensor */
+    GD_QUANT_COLUMN_MEAN = 4  /* per column of each tensor's row-major matrix view (gd_set_columns):
+                                 averages of the column's kept positives and negatives */
 } gd_quant;
 
 /* Opaque handle: the tensor layout and the device scratch the kernels use.
@@ -90,11 +101,13 @@ uint64_t gd_keep_total(const gd_ctx* ctx, double drop_ratio, gd_threshold mode);
 typedef struct {
     uint32_t* idx;           /* [capacity] kept flat indices, ascending */
     float* val;              /* [capacity] kept values acc[idx] (before quantisation) */
-    uint32_t* sign_bits;     /* GD_QUANT_SIGN_MEAN: [ceil(capacity/32)] words, bit j of
+    uint32_t* sign_bits;     /* quantised forms: [ceil(capacity/32)] words, bit j of
                                 word j/32 (LSB first) set when kept value j is negative;
                                 unused bits are 0.  Ignored for GD_QUANT_NONE. */
-    float* means;            /* GD_QUANT_SIGN_MEAN: [2*T] (positive centre, negative centre)
-                                per tensor.  Ignored for GD_QUANT_NONE. */
+    float* means;            /* quantised forms: gd_quant_centres() floats, (positive centre,
+                                negative centre) per tensor, or per column of tensor 0, then of
+                                tensor 1, ... for GD_QUANT_COLUMN_MEAN.  Ignored for
+                                GD_QUANT_NONE. */
     uint32_t* tensor_counts; /* [T] kept entries per tensor */
     uint64_t capacity;       /* host value: entries idx/val can hold, >= gd_keep_total() */
 } gd_sparse;
@@ -107,7 +120,7 @@ typedef struct {
  *     compressed quantity is then grad - base (Section 4, paragraph on pulls).
  *   residual (device, N floats, in/out): the carried residual.  On return it
  *     holds the new residual: +0.0 at kept entries (or acc minus the sent
- *     centre under GD_QUANT_SIGN_MEAN) and acc elsewhere.
+ *     centre under a quantised form) and acc elsewhere.
  *   With acc = (grad [- base]) + residual, exactly k entries are kept per
  *   threshold segment: the k largest |acc|, equal magnitudes taken in
  *   ascending flat index (so -0 ties +0; Inf ranks above finite values and
@@ -119,6 +132,23 @@ typedef struct {
 gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* residual,
                       double drop_ratio, gd_threshold mode, gd_quant quant, const gd_sparse* out,
                       void* stream);
+
+/*
+ * gd_set_columns - the matrix view used by GD_QUANT_COLUMN_MEAN (Section 5.4:
+ * centres per column rather than chosen globally).
+ *   columns (host, T entries): tensor t is a row-major matrix of columns[t]
+ *     columns; columns[t] must be at least 1 and divide the tensor's size.
+ *     Entry e of tensor t is in column (e - tensor_offsets[t]) % columns[t].
+ *   Until it is called every tensor is one column (the per-tensor sign mean).
+ *   Waits for the device (no call may still be running on this ctx) and
+ *   allocates the column tables.  GD_ERR_LAYOUT for a bad column count,
+ *   GD_ERR_OOM when allocation fails (the previous columns stay in force).
+ */
+gd_status gd_set_columns(gd_ctx* ctx, const uint32_t* columns);
+
+/* Number of floats gd_compress writes to out->means for `quant`: 2*T, or twice
+ * the total column count for GD_QUANT_COLUMN_MEAN; 0 for GD_QUANT_NONE. */
+uint64_t gd_quant_centres(const gd_ctx* ctx, gd_quant quant);
 
 /*
  * gd_compress_sampled - Algorithm 1 with the threshold selected on a sample,

@@ -65,6 +65,38 @@ void free_all(gd_ctx* ctx) {
     ctx->events.clear();
 }
 
+// Column layout for the column-wise centres: the tables and the zeroed
+// accumulators (two sums and two counts per column).  Replaces any earlier one.
+bool set_columns(gd_ctx* ctx, const std::vector<uint32_t>& columns) {
+    std::vector<uint32_t> colbase(ctx->T + 1, 0);
+    for (uint32_t t = 0; t < ctx->T; ++t) colbase[t + 1] = colbase[t] + columns[t];
+    const uint32_t groups = colbase[ctx->T];
+    gd::ColumnTables c{};
+    const size_t before = ctx->allocations.size();
+    bool ok = dev_upload(ctx, &c.columns, columns) && dev_upload(ctx, &c.colbase, colbase) &&
+              dev_alloc(ctx, &c.csum, 2 * (size_t)groups) && dev_alloc(ctx, &c.ccnt, 2 * (size_t)groups);
+    ok = ok && hipMemset(c.csum, 0, 2 * (size_t)std::max<uint32_t>(groups, 1) * sizeof(double)) == hipSuccess &&
+         hipMemset(c.ccnt, 0, 2 * (size_t)std::max<uint32_t>(groups, 1) * sizeof(uint32_t)) == hipSuccess &&
+         hipDeviceSynchronize() == hipSuccess;
+    if (!ok) {
+        for (size_t i = before; i < ctx->allocations.size(); ++i) (void)hipFree(ctx->allocations[i]);
+        ctx->allocations.resize(before);
+        return false;
+    }
+    // the previous tables are freed
+    for (void* p : {(void*)ctx->cols.columns, (void*)ctx->cols.colbase, (void*)ctx->cols.csum, (void*)ctx->cols.ccnt}) {
+        if (!p) continue;
+        auto it = std::find(ctx->allocations.begin(), ctx->allocations.end(), p);
+        if (it != ctx->allocations.end()) {
+            (void)hipFree(p);
+            ctx->allocations.erase(it);
+        }
+    }
+    c.groups = groups;
+    ctx->cols = c;
+    return true;
+}
+
 // The passes after the threshold bracket is set: the dense stream, the
 // candidate layout, exact selection or plain compaction, and quantisation.
 // k_total is the host-known output size (exact threshold) or 0 (sampled).
@@ -137,7 +169,12 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     ea.val = out->val;
     ea.tensor_counts = out->tensor_counts;
     ea.capacity = out->capacity;
-    const bool q = quant == GD_QUANT_SIGN_MEAN;
+    const bool q = quant != GD_QUANT_NONE;
+    ea.qkind = (uint32_t)quant;
+    ea.columns = ctx->cols.columns;
+    ea.colbase = ctx->cols.colbase;
+    ea.csum = ctx->cols.csum;
+    ea.ccnt = ctx->cols.ccnt;
     if (gd::launch_layout(ca, st) != hipSuccess) return GD_ERR_HIP;
     if (gd::launch_candidates(ca, ea, q, ctx->max_tiles, st) != hipSuccess) return GD_ERR_HIP;
 
@@ -155,6 +192,17 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
         qa.T = ctx->T;
         qa.N = (uint32_t)ctx->N;
         qa.k_total = k_total;
+        qa.qkind = (uint32_t)quant;
+        qa.per_tensor = per;
+        qa.keep_ppm = ppm;
+        qa.seg_off = seg_off;
+        qa.tensor_off = ctx->tab.tensor_off;
+        qa.seg = ctx->scr.seg;
+        qa.columns = ctx->cols.columns;
+        qa.colbase = ctx->cols.colbase;
+        qa.groups = ctx->cols.groups;
+        qa.csum = ctx->cols.csum;
+        qa.ccnt = ctx->cols.ccnt;
         if (gd::launch_quant(qa, st) != hipSuccess) return GD_ERR_HIP;
     }
     return GD_OK;
@@ -268,6 +316,11 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
         delete ctx;
         return GD_ERR_OOM;
     }
+    if (!set_columns(ctx, std::vector<uint32_t>(T, 1u))) {
+        free_all(ctx);
+        delete ctx;
+        return GD_ERR_OOM;
+    }
     if (hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
         hipMemset(ctx->scr.shist, 0, (size_t)S_max * gd::kSHistWords * sizeof(uint32_t)) != hipSuccess ||
         hipMemset(ctx->scr.sshist, 0, (size_t)S_max * gd::kSsCopies * gd::kSsNB0 * sizeof(uint32_t)) != hipSuccess ||
@@ -291,10 +344,10 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
                       gd_threshold mode, gd_quant quant, const gd_sparse* out, void* stream) {
     if (!ctx || !grad || !residual || !out) return GD_ERR_ARG;
     if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
-    if (quant != GD_QUANT_NONE && quant != GD_QUANT_SIGN_MEAN) return GD_ERR_ARG;
+    if (quant < GD_QUANT_NONE || quant > GD_QUANT_COLUMN_MEAN) return GD_ERR_ARG;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
     if (!out->idx || !out->val || !out->tensor_counts) return GD_ERR_ARG;
-    if (quant == GD_QUANT_SIGN_MEAN && (!out->sign_bits || !out->means)) return GD_ERR_ARG;
+    if (quant != GD_QUANT_NONE && (!out->sign_bits || !out->means)) return GD_ERR_ARG;
     if (!aligned16(grad) || !aligned16(residual) || (base && !aligned16(base))) return GD_ERR_ALIGN;
     const uint64_t k_total = gd_keep_total(ctx, drop_ratio, mode);
     if (out->capacity < k_total) return GD_ERR_CAPACITY;
@@ -326,6 +379,27 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     if (gd::launch_sample(sa, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
 
     return run_after_bracket(ctx, grad, base, residual, per, ppm, false, quant, k_total, out, st);
+}
+
+gd_status gd_set_columns(gd_ctx* ctx, const uint32_t* columns) {
+    if (!ctx || !columns) return GD_ERR_ARG;
+    std::vector<uint32_t> c(columns, columns + ctx->T);
+    uint64_t total = 0;
+    for (uint32_t t = 0; t < ctx->T; ++t) {
+        const uint64_t n = ctx->offsets[t + 1] - ctx->offsets[t];
+        if (c[t] == 0 || n % c[t] != 0) return GD_ERR_LAYOUT;
+        total += c[t];
+    }
+    if (total >= 0x80000000ull) return GD_ERR_LAYOUT;
+    DeviceGuard guard(ctx->device);
+    if (!guard.ok) return GD_ERR_HIP;
+    if (hipDeviceSynchronize() != hipSuccess) return GD_ERR_HIP;  // no call may still use the old tables
+    return set_columns(ctx, c) ? GD_OK : GD_ERR_OOM;
+}
+
+uint64_t gd_quant_centres(const gd_ctx* ctx, gd_quant quant) {
+    if (!ctx || quant == GD_QUANT_NONE) return 0;
+    return quant == GD_QUANT_COLUMN_MEAN ? 2 * (uint64_t)ctx->cols.groups : 2 * (uint64_t)ctx->T;
 }
 
 gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base, float* residual,

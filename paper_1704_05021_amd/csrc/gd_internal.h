@@ -56,6 +56,15 @@ struct Scratch {
     uint32_t* sshist = nullptr;      // [S_max * kSsCopies * kSsNB0] sampled mode: top-digit histograms
 };
 
+// Column-wise centres: each tensor's matrix view and the per-column sums.
+struct ColumnTables {
+    uint32_t* columns = nullptr;  // [T]
+    uint32_t* colbase = nullptr;  // [T + 1] first column group of each tensor
+    double* csum = nullptr;       // [2 * groups] positive and negative sums
+    uint32_t* ccnt = nullptr;     // [2 * groups] positive and negative counts
+    uint32_t groups = 0;
+};
+
 }  // namespace gd
 
 struct gd_ctx {
@@ -69,6 +78,7 @@ struct gd_ctx {
     uint32_t skeys_global = 0;
     gd::Tables tab;
     gd::Scratch scr;
+    gd::ColumnTables cols;
     std::vector<void*> allocations;
     uint32_t debug_bracket = 0;
     bool profile = false;

@@ -108,11 +108,20 @@ struct CandArgs {
     uint32_t sampled;     // sampled threshold: every candidate is kept, no bracket can miss
 };
 
+// 1-bit centres (Section 5.4): per-tensor sign means, the dropping threshold,
+// one global average, or column-wise averages.
+constexpr uint32_t kQuantSignMean = 1, kQuantThreshold = 2, kQuantGlobalMean = 3, kQuantColumnMean = 4;
+
 struct EmitArgs {
     uint32_t* idx;
     float* val;
     uint32_t* tensor_counts;
     uint64_t capacity;
+    uint32_t qkind;             // 0 or a kQuant* kind
+    const uint32_t* columns;    // [T] columns of each tensor's matrix view (column-wise centres)
+    const uint32_t* colbase;    // [T + 1] first column group of each tensor
+    double* csum;               // [2 * groups] column sums (positive, negative), zero on entry
+    uint32_t* ccnt;             // [2 * groups] column counts, zero on entry
 };
 
 struct QuantArgs {
@@ -128,6 +137,17 @@ struct QuantArgs {
     uint32_t T;
     uint32_t N;
     uint64_t k_total;
+    uint32_t qkind;
+    uint32_t per_tensor;
+    uint32_t keep_ppm;
+    const uint32_t* seg_off;    // [S + 1]
+    const uint32_t* tensor_off; // [T + 1]
+    const SegState* seg;
+    const uint32_t* columns;
+    const uint32_t* colbase;
+    uint32_t groups;            // column groups (column-wise centres)
+    double* csum;               // cleared again after use
+    uint32_t* ccnt;
 };
 
 constexpr uint32_t kMaxPushes = 64;

@@ -1,42 +1,82 @@
-// Sign-mean 1-bit quantisation of the kept values (Section 5.4), with the
+// 1-bit quantisation of the kept values (Section 5.4), with the
 // quantisation error fed back into the residual (gfx950, wave64).
 //
-// After dropping, each kept value is replaced by one of two centres per
-// tensor: the average of that tensor's kept positive values (values not
-// below zero) or of its kept negative values.  Sums are taken in fp64 in a
-// fixed order (per candidate tile, then tiles in order), so results are
-// deterministic.  The sent bits are packed LSB-first, 32 per word, and
-// residual[idx] becomes acc - centre.
+// After dropping, each kept value is replaced by one of two centres, chosen by
+// its sign (values not below zero are positive).  Section 5.4 compares
+// several ways of choosing the centres; all four are here:
+//   sign mean    : per tensor, the average of its kept positive values and of
+//                  its kept negative values;
+//   threshold    : +-T, T the dropping threshold, i.e. the smallest kept
+//                  magnitude of the threshold segment;
+//   global mean  : one positive and one negative average over every kept
+//                  value of the call;
+//   column mean  : per column of each tensor's row-major matrix view.
+// Per-tensor and global sums are taken in fp64 in a fixed order (per
+// candidate tile, then tiles in order), so they are deterministic; column
+// sums are fp64 atomics.  The sent bits are packed LSB-first, 32 per word,
+// and residual[idx] becomes acc - centre.
 
 #include "gd_kernels.h"
 
 namespace gd {
 
+// Centres per tensor (every kind but the column mean) and the first output
+// slot of each tensor.  One wave per tensor.
 __global__ __launch_bounds__(kBlock) void k_means(QuantArgs q) {
     const int w = threadIdx.x >> 6, lane = lane_id();
     const uint32_t t = blockIdx.x * kWavesPerBlock + w;
     if (t >= q.T) return;
-    const uint32_t g0 = q.tile_base[t], g1 = q.tile_base[t + 1];
-    double sp = 0.0, sn = 0.0, np = 0.0, nn = 0.0;
-    for (uint32_t g = g0 + lane; g < g1; g += kWave) {
-        sp += q.tile_q[4 * (size_t)g + 0];
-        sn += q.tile_q[4 * (size_t)g + 1];
-        np += q.tile_q[4 * (size_t)g + 2];
-        nn += q.tile_q[4 * (size_t)g + 3];
-    }
-    sp = wave_sum(sp);
-    sn = wave_sum(sn);
-    np = wave_sum(np);
-    nn = wave_sum(nn);
     uint32_t before = 0;
     for (uint32_t u = lane; u < t; u += kWave) before += q.tensor_counts[u];
     before = wave_sum(before);
     if (lane == 0) {
-        q.means[2 * t + 0] = np > 0.0 ? (float)(sp / np) : 0.0f;
-        q.means[2 * t + 1] = nn > 0.0 ? (float)(sn / nn) : 0.0f;
         q.qbase[t] = before;
         if (t + 1 == q.T) q.qbase[q.T] = before + q.tensor_counts[t];
     }
+    if (q.qkind == kQuantColumnMean) return;
+    float pos = 0.0f, neg = 0.0f;
+    if (q.qkind == kQuantThreshold) {
+        // the exact threshold key is the smallest kept magnitude
+        const uint32_t s = q.per_tensor ? t : 0u;
+        if (keep_of(q.seg_off[s + 1] - q.seg_off[s], q.keep_ppm) > 0) {
+            pos = __uint_as_float(q.seg[s].thr);
+            neg = __uint_as_float(q.seg[s].thr | 0x80000000u);
+        }
+    } else {
+        const bool global = q.qkind == kQuantGlobalMean;
+        const uint32_t g0 = global ? 0u : q.tile_base[t], g1 = global ? q.tile_base[q.T] : q.tile_base[t + 1];
+        double sp = 0.0, sn = 0.0, np = 0.0, nn = 0.0;
+        for (uint32_t g = g0 + lane; g < g1; g += kWave) {
+            sp += q.tile_q[4 * (size_t)g + 0];
+            sn += q.tile_q[4 * (size_t)g + 1];
+            np += q.tile_q[4 * (size_t)g + 2];
+            nn += q.tile_q[4 * (size_t)g + 3];
+        }
+        sp = wave_sum(sp);
+        sn = wave_sum(sn);
+        np = wave_sum(np);
+        nn = wave_sum(nn);
+        pos = np > 0.0 ? (float)(sp / np) : 0.0f;
+        neg = nn > 0.0 ? (float)(sn / nn) : 0.0f;
+    }
+    if (lane == 0) {
+        q.means[2 * t + 0] = pos;
+        q.means[2 * t + 1] = neg;
+    }
+}
+
+// Column-wise centres from the column sums, which are cleared for the next call.
+__global__ __launch_bounds__(kBlock) void k_colmeans(QuantArgs q) {
+    const uint32_t g = blockIdx.x * kBlock + threadIdx.x;
+    if (g >= q.groups) return;
+    const double sp = q.csum[2 * g + 0], sn = q.csum[2 * g + 1];
+    const uint32_t np = q.ccnt[2 * g + 0], nn = q.ccnt[2 * g + 1];
+    q.means[2 * g + 0] = np ? (float)(sp / (double)np) : 0.0f;
+    q.means[2 * g + 1] = nn ? (float)(sn / (double)nn) : 0.0f;
+    q.csum[2 * g + 0] = 0.0;
+    q.csum[2 * g + 1] = 0.0;
+    q.ccnt[2 * g + 0] = 0;
+    q.ccnt[2 * g + 1] = 0;
 }
 
 __global__ __launch_bounds__(kBlock) void k_quant(QuantArgs q) {
@@ -53,8 +93,9 @@ __global__ __launch_bounds__(kBlock) void k_quant(QuantArgs q) {
         }
         const float x = q.val[j];
         neg = x < 0.0f;
-        const float centre = neg ? q.means[2 * lo + 1] : q.means[2 * lo + 0];
         const uint32_t i = q.idx[j];
+        const uint32_t g = q.qkind == kQuantColumnMean ? q.colbase[lo] + (i - q.tensor_off[lo]) % q.columns[lo] : lo;
+        const float centre = neg ? q.means[2 * g + 1] : q.means[2 * g + 0];
         if (i < q.N) q.res[i] = x - centre;
     }
     const uint64_t m = ballot(valid && neg);
@@ -68,6 +109,8 @@ static inline uint32_t blocks_for_waves(uint32_t waves) { return (waves + kWaves
 
 hipError_t launch_quant(const QuantArgs& q, hipStream_t st) {
     hipLaunchKernelGGL(k_means, dim3(blocks_for_waves(q.T)), dim3(kBlock), 0, st, q);
+    if (q.qkind == kQuantColumnMean && q.groups > 0)
+        hipLaunchKernelGGL(k_colmeans, dim3((q.groups + kBlock - 1) / kBlock), dim3(kBlock), 0, st, q);
     if (q.k_total > 0) {
         const uint64_t blocks = (q.k_total + kBlock - 1) / kBlock;
         hipLaunchKernelGGL(k_quant, dim3((uint32_t)blocks), dim3(kBlock), 0, st, q);

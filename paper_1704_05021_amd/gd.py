@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgd.so")
 
 GD_GLOBAL, GD_PER_TENSOR = 0, 1
-GD_QUANT_NONE, GD_QUANT_SIGN_MEAN = 0, 1
+GD_QUANT_NONE, GD_QUANT_SIGN_MEAN, GD_QUANT_THRESHOLD, GD_QUANT_GLOBAL_MEAN, GD_QUANT_COLUMN_MEAN = 0, 1, 2, 3, 4
 
 STATUS = {
     0: "GD_OK",
@@ -36,6 +36,8 @@ EXPORTS = [
     "gd_keep_total",
     "gd_compress",
     "gd_compress_sampled",
+    "gd_set_columns",
+    "gd_quant_centres",
     "gd_apply_sparse",
     "gd_status_string",
     "gd_profile_enable",
@@ -86,6 +88,10 @@ def _lib() -> ctypes.CDLL:
     lib.gd_compress.restype = i32
     lib.gd_compress_sampled.argtypes = [vp, vp, vp, vp, dbl, i32, u32, u64, ctypes.POINTER(_Sparse), vp]
     lib.gd_compress_sampled.restype = i32
+    lib.gd_set_columns.argtypes = [vp, vp]
+    lib.gd_set_columns.restype = i32
+    lib.gd_quant_centres.argtypes = [vp, i32]
+    lib.gd_quant_centres.restype = u64
     lib.gd_apply_sparse.argtypes = [vp, u64, u32, vp, vp, vp, ctypes.c_float, vp]
     lib.gd_apply_sparse.restype = i32
     lib.gd_status_string.argtypes = [i32]
@@ -166,7 +172,7 @@ class Compressor:
     def keep_total(self, drop_ratio: float, per_tensor: bool = False) -> int:
         return int(_lib().gd_keep_total(self._h, float(drop_ratio), GD_PER_TENSOR if per_tensor else GD_GLOBAL))
 
-    def alloc_out(self, drop_ratio: float, per_tensor: bool = False, quant: bool = False,
+    def alloc_out(self, drop_ratio: float, per_tensor: bool = False, quant=False,
                   capacity: Optional[int] = None) -> SparseOut:
         k = self.keep_total(drop_ratio, per_tensor)
         cap = max(k if capacity is None else capacity, 1)
@@ -178,14 +184,18 @@ class Compressor:
             k=k,
         )
         if quant:
+            centres = int(_lib().gd_quant_centres(self._h, int(quant)))
             out.sign_bits = torch.empty(max((cap + 31) // 32, 1), dtype=torch.int32, device=dev)
-            out.means = torch.empty(max(2 * self.T, 1), dtype=torch.float32, device=dev)
+            out.means = torch.empty(max(centres, 1), dtype=torch.float32, device=dev)
         return out
 
     def compress(self, grad: torch.Tensor, residual: torch.Tensor, drop_ratio: float = 0.99,
-                 per_tensor: bool = False, quant: bool = False, base: Optional[torch.Tensor] = None,
+                 per_tensor: bool = False, quant=False, base: Optional[torch.Tensor] = None,
                  out: Optional[SparseOut] = None, stream: Optional[torch.cuda.Stream] = None) -> SparseOut:
-        """One gd_compress call; ``residual`` is updated in place."""
+        """One gd_compress call; ``residual`` is updated in place.
+
+        quant: False/GD_QUANT_NONE, True/GD_QUANT_SIGN_MEAN, or another GD_QUANT_* form.
+        """
         _check_f32(grad, "grad", self.N)
         _check_f32(residual, "residual", self.N)
         if base is not None:
@@ -203,11 +213,25 @@ class Compressor:
         st = _lib().gd_compress(
             self._h, grad.data_ptr(), None if base is None else base.data_ptr(), residual.data_ptr(),
             float(drop_ratio), GD_PER_TENSOR if per_tensor else GD_GLOBAL,
-            GD_QUANT_SIGN_MEAN if quant else GD_QUANT_NONE, ctypes.byref(sp), _stream_handle(stream))
+            int(quant), ctypes.byref(sp), _stream_handle(stream))
         if st != 0:
             raise GDError(st, "gd_compress")
         out.k = self.keep_total(drop_ratio, per_tensor)
         return out
+
+    def set_columns(self, columns) -> None:
+        """Matrix view of every tensor for the column-wise centres (gd_set_columns)."""
+        import numpy as np
+
+        c = np.ascontiguousarray(columns, dtype=np.uint32)
+        if c.size != self.T:
+            raise ValueError(f"need {self.T} column counts, got {c.size}")
+        st = _lib().gd_set_columns(self._h, c.ctypes.data)
+        if st != 0:
+            raise GDError(st, "gd_set_columns")
+
+    def quant_centres(self, quant: int) -> int:
+        return int(_lib().gd_quant_centres(self._h, int(quant)))
 
     def compress_sampled(self, grad: torch.Tensor, residual: torch.Tensor, drop_ratio: float = 0.99,
                          per_tensor: bool = False, sample_ppm: int = 1000, seed: int = 0,

@@ -50,12 +50,13 @@ def gpu_compress(comp: gd.Compressor, grad: np.ndarray, residual: np.ndarray, dr
     )
     if quant:
         res.sign_bits = o.sign_bits[:(k + 31) // 32].cpu().numpy().view(np.uint32).copy()
-        res.means = o.means[:2 * comp.T].cpu().numpy().copy()
+        res.means = o.means[:comp.quant_centres(int(quant))].cpu().numpy().copy()
     return res
 
 
-def oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base=None) -> Result:
-    o = oracle.compress(grad, residual, offsets, drop, per_tensor=per_tensor, quant=quant, base=base)
+def oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base=None, columns=None) -> Result:
+    o = oracle.compress(grad, residual, offsets, drop, per_tensor=per_tensor, quant=quant, base=base,
+                        columns=columns)
     return Result(o.idx, o.val, o.residual, o.tensor_counts, o.sign_bits, o.means)
 
 
@@ -88,15 +89,20 @@ def assert_parity(g: Result, o: Result, quant: bool, what: str = "") -> None:
         assert np.array_equal(bits(g.residual), bits(o.residual)), f"{what}: equal centres but residuals differ"
 
 
-def check_case(grad, residual, offsets: Sequence[int], drop: float, per_tensor: bool, quant: bool,
+def check_case(grad, residual, offsets: Sequence[int], drop: float, per_tensor: bool, quant,
                base=None, comp: Optional[gd.Compressor] = None, debug_bracket: int = 0,
-               what: str = "") -> Result:
-    comp = comp or gd.Compressor(offsets)
+               what: str = "", columns: Optional[Sequence[int]] = None) -> Result:
+    """quant: False/True or a GD_QUANT_* form; columns: the matrix view for the column-wise centres
+    (``comp`` must already have them set when it is passed in)."""
+    if comp is None:
+        comp = gd.Compressor(offsets)
+        if columns is not None:
+            comp.set_columns(columns)
     comp.debug_force_bracket(debug_bracket)
     try:
         g = gpu_compress(comp, grad, residual, drop, per_tensor, quant, base)
     finally:
         comp.debug_force_bracket(0)
-    o = oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base)
+    o = oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base, columns)
     assert_parity(g, o, quant, what)
     return o
