@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 METRIC = "G grad-elements/s compressed at 99% drop; % of HBM peak (1 GPU)"
 SAMPLED_CAPACITY_PCT = 4  # output room of the sampled mode, in percent of the elements
+QUANT_KINDS = {"none": 0, "sign_mean": 1, "threshold": 2, "global_mean": 3, "column_mean": 4}
 
 
 def parse():
@@ -37,6 +38,8 @@ def parse():
     ap.add_argument("--selection", choices=("exact", "sampled"), default="exact",
                     help="exact k-th largest threshold (gd_compress, the default), or the paper's threshold "
                          "selected on a sample (gd_compress_sampled, Section 4)")
+    ap.add_argument("--quant", choices=("workload",) + tuple(QUANT_KINDS), default="workload",
+                    help="1-bit centres of Section 5.4 (default: the workload's own)")
     ap.add_argument("--sample-ppm", type=int, default=1000,
                     help="sample size per million entries for --selection sampled (1000 = 0.1%%)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=12.0,
@@ -47,7 +50,7 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(w, grads_host, budget_s, sample_ppm=0):
+def cpu_baseline(w, grads_host, budget_s, sample_ppm=0, quant=0):
     """The oracle, single-threaded, on consecutive steps of the same workload.
 
     Steps cycle through the staged gradients with the residual carried, as
@@ -68,7 +71,8 @@ def cpu_baseline(w, grads_host, budget_s, sample_ppm=0):
             o = oracle.compress_sampled(g, residual, off, w.drop, per_tensor=w.per_tensor, sample_ppm=sample_ppm,
                                         seed=done, capacity=SAMPLED_CAPACITY_PCT * w.layout.numel // 100, lib=lib)
         else:
-            o = oracle.compress(g, residual, off, w.drop, per_tensor=w.per_tensor, quant=w.quant, lib=lib)
+            o = oracle.compress(g, residual, off, w.drop, per_tensor=w.per_tensor, quant=quant, lib=lib,
+                                columns=w.layout.columns if quant == 4 else None)
         elapsed += time.perf_counter() - t0
         if first is None:
             first = o
@@ -164,8 +168,11 @@ def main():
     residual = torch.zeros(N, dtype=torch.float32, device="cuda")
     comp = gd.Compressor(off)
     sampled = args.selection == "sampled"
+    quant = int(w.quant) if args.quant == "workload" else QUANT_KINDS[args.quant]
+    if quant == 4:
+        comp.set_columns(w.layout.columns)
     if sampled:
-        if w.quant:
+        if quant:
             print("the sampled selection has no quantised form", file=sys.stderr)
             sys.exit(2)
         cap = SAMPLED_CAPACITY_PCT * N // 100
@@ -179,10 +186,10 @@ def main():
             return int(out.tensor_counts[:comp.T].cpu().numpy().view(np.uint32).astype(np.int64).sum())
     else:
         k = comp.keep_total(w.drop, w.per_tensor)
-        out = comp.alloc_out(w.drop, w.per_tensor, w.quant)
+        out = comp.alloc_out(w.drop, w.per_tensor, quant)
 
         def step(i):
-            comp.compress(grads[i % len(grads)], residual, w.drop, per_tensor=w.per_tensor, quant=w.quant,
+            comp.compress(grads[i % len(grads)], residual, w.drop, per_tensor=w.per_tensor, quant=quant,
                           out=out)
 
         def kept_now():
@@ -237,7 +244,7 @@ def main():
             "selection": f"sampled, {args.sample_ppm} ppm sample, count of the last step" if sampled
                          else "exact k-th largest",
             "threshold": "per_tensor" if w.per_tensor else "global",
-            "quant": "sign_mean" if w.quant else "none",
+            "quant": {v: k for k, v in QUANT_KINDS.items()}[quant],
             "drop": w.drop,
             "gradient_steps_cycled": len(grads),
             "byte_model": "12 B/element + 8 B/kept element",
@@ -255,10 +262,14 @@ def main():
         },
     }
     if args.cpu_baseline_seconds > 0:
-        cb, first = cpu_baseline(w, grads_host, args.cpu_baseline_seconds, args.sample_ppm if sampled else 0)
+        cb, first = cpu_baseline(w, grads_host, args.cpu_baseline_seconds, args.sample_ppm if sampled else 0, quant)
         line["cpu_baseline"] = cb
-        line["parity_step0"] = bool(np.array_equal(first.idx, first_idx) and
-                                    np.array_equal(first.residual.view(np.uint32), first_res.view(np.uint32)))
+        if quant in (0, 2):  # no float reduction: bit-exact
+            res_ok = np.array_equal(first.residual.view(np.uint32), first_res.view(np.uint32))
+        else:  # centres are fp64 sums in another order: within 1e-6 of the largest centre
+            scale = float(np.max(np.abs(first.means))) if first.means is not None and first.means.size else 0.0
+            res_ok = bool(np.all(np.abs(first.residual.astype(np.float64) - first_res) <= 1e-6 * scale))
+        line["parity_step0"] = bool(np.array_equal(first.idx, first_idx) and res_ok)
     print(json.dumps(line), flush=True)
 
 

@@ -72,6 +72,11 @@ class Layout:
     def num_tensors(self) -> int:
         return len(self.names)
 
+    @property
+    def columns(self) -> List[int]:
+        """Columns of each tensor read as a row-major matrix (a vector is one row)."""
+        return [int(s[-1]) if len(s) else 1 for s in self.shapes]
+
 
 def mlp_layout(widths: Sequence[int]) -> Layout:
     """Weights and biases of a fully connected net, interleaved W1, b1, W2, b2, ...
