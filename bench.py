@@ -34,7 +34,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="nmt_85k_per_tensor")
+    ap.add_argument("--workload", default="nmt_85k_per_tensor",
+                    help="a compress workload, or shard_apply_pull for the server side (apply + pull delta)")
     ap.add_argument("--selection", choices=("exact", "sampled"), default="exact",
                     help="exact k-th largest threshold (gd_compress, the default), or the paper's threshold "
                          "selected on a sample (gd_compress_sampled, Section 4)")
@@ -140,6 +141,107 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes": 4 * n, "launches": 5}), flush=True)
 
 
+def main_shard(args, torch, np, gd, wl):
+    """The server side at one GPU's shard (37M parameters, 4 clients x 370,000 pushes,
+    about 5% shared): per step, apply the four pushes (gd_apply_sparse), then compress the
+    pull delta p - p_last with a global threshold and a carried pull residual."""
+    sh = wl.server_shard(**wl.SHARD_FULL)
+    N = sh.params.size
+    print(f"[bench] shard of {N} parameters, {len(sh.idx)} pushes", file=sys.stderr, flush=True)
+    p = torch.from_numpy(sh.params).cuda()
+    p_last = p.clone()
+    pull_res = torch.zeros_like(p)
+    idx = [torch.from_numpy(a.view(np.int32)).cuda() for a in sh.idx]
+    val = [torch.from_numpy(a).cuda() for a in sh.val]
+    comp = gd.Compressor([0, N])
+    drop = 0.99
+    k = comp.keep_total(drop, False)
+    out = comp.alloc_out(drop, False)
+    entries = sum(int(a.size) for a in sh.idx)
+
+    def step(i):
+        gd.apply_sparse(p, idx, val, lr=1.0)
+        comp.compress(p, pull_res, drop, per_tensor=False, base=p_last, out=out)
+
+    # parity of step 0 (apply, then the pull) against the oracle
+    step(0)
+    torch.cuda.synchronize()
+    first_p = p.cpu().numpy().copy()
+    first_idx = out.idx[:k].cpu().numpy().view(np.uint32).copy()
+    first_res = pull_res.cpu().numpy().copy()
+    p.copy_(p_last)
+    pull_res.zero_()
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    comp.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    dense_ms, dense_n = comp.profile_read()
+    comp.profile_enable(False)
+    sec = (t1 - t0) / args.steps
+    dense_avg_s = dense_ms / 1e3 / max(dense_n, 1)
+    achieved = 16 * N / dense_avg_s / 1e9  # grad, base and residual read, residual written
+    model_bytes = 16 * entries + 16 * N + 8 * k
+    line = {
+        "metric": METRIC,
+        "value": round(N / sec / 1e9, 3),
+        "unit": "G grad-elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "hbm_model_frac": round(model_bytes / sec / 1e9 / HBM_PEAK_GBPS, 4),
+        "config": {
+            "workload": "shard_apply_pull",
+            "elements": N,
+            "pushes": len(sh.idx),
+            "push_entries": entries,
+            "kept_per_step": k,
+            "threshold": "global",
+            "drop": drop,
+            "byte_model": "16 B/push entry + 16 B/element (pull delta with residual) + 8 B/kept element",
+        },
+        "roofline": {
+            "kernel": "k_dense<true>",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "dense_us": round(dense_avg_s * 1e6, 2),
+            "dense_launches": dense_n,
+        },
+    }
+    if args.cpu_baseline_seconds > 0:
+        import oracle
+
+        lib = oracle.load()
+        t0 = time.perf_counter()
+        p1 = oracle.apply_sparse(sh.params, sh.idx, sh.val, 1.0, lib=lib)
+        o = oracle.compress(p1, np.zeros(N, np.float32), [0, N], drop, base=sh.params, lib=lib)
+        el = time.perf_counter() - t0
+        line["cpu_baseline"] = {
+            "value": N / el / 1e9, "unit": "G grad-elements/s", "cores": 1, "kind": "oracle",
+            "sample": f"one step (apply of {len(sh.idx)} pushes, then the pull delta) of the 37M shard "
+                      f"({el:.1f} s of single-threaded oracle time)",
+        }
+        line["parity_step0"] = bool(np.array_equal(p1.view(np.uint32), first_p.view(np.uint32)) and
+                                    np.array_equal(o.idx, first_idx) and
+                                    np.array_equal(o.residual.view(np.uint32), first_res.view(np.uint32)))
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -158,6 +260,9 @@ def main():
     torch.cuda.set_device(0)
     if args.copy_calibration_mib:
         copy_calibration(args.copy_calibration_mib)
+        return
+    if args.workload == "shard_apply_pull":
+        main_shard(args, torch, np, gd, wl)
         return
     w = wl.workload(args.workload)
     N = w.layout.numel

@@ -3,101 +3,136 @@
 //
 // For an index pushed by several clients the values are summed in client
 // order starting from +0, and the parameter is updated once:
-// p[i] -= lr * s[i].  The lowest client holding an index owns it: it finds
-// the index in the later clients' (ascending) lists through a window of
-// their indices staged in LDS, sums, and writes.  No atomics, so the result
-// is deterministic.
+// p[i] -= lr * s[i].  No atomics, so the result is deterministic.
+//
+// One block per bucket of 2^15 consecutive parameter indices.  The block
+// finds where the bucket starts and ends in every client's (ascending) index
+// list by a 32-way search per half-wave (four rounds of loads for a list of a
+// few hundred thousand entries, instead of a binary search's twenty), stages
+// those entries in LDS, and then gives every index to the lowest client
+// holding it, which sums all clients' values for it in client order and
+// writes p once.  The parameter writes of a block stay inside its bucket.
 
 #include "gd_kernels.h"
 
 namespace gd {
 
-// First position in list[lo, hi) whose value is >= x.
-__device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* list, uint32_t lo, uint32_t hi, uint32_t x) {
-    while (lo < hi) {
-        const uint32_t mid = lo + ((hi - lo) >> 1);
-        if (list[mid] < x) lo = mid + 1;
-        else hi = mid;
+constexpr int kApplyBucketShift = 15;
+constexpr int kApplyLds = 4096;  // entries of all clients staged per bucket
+
+// First position in list[lo, hi) whose value is >= x, found by the 32 lanes of
+// one half-wave together (g: lane within the half, mask: the half's lanes).
+__device__ uint32_t half_lower_bound(const uint32_t* list, uint32_t lo, uint32_t hi, uint32_t x, uint32_t g,
+                                     uint64_t mask) {
+    while (hi > lo) {
+        const uint32_t len = hi - lo;
+        if (len <= 32u) {
+            const bool below = g < len && list[lo + (g < len ? g : 0u)] < x;
+            return lo + popc64(ballot(below) & mask);
+        }
+        const uint32_t step = (len + 31u) / 32u;
+        uint32_t q = lo + (g + 1u) * step - 1u;
+        if (q >= hi) q = hi - 1u;
+        // probes rise with g, so the lanes below x form a prefix of the half
+        const uint32_t t = popc64(ballot(list[q] < x) & mask);
+        const uint64_t nlo = (uint64_t)lo + (uint64_t)t * step, nhi = nlo + step;
+        lo = nlo < hi ? (uint32_t)nlo : hi;
+        hi = nhi < hi ? (uint32_t)nhi : hi;
     }
     return lo;
 }
 
-// First position in list[lo, hi) whose value is > x.
-__device__ __forceinline__ uint32_t upper_bound_u32(const uint32_t* list, uint32_t lo, uint32_t hi, uint32_t x) {
-    while (lo < hi) {
-        const uint32_t mid = lo + ((hi - lo) >> 1);
-        if (list[mid] <= x) lo = mid + 1;
-        else hi = mid;
+// First position in list[lo, hi) holding x, or hi.
+__device__ __forceinline__ uint32_t find_u32(const uint32_t* list, uint32_t lo, uint32_t hi, uint32_t x) {
+    uint32_t a = lo, b = hi;
+    while (a < b) {
+        const uint32_t mid = a + ((b - a) >> 1);
+        if (list[mid] < x) a = mid + 1;
+        else b = mid;
     }
-    return lo;
+    return a < hi && list[a] == x ? a : hi;
 }
-
-constexpr int kApplyWindow = 256;
 
 __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
-    __shared__ uint32_t win[kWavesPerBlock][kApplyWindow];
-    const int w = threadIdx.x >> 6, lane = lane_id();
-    const uint32_t c = blockIdx.y;
-    const uint32_t nnz = a.nnz[c];
-    const uint32_t j0 = (blockIdx.x * kWavesPerBlock + w) * kWave;
-    if (j0 >= nnz) return;
-    const uint32_t j = j0 + lane;
-    const bool have = j < nnz;
-    const uint32_t i = have ? a.idx[c][j] : 0u;
-    const bool valid = have && i < a.n;
-    // index range covered by this wave (lists are ascending)
-    const uint32_t last_j = (j0 + kWave <= nnz ? j0 + kWave : nnz) - 1;
-    const uint32_t i_first = a.idx[c][j0], i_last = a.idx[c][last_j];
-    float s = 0.0f;
-    bool owner = true;
-    for (uint32_t cc = 0; cc < a.C; ++cc) {
-        if (cc == c) {
-            s = s + (valid ? a.val[c][j] : 0.0f);
-            continue;
-        }
-        const uint32_t* list = a.idx[cc];
-        const uint32_t m = a.nnz[cc];
-        uint32_t wlo = 0, whi = 0;
-        if (lane == 0) wlo = lower_bound_u32(list, 0, m, i_first);
-        if (lane == 1) whi = upper_bound_u32(list, 0, m, i_last);
-        wlo = __shfl(wlo, 0, kWave);
-        whi = __shfl(whi, 1, kWave);
-        const uint32_t wn = whi - wlo;
-        uint32_t pos = 0;
-        bool found = false;
-        if (wn <= (uint32_t)kApplyWindow) {
-            for (uint32_t q = lane; q < wn; q += kWave) win[w][q] = list[wlo + q];
-            wave_lds_sync();
-            if (valid) {
-                uint32_t lo = 0, hi = wn;
-                while (lo < hi) {
-                    const uint32_t mid = (lo + hi) >> 1;
-                    if (win[w][mid] < i) lo = mid + 1;
-                    else hi = mid;
-                }
-                found = lo < wn && win[w][lo] == i;
-                pos = wlo + lo;
-            }
-            wave_lds_sync();
-        } else if (valid) {
-            pos = lower_bound_u32(list, wlo, whi, i);
-            found = pos < whi && list[pos] == i;
-        }
-        if (found) {
-            if (cc < c) owner = false;
-            else s = s + a.val[cc][pos];
-        }
+    __shared__ uint32_t rng[kMaxPushes][2];  // bucket's [begin, end) in each client's list
+    __shared__ uint32_t base[kMaxPushes + 1];  // first staged entry of each client
+    __shared__ uint32_t sidx[kApplyLds];
+    __shared__ float sval[kApplyLds];
+    const int tid = threadIdx.x, w = tid >> 6, lane = lane_id();
+    const uint32_t b = blockIdx.x;
+    const uint32_t i_lo = b << kApplyBucketShift;
+    const uint64_t i_hi64 = ((uint64_t)b + 1) << kApplyBucketShift;
+    const uint32_t i_hi = i_hi64 < a.n ? (uint32_t)i_hi64 : a.n;
+    // 1. the bucket's range in every list: one client per wave, the two bounds
+    //    by the two half-waves
+    const uint32_t half = (uint32_t)lane >> 5, g = (uint32_t)lane & 31u;
+    const uint64_t mask = half ? 0xFFFFFFFF00000000ull : 0x00000000FFFFFFFFull;
+    for (uint32_t c = w; c < a.C; c += kWavesPerBlock) {
+        const uint32_t pos = half_lower_bound(a.idx[c], 0, a.nnz[c], half ? i_hi : i_lo, g, mask);
+        if (g == 0) rng[c][half] = pos;
     }
-    if (valid && owner) {
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t acc = 0;
+        for (uint32_t c = 0; c < a.C; ++c) {
+            base[c] = acc;
+            acc += rng[c][1] - rng[c][0];
+        }
+        base[a.C] = acc;
+    }
+    __syncthreads();
+    const uint32_t total = base[a.C];
+    if (total == 0) return;
+    const bool staged = total <= (uint32_t)kApplyLds;
+    // 2. stage the bucket's entries (index, value) of every client
+    if (staged) {
+        for (uint32_t c = 0; c < a.C; ++c) {
+            const uint32_t r0 = rng[c][0], cnt = rng[c][1] - r0, o = base[c];
+            for (uint32_t q = tid; q < cnt; q += kBlock) {
+                sidx[o + q] = a.idx[c][r0 + q];
+                sval[o + q] = a.val[c][r0 + q];
+            }
+        }
+        __syncthreads();
+    }
+    // 3. each entry: skip it if a lower client holds the same index, else sum
+    //    every client's value for it in client order and update p once
+    for (uint32_t e = tid; e < total; e += kBlock) {
+        uint32_t c = 0;
+        while (base[c + 1] <= e) ++c;  // client of staged entry e
+        const uint32_t q = e - base[c];
+        const uint32_t i = staged ? sidx[e] : a.idx[c][rng[c][0] + q];
+        bool owner = true;
+        for (uint32_t cc = 0; cc < c && owner; ++cc) {
+            const uint32_t hit = staged ? find_u32(sidx, base[cc], base[cc + 1], i)
+                                        : find_u32(a.idx[cc], rng[cc][0], rng[cc][1], i);
+            owner = staged ? hit == base[cc + 1] : hit == rng[cc][1];
+        }
+        if (!owner) continue;
+        float s = 0.0f;
+        for (uint32_t cc = 0; cc < a.C; ++cc) {
+            if (cc < c) continue;
+            if (cc == c) {
+                s = s + (staged ? sval[e] : a.val[c][rng[c][0] + q]);
+                continue;
+            }
+            if (staged) {
+                const uint32_t hit = find_u32(sidx, base[cc], base[cc + 1], i);
+                if (hit != base[cc + 1]) s = s + sval[hit];
+            } else {
+                const uint32_t hit = find_u32(a.idx[cc], rng[cc][0], rng[cc][1], i);
+                if (hit != rng[cc][1]) s = s + a.val[cc][hit];
+            }
+        }
         const float step = a.lr * s;
         a.p[i] = a.p[i] - step;
     }
 }
 
 hipError_t launch_apply(const ApplyArgs& a, uint32_t max_nnz, hipStream_t st) {
-    if (a.C == 0 || max_nnz == 0) return hipSuccess;
-    dim3 grid((max_nnz + kBlock - 1) / kBlock, a.C);
-    hipLaunchKernelGGL(k_apply, grid, dim3(kBlock), 0, st, a);
+    if (a.C == 0 || max_nnz == 0 || a.n == 0) return hipSuccess;
+    const uint32_t buckets = (uint32_t)(((uint64_t)a.n + (1u << kApplyBucketShift) - 1) >> kApplyBucketShift);
+    hipLaunchKernelGGL(k_apply, dim3(buckets), dim3(kBlock), 0, st, a);
     return hipGetLastError();
 }
 

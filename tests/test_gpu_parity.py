@@ -201,6 +201,33 @@ def test_apply_small(C, dup, lr):
     _apply_case(60_000, C, 1500, dup, seed=C, lr=lr)
 
 
+def test_apply_dense_buckets_and_many_clients():
+    # buckets too full for the staged (LDS) path: about 28,000 entries per bucket
+    _apply_case(70_000, 4, 15_000, 0.3, seed=11)
+    # the most clients one call takes, heavy sharing, a ragged last bucket
+    _apply_case(100_003, 64, 40, 0.5, seed=12, lr=0.5)
+
+
+def test_apply_skips_out_of_range_and_empty_pushes():
+    rng = np.random.default_rng(13)
+    n = 40_000
+    p0 = rng.normal(0, 0.1, n).astype(np.float32)
+    a = np.sort(rng.choice(n, 3000, replace=False)).astype(np.uint32)
+    b = np.sort(np.concatenate([rng.choice(a, 500, replace=False),
+                                rng.choice(np.setdiff1d(np.arange(n), a), 500, replace=False)])).astype(np.uint32)
+    b_out = np.concatenate([b, np.array([n, n + 7, 2 ** 31], np.uint32)])  # entries past the shard are skipped
+    va = rng.normal(0, 1e-3, a.size).astype(np.float32)
+    vb = rng.normal(0, 1e-3, b_out.size).astype(np.float32)
+    empty_i, empty_v = np.zeros(0, np.uint32), np.zeros(0, np.float32)
+    want = oracle.apply_sparse(p0, [a, empty_i, b], [va, empty_v, vb[:b.size]], 1.0)
+    p = torch.from_numpy(p0).cuda()
+    idx = [torch.from_numpy(x.view(np.int32)).cuda() for x in (a, empty_i, b_out)]
+    val = [torch.from_numpy(x).cuda() for x in (va, empty_v, vb)]
+    gd.apply_sparse(p, idx, val, 1.0)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(p.cpu().numpy()), bits(want))
+
+
 def test_apply_and_pull_full_shard():
     cfg = wl.SHARD_FULL
     s, p1 = _apply_case(cfg["n"], cfg["clients"], cfg["nnz"], cfg["dup_frac"], cfg["seed"])
