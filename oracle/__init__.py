@@ -50,6 +50,8 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.gdo_compress.restype = i32
     lib.gdo_apply_sparse.argtypes = [vp, u64, u32, vp, vp, vp, f32]
     lib.gdo_apply_sparse.restype = i32
+    lib.gdo_compress_pull.argtypes = [vp, vp, vp, u32, dbl, i32, vp, vp, vp, u64, ctypes.POINTER(u64)]
+    lib.gdo_compress_pull.restype = i32
     lib.gdo_splitmix64.argtypes = [u64, u64]
     lib.gdo_splitmix64.restype = u64
     lib.gdo_sample_position.argtypes = [u64, u32, u64, u64, u64, u64]
@@ -143,6 +145,29 @@ def compress(
     k = int(k.value)
     return Compressed(idx[:k].copy(), val[:k].copy(), r, counts,
                       None if bits is None else bits[:(k + 31) // 32].copy(), means)
+
+
+def compress_pull(params: np.ndarray, copy: np.ndarray, offsets: Sequence[int], drop_ratio: float = 0.99,
+                  per_tensor: bool = False, lib: Optional[ctypes.CDLL] = None):
+    """A pull as a delta from the last pulled copy (R11): returns (Compressed with
+    idx/val/tensor_counts, the updated copy); inputs are not modified."""
+    lib = lib or load()
+    p = np.ascontiguousarray(params, dtype=np.float32)
+    c = np.array(copy, dtype=np.float32, copy=True)
+    off = np.ascontiguousarray(offsets, dtype=np.uint64)
+    T = off.size - 1
+    assert off[-1] == p.size == c.size
+    cap = int(p.size)
+    idx = np.zeros(max(cap, 1), np.uint32)
+    val = np.zeros(max(cap, 1), np.float32)
+    counts = np.zeros(T, np.uint32)
+    k = ctypes.c_uint64(0)
+    rc = lib.gdo_compress_pull(_ptr(p), _ptr(c), _ptr(off), T, float(drop_ratio), int(per_tensor), _ptr(idx),
+                               _ptr(val), _ptr(counts), cap, ctypes.byref(k))
+    if rc != 0:
+        raise ValueError(f"gdo_compress_pull failed with status {rc}")
+    k = int(k.value)
+    return Compressed(idx[:k].copy(), val[:k].copy(), None, counts, None, None), c
 
 
 def splitmix64(seed: int, i: int, lib: Optional[ctypes.CDLL] = None) -> int:

@@ -49,6 +49,12 @@
 //         positives and negatives are averaged separately, pairs stored for
 //         the columns of tensor 0, then tensor 1, ... (columns NULL: one
 //         column per tensor, which is R5).
+//   R11 pull with the last pulled copy (Section 4, paragraph on pulls: the
+//       server stores the copy a client last pulled and sends deltas from
+//       it): acc = p - copy (one float rounding, no residual buffer: what is
+//       not sent stays in the difference), the same exact selection as R2,
+//       (idx, acc) sent, and the copy becomes what the client holds after
+//       adding the sent values: copy[kept] = copy[kept] + acc.
 //   R9  sampled threshold (Section 4: select on a 0.1% sample of the
 //       gradient, then keep what lies strictly above the threshold):
 //       segment s of n entries draws m = ceil(n * sample_ppm / 1e6)
@@ -82,6 +88,54 @@ inline uint32_t key_of(float x) {
 #else
     return b & 0x7FFFFFFFu;
 #endif
+}
+
+}  // namespace
+extern "C" uint64_t gdo_keep_count(uint64_t n, double drop_ratio);
+namespace {
+uint64_t keep_count_of(uint64_t n, double drop_ratio) { return gdo_keep_count(n, drop_ratio); }
+
+// Algorithm 1, threshold selection and the keep mask (R2): in each segment
+// the k largest keys, equal keys in ascending index.
+std::vector<uint8_t> exact_keep(const std::vector<float>& acc, const std::vector<std::pair<uint64_t, uint64_t>>& seg,
+                                double drop_ratio) {
+    const uint64_t N = acc.size();
+    (void)N;
+    std::vector<uint8_t> keep(acc.size(), 0);
+    for (auto& s : seg) {
+        const uint64_t n = s.second - s.first;
+#ifdef GDO_MUTANT_GLOBAL_K_PER_TENSOR
+        const uint64_t k = std::min<uint64_t>(n, keep_count_of(N, drop_ratio) / seg.size());
+#else
+        const uint64_t k = keep_count_of(n, drop_ratio);
+#endif
+        if (k == 0) continue;
+        std::vector<uint32_t> keys(n);
+        for (uint64_t i = 0; i < n; ++i) keys[i] = key_of(acc[s.first + i]);
+        std::nth_element(keys.begin(), keys.begin() + (k - 1), keys.end(), std::greater<uint32_t>());
+        const uint32_t thr = keys[k - 1];  // the k-th largest key
+        uint64_t above = 0;
+        for (uint64_t i = s.first; i < s.second; ++i) above += key_of(acc[i]) > thr;
+        uint64_t ties_left = k - above;  // entries equal to thr still to take
+#ifdef GDO_MUTANT_STRICT_ONLY
+        ties_left = 0;  // mutant: Algorithm 1's strict ">" without the exact-k rule
+#endif
+#ifdef GDO_MUTANT_TIES_HIGH_INDEX
+        for (uint64_t i = s.second; i-- > s.first;) {
+#else
+        for (uint64_t i = s.first; i < s.second; ++i) {
+#endif
+            const uint32_t kk = key_of(acc[i]);
+            if (kk > thr) {
+                keep[i] = 1;
+            } else if (kk == thr && ties_left > 0) {
+                keep[i] = 1;
+                --ties_left;
+            }
+        }
+    }
+
+    return keep;
 }
 
 }  // namespace
@@ -162,40 +216,7 @@ int gdo_compress(const float* grad, const float* base, float* residual, const ui
 #endif
     }
 
-    // Algorithm 1, threshold selection and the keep mask (R2).
-    std::vector<uint8_t> keep(N, 0);
-    for (auto& s : seg) {
-        const uint64_t n = s.second - s.first;
-#ifdef GDO_MUTANT_GLOBAL_K_PER_TENSOR
-        const uint64_t k = std::min<uint64_t>(n, gdo_keep_count(N, drop_ratio) / seg.size());
-#else
-        const uint64_t k = gdo_keep_count(n, drop_ratio);
-#endif
-        if (k == 0) continue;
-        std::vector<uint32_t> keys(n);
-        for (uint64_t i = 0; i < n; ++i) keys[i] = key_of(acc[s.first + i]);
-        std::nth_element(keys.begin(), keys.begin() + (k - 1), keys.end(), std::greater<uint32_t>());
-        const uint32_t thr = keys[k - 1];  // the k-th largest key
-        uint64_t above = 0;
-        for (uint64_t i = s.first; i < s.second; ++i) above += key_of(acc[i]) > thr;
-        uint64_t ties_left = k - above;  // entries equal to thr still to take
-#ifdef GDO_MUTANT_STRICT_ONLY
-        ties_left = 0;  // mutant: Algorithm 1's strict ">" without the exact-k rule
-#endif
-#ifdef GDO_MUTANT_TIES_HIGH_INDEX
-        for (uint64_t i = s.second; i-- > s.first;) {
-#else
-        for (uint64_t i = s.first; i < s.second; ++i) {
-#endif
-            const uint32_t kk = key_of(acc[i]);
-            if (kk > thr) {
-                keep[i] = 1;
-            } else if (kk == thr && ties_left > 0) {
-                keep[i] = 1;
-                --ties_left;
-            }
-        }
-    }
+    std::vector<uint8_t> keep = exact_keep(acc, seg, drop_ratio);
 
     // Algorithm 1, sparse(dropped): ascending flat indices and values.
     uint64_t j = 0;
@@ -346,6 +367,57 @@ int gdo_compress(const float* grad, const float* base, float* residual, const ui
 #endif
             const float sent = neg ? means[2 * group[q] + 1] : means[2 * group[q] + 0];
             residual[idx[q]] = val[q] - sent;
+        }
+    }
+    return 0;
+}
+
+// Section 4, pulls as deltas from the last pulled copy (R11).  params (N),
+// copy (N, read and rewritten), outputs as gdo_compress without quantisation.
+// Returns 0 on success, 1 on bad arguments, 3 when capacity is too small.
+int gdo_compress_pull(const float* params, float* copy, const uint64_t* offsets, uint32_t T, double drop_ratio,
+                      int per_tensor, uint32_t* idx, float* val, uint32_t* tensor_counts, uint64_t capacity,
+                      uint64_t* out_k) {
+    if (!params || !copy || !offsets || T == 0 || !idx || !val || !tensor_counts) return 1;
+    if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return 1;
+    const uint64_t N = offsets[T];
+    if (offsets[0] != 0 || N > 0xFFFFFFFFull) return 1;
+    for (uint32_t t = 0; t < T; ++t)
+        if (offsets[t + 1] < offsets[t]) return 1;
+    std::vector<std::pair<uint64_t, uint64_t>> seg;
+    if (per_tensor) {
+        for (uint32_t t = 0; t < T; ++t) seg.push_back({offsets[t], offsets[t + 1]});
+    } else {
+        seg.push_back({0, N});
+    }
+    uint64_t k_total = 0;
+    for (auto& sg : seg) k_total += gdo_keep_count(sg.second - sg.first, drop_ratio);
+    if (out_k) *out_k = k_total;
+    if (capacity < k_total) return 3;
+    // the delta from the last pulled copy
+    std::vector<float> acc(N);
+    for (uint64_t i = 0; i < N; ++i) {
+#ifdef GDO_MUTANT_PULL_ADDS_ZERO
+        acc[i] = (params[i] - copy[i]) + 0.0f;  // mutant: an added zero residual turns -0 into +0
+#else
+        acc[i] = params[i] - copy[i];
+#endif
+    }
+    std::vector<uint8_t> keep = exact_keep(acc, seg, drop_ratio);
+    uint64_t j = 0;
+    for (uint32_t t = 0; t < T; ++t) tensor_counts[t] = 0;
+    for (uint32_t t = 0; t < T; ++t) {
+        for (uint64_t i = offsets[t]; i < offsets[t + 1]; ++i) {
+            if (!keep[i]) continue;
+            idx[j] = (uint32_t)i;
+            val[j] = acc[i];
+            ++j;
+            ++tensor_counts[t];
+#ifdef GDO_MUTANT_PULL_COPY_IS_P
+            copy[i] = params[i];  // mutant: assumes the client ends up holding p exactly
+#else
+            copy[i] = copy[i] + acc[i];  // what the client holds after adding the sent delta
+#endif
         }
     }
     return 0;

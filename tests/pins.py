@@ -406,6 +406,40 @@ def pin_quant_column_limits(lib):
         assert np.array_equal(bits(c.val), bits((g + r)[c.idx]))
 
 
+def pin_pull_copy(lib):
+    """Pulls from the last pulled copy (Section 4): the delta sent and what the copy becomes."""
+    rng = np.random.default_rng(14)
+    offsets = [0, 3000, 3005, 8000]
+    N = offsets[-1]
+    copy0 = rng.normal(0, 0.1, N).astype(np.float32)
+    p = (copy0 * (1 + rng.normal(0, 1e-2, N))).astype(np.float32)  # within a factor 2: p - copy is exact
+    for per in (False, True):
+        out, copy1 = oracle.compress_pull(p, copy0, offsets, 0.99, per_tensor=per, lib=lib)
+        # the sent part is Algorithm 1 on the delta (the exact mode, pinned by brute force)
+        ref = oracle.compress(p, np.zeros(N, np.float32), offsets, 0.99, per_tensor=per, base=copy0, lib=lib)
+        assert np.array_equal(out.idx, ref.idx) and np.array_equal(bits(out.val), bits(ref.val))
+        # Sterbenz: the delta is exact, so the client (copy + sent) holds p exactly where sent
+        assert np.array_equal(bits(copy1[out.idx]), bits(p[out.idx]))
+        unsent = np.ones(N, bool)
+        unsent[out.idx] = False
+        assert np.array_equal(bits(copy1[unsent]), bits(copy0[unsent]))
+    # scales far apart: the client holds copy + fl32(p - copy), which is not p
+    c = f32([1.0, 1.0, -2.0, 3.0])
+    q = f32([1e-8, 5.0, -2.0 - 2.0 ** -22, 3.0])
+    out, c1 = oracle.compress_pull(q, c, [0, 4], 0.5, lib=lib)  # k = 2: |delta| 4.0 and 1.0 - 1e-8
+    assert out.idx.tolist() == [0, 1]
+    assert bits(out.val).tolist() == bits(f32([-1.0, 4.0])).tolist()  # 1e-8 - 1 rounds to -1
+    assert bits(c1).tolist() == bits(f32([0.0, 5.0, -2.0, 3.0])).tolist()
+    # a delta of -0 is sent as -0 (no residual is added to it)
+    out, _ = oracle.compress_pull(f32([-0.0, 1.0]), f32([0.0, 0.0]), [0, 2], 0.0, lib=lib)
+    assert bits(out.val).tolist() == [0x80000000, bits(f32([1.0]))[0]]
+    # pulling a fixed p repeatedly at 50% drains the difference (Sterbenz holds)
+    cc = copy0.copy()
+    for _ in range(40):
+        _, cc = oracle.compress_pull(p, cc, offsets, 0.5, lib=lib)
+    assert np.array_equal(bits(cc), bits(p))
+
+
 def pin_apply_exact(lib):
     rng = np.random.default_rng(5)
     n = 5000
@@ -608,6 +642,7 @@ ALL_PINS = [
     pin_quant_other_centres,
     pin_quant_column_limits,
     pin_apply_exact,
+    pin_pull_copy,
     pin_pull_delta,
     pin_splitmix64_reference,
     pin_sample_positions,

@@ -32,6 +32,8 @@ MUTANTS = [
     "GDO_MUTANT_THRESHOLD_MAX",
     "GDO_MUTANT_GLOBAL_MEAN_PER_TENSOR",
     "GDO_MUTANT_COLUMN_IS_ROW",
+    "GDO_MUTANT_PULL_ADDS_ZERO",
+    "GDO_MUTANT_PULL_COPY_IS_P",
 ]
 
 
