@@ -41,6 +41,9 @@ def parse():
                          "selected on a sample (gd_compress_sampled, Section 4)")
     ap.add_argument("--quant", choices=("workload",) + tuple(QUANT_KINDS), default="workload",
                     help="1-bit centres of Section 5.4 (default: the workload's own)")
+    ap.add_argument("--pull", choices=("residual", "copy"), default="residual",
+                    help="shard_apply_pull: the pull delta with a residual (gd_compress with a base) or from "
+                         "the last pulled copy (gd_compress_pull)")
     ap.add_argument("--sample-ppm", type=int, default=1000,
                     help="sample size per million entries for --selection sampled (1000 = 0.1%%)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=12.0,
@@ -159,17 +162,24 @@ def main_shard(args, torch, np, gd, wl):
     out = comp.alloc_out(drop, False)
     entries = sum(int(a.size) for a in sh.idx)
 
+    use_copy = args.pull == "copy"
+
     def step(i):
         gd.apply_sparse(p, idx, val, lr=1.0)
-        comp.compress(p, pull_res, drop, per_tensor=False, base=p_last, out=out)
+        if use_copy:
+            comp.compress_pull(p, p_last, drop, per_tensor=False, out=out)
+        else:
+            comp.compress(p, pull_res, drop, per_tensor=False, base=p_last, out=out)
 
     # parity of step 0 (apply, then the pull) against the oracle
     step(0)
     torch.cuda.synchronize()
     first_p = p.cpu().numpy().copy()
     first_idx = out.idx[:k].cpu().numpy().view(np.uint32).copy()
-    first_res = pull_res.cpu().numpy().copy()
-    p.copy_(p_last)
+    first_res = (p_last if use_copy else pull_res).cpu().numpy().copy()
+    p0 = torch.from_numpy(sh.params).cuda()
+    p.copy_(p0)
+    p_last.copy_(p0)
     pull_res.zero_()
     for i in range(args.warmup):
         step(i)
@@ -185,8 +195,9 @@ def main_shard(args, torch, np, gd, wl):
     comp.profile_enable(False)
     sec = (t1 - t0) / args.steps
     dense_avg_s = dense_ms / 1e3 / max(dense_n, 1)
-    achieved = 16 * N / dense_avg_s / 1e9  # grad, base and residual read, residual written
-    model_bytes = 16 * entries + 16 * N + 8 * k
+    dense_bytes = 8 if use_copy else 16  # params and copy read; or params, base and residual read, residual written
+    achieved = dense_bytes * N / dense_avg_s / 1e9
+    model_bytes = 16 * entries + dense_bytes * N + 8 * k
     line = {
         "metric": METRIC,
         "value": round(N / sec / 1e9, 3),
@@ -209,10 +220,11 @@ def main_shard(args, torch, np, gd, wl):
             "kept_per_step": k,
             "threshold": "global",
             "drop": drop,
-            "byte_model": "16 B/push entry + 16 B/element (pull delta with residual) + 8 B/kept element",
+            "pull": "from the last pulled copy" if use_copy else "delta with a carried residual",
+            "byte_model": f"16 B/push entry + {dense_bytes} B/element + 8 B/kept element",
         },
         "roofline": {
-            "kernel": "k_dense<true>",
+            "kernel": "k_dense<2>" if use_copy else "k_dense<1>",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
@@ -229,7 +241,11 @@ def main_shard(args, torch, np, gd, wl):
         lib = oracle.load()
         t0 = time.perf_counter()
         p1 = oracle.apply_sparse(sh.params, sh.idx, sh.val, 1.0, lib=lib)
-        o = oracle.compress(p1, np.zeros(N, np.float32), [0, N], drop, base=sh.params, lib=lib)
+        if use_copy:
+            o, want_state = oracle.compress_pull(p1, sh.params, [0, N], drop, lib=lib)
+        else:
+            o = oracle.compress(p1, np.zeros(N, np.float32), [0, N], drop, base=sh.params, lib=lib)
+            want_state = o.residual
         el = time.perf_counter() - t0
         line["cpu_baseline"] = {
             "value": N / el / 1e9, "unit": "G grad-elements/s", "cores": 1, "kind": "oracle",
@@ -238,7 +254,7 @@ def main_shard(args, torch, np, gd, wl):
         }
         line["parity_step0"] = bool(np.array_equal(p1.view(np.uint32), first_p.view(np.uint32)) and
                                     np.array_equal(o.idx, first_idx) and
-                                    np.array_equal(o.residual.view(np.uint32), first_res.view(np.uint32)))
+                                    np.array_equal(want_state.view(np.uint32), first_res.view(np.uint32)))
     print(json.dumps(line), flush=True)
 
 

@@ -134,6 +134,25 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
                       void* stream);
 
 /*
+ * gd_compress_pull - a parameter pull sent as a delta from the client's last
+ * pulled copy (Section 4, paragraph on pulls: the server stores that copy and
+ * compresses the difference like any other transmission).
+ *   params (device, N floats): the server's current parameters.
+ *   copy (device, N floats, in/out): what the client holds, as of its last
+ *     pull.  acc = params - copy (one binary32 subtraction); the k entries of
+ *     largest |acc| are selected exactly as by gd_compress (ties to the lower
+ *     index, global or per tensor) and sent as (index, acc); then
+ *     copy[i] += acc[i] at every sent entry, so that copy again equals what
+ *     the client holds after adding the sent values.  There is no residual
+ *     buffer: what is not sent remains in params - copy.
+ *   out: as gd_compress without quantisation (sign_bits, means ignored).
+ *   params and copy must be 16-byte aligned and must not overlap each other
+ *   or the outputs.  Errors as gd_compress.
+ */
+gd_status gd_compress_pull(gd_ctx* ctx, const float* params, float* copy, double drop_ratio, gd_threshold mode,
+                           const gd_sparse* out, void* stream);
+
+/*
  * gd_set_columns - the matrix view used by GD_QUANT_COLUMN_MEAN (Section 5.4:
  * centres per column rather than chosen globally).
  *   columns (host, T entries): tensor t is a row-major matrix of columns[t]

@@ -164,6 +164,10 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     ca.tile_q = ctx->scr.tile_q;
     ca.out_base = ctx->scr.out_base;
     ca.sampled = sampled ? 1u : 0u;
+    if (!residual) {  // a pull from the last pulled copy (base)
+        ca.pull_p = grad;
+        ca.pull_copy = const_cast<float*>(base);
+    }
     gd::EmitArgs ea{};
     ea.idx = out->idx;
     ea.val = out->val;
@@ -379,6 +383,41 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
     if (gd::launch_sample(sa, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
 
     return run_after_bracket(ctx, grad, base, residual, per, ppm, false, quant, k_total, out, st);
+}
+
+gd_status gd_compress_pull(gd_ctx* ctx, const float* params, float* copy, double drop_ratio, gd_threshold mode,
+                           const gd_sparse* out, void* stream) {
+    if (!ctx || !params || !copy || !out) return GD_ERR_ARG;
+    if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
+    if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
+    if (!out->idx || !out->val || !out->tensor_counts) return GD_ERR_ARG;
+    if (!aligned16(params) || !aligned16(copy)) return GD_ERR_ALIGN;
+    const uint64_t k_total = gd_keep_total(ctx, drop_ratio, mode);
+    if (out->capacity < k_total) return GD_ERR_CAPACITY;
+
+    DeviceGuard guard(ctx->device);
+    if (!guard.ok) return GD_ERR_HIP;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool per = mode == GD_PER_TENSOR;
+    const uint32_t ppm = (uint32_t)keep_ppm_of(drop_ratio);
+    gd::SampleArgs sa{};
+    sa.grad = params;
+    sa.base = copy;
+    sa.res = nullptr;  // acc = params - copy
+    sa.seg_off = per ? ctx->tab.tensor_off : ctx->tab.global_off;
+    sa.skey_base = per ? ctx->tab.skey_base_tensor : ctx->tab.skey_base_global;
+    sa.S = per ? ctx->T : 1u;
+    sa.T = ctx->T;
+    sa.keep_ppm = ppm;
+    sa.debug_bracket = ctx->debug_bracket;
+    sa.skeys = ctx->scr.skeys;
+    sa.seg = ctx->scr.seg;
+    sa.hist = ctx->scr.hist;
+    sa.shist = ctx->scr.shist;
+    sa.out_base = ctx->scr.out_base;
+    sa.tensor_counts = out->tensor_counts;
+    if (gd::launch_sample(sa, true, st) != hipSuccess) return GD_ERR_HIP;
+    return run_after_bracket(ctx, params, copy, nullptr, per, ppm, false, GD_QUANT_NONE, k_total, out, st);
 }
 
 gd_status gd_set_columns(gd_ctx* ctx, const uint32_t* columns) {

@@ -137,7 +137,9 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
             for (int r = 0; r < kRows; ++r) {
                 const uint32_t pl = v.p0 + r * kWave + lane;
                 ix[r] = e_base + pl;
-                const uint32_t x = __float_as_uint(a.res[e_base + (pl < v.p1 ? pl : v.p0)]);
+                const uint32_t e = e_base + (pl < v.p1 ? pl : v.p0);
+                // acc is the restored residual, or for a pull from the copy p - copy
+                const uint32_t x = __float_as_uint(a.res ? a.res[e] : a.pull_p[e] - a.pull_copy[e]);
                 vb[r] = pl < v.p1 ? x : 0u;
             }
         } else {
@@ -399,14 +401,20 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         // the cache holds whole.  A lone partial-line write reaches HBM as a
         // read-modify-write when the line is evicted, which the next dense
         // pass pays for many times over.
+        // A pull from the copy instead reads the copy word of every entry that
+        // may be kept, to add the sent value to it.
+        const bool pull = a.res == nullptr;
         float old[kRows];
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
             const uint32_t key = vb[r] & 0x7FFFFFFFu;
             const bool valid = v.p0 + r * kWave + lane < v.p1;
             old[r] = 0.0f;
-            if (valid && ((key > thr) != (key >= hi) || key == thr))
+            if (pull) {
+                if (valid && key >= thr) old[r] = a.pull_copy[ix[r]];
+            } else if (valid && ((key > thr) != (key >= hi) || key == thr)) {
                 old[r] = *reinterpret_cast<const volatile float*>(a.res + ix[r]);
+            }
         }
         // candidates above / equal to the threshold in earlier tiles of the segment
         uint32_t bg = 0, be = 0;
@@ -465,10 +473,15 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
                     }
                 }
             }
-            const bool wz = valid && key >= hi;
-            if (kept != wz) {
-                asm volatile("" ::"v"(old[r]));  // the line read above precedes the write
-                a.res[ix[r]] = kept ? 0.0f : __uint_as_float(vb[r]);
+            if (pull) {
+                // the client adds the sent value to what it holds; so does its copy
+                if (kept) a.pull_copy[ix[r]] = old[r] + __uint_as_float(vb[r]);
+            } else {
+                const bool wz = valid && key >= hi;
+                if (kept != wz) {
+                    asm volatile("" ::"v"(old[r]));  // the line read above precedes the write
+                    a.res[ix[r]] = kept ? 0.0f : __uint_as_float(vb[r]);
+                }
             }
             bg += popc64(mg);
             be += popc64(me);

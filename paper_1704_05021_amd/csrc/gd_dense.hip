@@ -8,7 +8,8 @@
 // elements whose key reaches the sampled bracket (key >= lo) to per-unit
 // slots in ascending index order.  Elements with key >= hi are almost
 // surely kept, so their residual is written as +0 now; the emit pass fixes
-// the few that end up on the other side of the exact threshold.
+// the few that end up on the other side of the exact threshold.  A pull from
+// the last pulled copy has no residual: it reads params and the copy only.
 //
 // A unit is the 1024 elements [1024u, 1024u + 1024) of the flat gradient,
 // one block of 256 threads with one 16-byte vector per thread, so every
@@ -44,8 +45,12 @@ __device__ __forceinline__ uint32_t tensor_of(const uint32_t* off, uint32_t T, u
     return lo;
 }
 
-template <bool BASE>
+// MODE 0: acc = grad + residual; 1: (grad - base) + residual (a pull with a
+// residual); 2: grad - base with no residual at all (a pull from the last
+// pulled copy, which keeps the unsent difference itself).
+template <int MODE>
 __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
+    constexpr bool BASE = MODE >= 1, NORES = MODE == 2;
     const uint32_t u = blockIdx.x;
     const int tid = threadIdx.x, w = tid >> 6, lane = lane_id();
     const uint32_t ustart = u * kUnitLen;
@@ -56,14 +61,14 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
     if (e0 + 4 <= uend) {
         g = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.grad) + (e0 >> 2));
         if (BASE) b = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.base) + (e0 >> 2));
-        r = reinterpret_cast<const f4*>(a.res)[e0 >> 2];
+        if (!NORES) r = reinterpret_cast<const f4*>(a.res)[e0 >> 2];
     } else {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             if (e0 + q < uend) {
                 g[q] = a.grad[e0 + q];
                 if (BASE) b[q] = a.base[e0 + q];
-                r[q] = a.res[e0 + q];
+                if (!NORES) r[q] = a.res[e0 + q];
             }
         }
     }
@@ -95,17 +100,19 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const bool valid = e0 + q < uend;
-        acc[q] = acc_of<BASE>(g[q], b[q], r[q]);
+        acc[q] = NORES ? g[q] - b[q] : acc_of<BASE>(g[q], b[q], r[q]);
         const uint32_t key = key_of(acc[q]);
         cand[q] = valid && key >= lo[q];
         ov[q] = (valid && key >= hi[q]) ? 0.0f : acc[q];
     }
-    if (e0 + 4 <= uend) {
-        reinterpret_cast<f4*>(a.res)[e0 >> 2] = ov;
-    } else {
+    if (!NORES) {
+        if (e0 + 4 <= uend) {
+            reinterpret_cast<f4*>(a.res)[e0 >> 2] = ov;
+        } else {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            if (e0 + q < uend) a.res[e0 + q] = ov[q];
+            for (int q = 0; q < 4; ++q)
+                if (e0 + q < uend) a.res[e0 + q] = ov[q];
+        }
     }
     // ordered compaction over the unit: waves in order, lanes in order, then
     // the four elements of a lane, into one contiguous list per unit (fewer
@@ -159,8 +166,9 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
 hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st) {
     if (a.num_units == 0) return hipSuccess;
     const dim3 grid(a.num_units);
-    if (has_base) hipLaunchKernelGGL(k_dense<true>, grid, dim3(kBlock), 0, st, a);
-    else hipLaunchKernelGGL(k_dense<false>, grid, dim3(kBlock), 0, st, a);
+    if (has_base && a.res == nullptr) hipLaunchKernelGGL(k_dense<2>, grid, dim3(kBlock), 0, st, a);
+    else if (has_base) hipLaunchKernelGGL(k_dense<1>, grid, dim3(kBlock), 0, st, a);
+    else hipLaunchKernelGGL(k_dense<0>, grid, dim3(kBlock), 0, st, a);
     return hipGetLastError();
 }
 

@@ -106,6 +106,8 @@ struct CandArgs {
     uint64_t* out_base;   // [S] first output slot of each segment (the sampled mode writes it here)
     uint32_t* flags;      // [0]: some segment missed its bracket
     uint32_t sampled;     // sampled threshold: every candidate is kept, no bracket can miss
+    const float* pull_p;  // pull from the last pulled copy (res is then null): the parameters
+    float* pull_copy;     //   and the copy, which takes the sent values
 };
 
 // 1-bit centres (Section 5.4): per-tensor sign means, the dropping threshold,

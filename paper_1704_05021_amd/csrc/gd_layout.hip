@@ -191,7 +191,7 @@ __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
                 // direct tiles start at element offsets ta + j * kTile
                 const uint32_t lo_e = ta > ustart ? ta : ustart, hi_e = tb < uend ? tb : uend;
                 mark_tiles(a, t, ta, lo_e, hi_e, ne);
-                restore = restore || cnt > 0;
+                restore = restore || (cnt > 0 && a.res != nullptr);  // a pull from the copy zeroed nothing
             } else {
                 const uint32_t rb = a.raw_tbase[t], re = a.raw_tbase[t + 1];
                 const uint32_t p = raw > rb ? raw : rb, q = raw + cnt < re ? raw + cnt : re;

@@ -97,6 +97,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
     uint32_t k16[kUnit];
 #pragma unroll
     for (int q = 0; q < kUnit; ++q) k16[q] = kNoKey16;
+    const bool nores = a.res == nullptr;  // a pull from the last pulled copy has no residual
     if (j < U) {
         // stratum j: 16-element blocks [lo_j, hi_j) of the segment's aligned grid
         const uint32_t lo_j = (uint32_t)(((uint64_t)j * n16) / U);
@@ -106,13 +107,13 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
             // every block sampled: its 16 neighbours
             if (s0 >= seg_a && s0 + kUnit <= seg_b) {
                 const f4* g4 = reinterpret_cast<const f4*>(a.grad + s0);
-                const f4* r4 = reinterpret_cast<const f4*>(a.res + s0);
+                const f4* r4 = reinterpret_cast<const f4*>(nores ? a.grad + s0 : a.res + s0);
                 const f4* b4 = reinterpret_cast<const f4*>(BASE ? a.base + s0 : a.grad + s0);
                 f4 g[4], r[4], b[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     g[q] = g4[q];
-                    r[q] = r4[q];
+                    r[q] = nores ? f4{0.f, 0.f, 0.f, 0.f} : r4[q];
                     b[q] = BASE ? b4[q] : g[q];
                 }
 #pragma unroll
@@ -125,7 +126,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
                 for (int q = 0; q < kUnit; ++q) {
                     const uint32_t e = s0 + q;
                     if (e >= seg_a && e < seg_b)
-                        k16[q] = key16_of(key_of(acc_of<BASE>(a.grad[e], BASE ? a.base[e] : 0.0f, a.res[e])));
+                        k16[q] = key16_of(key_of(acc_of<BASE>(a.grad[e], BASE ? a.base[e] : 0.0f, nores ? 0.0f : a.res[e])));
                 }
             }
         } else {
@@ -137,7 +138,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
                 const uint32_t e = s0 + q * sub + (h % (sub / 4)) * 4;
                 if (e >= seg_a && e + 4 <= seg_b) {
                     const f4 g = *reinterpret_cast<const f4*>(a.grad + e);
-                    const f4 r = *reinterpret_cast<const f4*>(a.res + e);
+                    const f4 r = nores ? f4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<const f4*>(a.res + e);
                     const f4 b = BASE ? *reinterpret_cast<const f4*>(a.base + e) : g;
 #pragma unroll
                     for (int c = 0; c < 4; ++c) k16[4 * q + c] = key16_of(key_of(acc_of<BASE>(g[c], b[c], r[c])));
@@ -147,7 +148,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
                         const uint32_t x = e + c;
                         if (x >= seg_a && x < seg_b)
                             k16[4 * q + c] =
-                                key16_of(key_of(acc_of<BASE>(a.grad[x], BASE ? a.base[x] : 0.0f, a.res[x])));
+                                key16_of(key_of(acc_of<BASE>(a.grad[x], BASE ? a.base[x] : 0.0f, nores ? 0.0f : a.res[x])));
                     }
                 }
             }

@@ -37,6 +37,7 @@ EXPORTS = [
     "gd_compress",
     "gd_compress_sampled",
     "gd_set_columns",
+    "gd_compress_pull",
     "gd_quant_centres",
     "gd_apply_sparse",
     "gd_status_string",
@@ -88,6 +89,8 @@ def _lib() -> ctypes.CDLL:
     lib.gd_compress.restype = i32
     lib.gd_compress_sampled.argtypes = [vp, vp, vp, vp, dbl, i32, u32, u64, ctypes.POINTER(_Sparse), vp]
     lib.gd_compress_sampled.restype = i32
+    lib.gd_compress_pull.argtypes = [vp, vp, vp, dbl, i32, ctypes.POINTER(_Sparse), vp]
+    lib.gd_compress_pull.restype = i32
     lib.gd_set_columns.argtypes = [vp, vp]
     lib.gd_set_columns.restype = i32
     lib.gd_quant_centres.argtypes = [vp, i32]
@@ -216,6 +219,24 @@ class Compressor:
             int(quant), ctypes.byref(sp), _stream_handle(stream))
         if st != 0:
             raise GDError(st, "gd_compress")
+        out.k = self.keep_total(drop_ratio, per_tensor)
+        return out
+
+    def compress_pull(self, params: torch.Tensor, copy: torch.Tensor, drop_ratio: float = 0.99,
+                      per_tensor: bool = False, out: Optional[SparseOut] = None,
+                      stream: Optional[torch.cuda.Stream] = None) -> SparseOut:
+        """gd_compress_pull: send params - copy; ``copy`` takes the sent values in place."""
+        _check_f32(params, "params", self.N)
+        _check_f32(copy, "copy", self.N)
+        if out is None:
+            out = self.alloc_out(drop_ratio, per_tensor)
+        sp = _Sparse(out.idx.data_ptr(), out.val.data_ptr(), None, None, out.tensor_counts.data_ptr(),
+                     out.idx.numel())
+        st = _lib().gd_compress_pull(self._h, params.data_ptr(), copy.data_ptr(), float(drop_ratio),
+                                     GD_PER_TENSOR if per_tensor else GD_GLOBAL, ctypes.byref(sp),
+                                     _stream_handle(stream))
+        if st != 0:
+            raise GDError(st, "gd_compress_pull")
         out.k = self.keep_total(drop_ratio, per_tensor)
         return out
 
