@@ -50,6 +50,8 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.gdo_compress.restype = i32
     lib.gdo_apply_sparse.argtypes = [vp, u64, u32, vp, vp, vp, f32]
     lib.gdo_apply_sparse.restype = i32
+    lib.gdo_apply_quantised.argtypes = [vp, vp, u32, vp, u32, vp, vp, vp, vp, i32, f32]
+    lib.gdo_apply_quantised.restype = i32
     lib.gdo_compress_pull.argtypes = [vp, vp, vp, u32, dbl, i32, vp, vp, vp, u64, ctypes.POINTER(u64)]
     lib.gdo_compress_pull.restype = i32
     lib.gdo_splitmix64.argtypes = [u64, u64]
@@ -229,4 +231,28 @@ def apply_sparse(params: np.ndarray, idx: List[np.ndarray], val: List[np.ndarray
                               ctypes.cast(vptr, ctypes.c_void_p), _ptr(nnz) if C else None, float(lr))
     if rc != 0:
         raise ValueError(f"gdo_apply_sparse failed with status {rc}")
+    return p
+
+
+def apply_quantised(params: np.ndarray, offsets: Sequence[int], idx: List[np.ndarray], sign_bits: List[np.ndarray],
+                    means: List[np.ndarray], quant: int, lr: float = 1.0, columns: Optional[Sequence[int]] = None,
+                    lib: Optional[ctypes.CDLL] = None) -> np.ndarray:
+    """Server-side apply of quantised pushes (decoded per R12); returns the updated copy of ``params``."""
+    lib = lib or load()
+    p = np.array(params, dtype=np.float32, copy=True)
+    off = np.ascontiguousarray(offsets, dtype=np.uint64)
+    T = off.size - 1
+    C = len(idx)
+    ix = [np.ascontiguousarray(a, dtype=np.uint32) for a in idx]
+    bx = [np.ascontiguousarray(b, dtype=np.uint32) if b.size else np.zeros(1, np.uint32) for b in sign_bits]
+    mx = [np.ascontiguousarray(m, dtype=np.float32) for m in means]
+    cols = None if columns is None else np.ascontiguousarray(columns, dtype=np.uint32)
+    arr = lambda xs: (ctypes.c_void_p * max(C, 1))(*[a.ctypes.data for a in xs])
+    ip, bp, mp = arr(ix), arr(bx), arr(mx)
+    nnz = np.array([a.size for a in ix], dtype=np.uint64)
+    rc = lib.gdo_apply_quantised(_ptr(p), _ptr(off), T, _ptr(cols), C, ctypes.cast(ip, ctypes.c_void_p),
+                                 ctypes.cast(bp, ctypes.c_void_p), ctypes.cast(mp, ctypes.c_void_p),
+                                 _ptr(nnz) if C else None, int(quant), float(lr))
+    if rc != 0:
+        raise ValueError(f"gdo_apply_quantised failed with status {rc}")
     return p

@@ -55,6 +55,10 @@
 //       not sent stays in the difference), the same exact selection as R2,
 //       (idx, acc) sent, and the copy becomes what the client holds after
 //       adding the sent values: copy[kept] = copy[kept] + acc.
+//   R12 quantised pushes at the server (Section 3 with Section 5.4): entry j
+//       of a push decodes to the centre its sign bit (bit j%32 of word j/32)
+//       selects among the pair of its group (its tensor, or its column under
+//       column-wise centres), then the decoded pushes are applied as R6.
 //   R9  sampled threshold (Section 4: select on a 0.1% sample of the
 //       gradient, then keep what lies strictly above the threshold):
 //       segment s of n entries draws m = ceil(n * sample_ppm / 1e6)
@@ -421,6 +425,43 @@ int gdo_compress_pull(const float* params, float* copy, const uint64_t* offsets,
         }
     }
     return 0;
+}
+
+// Section 3 with Section 5.4: quantised pushes decoded, then applied (R12, R6).
+// The shard is the whole layout offsets[0..T]; quant 1..4 as gdo_compress
+// (columns only for quant 4, nullable).  Returns 0, or 1 on bad arguments.
+int gdo_apply_sparse(float* params, uint64_t n, uint32_t C, const uint32_t* const* idx,
+                     const float* const* val, const uint64_t* nnz, float lr);
+int gdo_apply_quantised(float* params, const uint64_t* offsets, uint32_t T, const uint32_t* columns, uint32_t C,
+                        const uint32_t* const* idx, const uint32_t* const* sign_bits, const float* const* means,
+                        const uint64_t* nnz, int quant, float lr) {
+    if (!params || !offsets || T == 0 || quant < 1 || quant > 4) return 1;
+    if (C && (!idx || !sign_bits || !means || !nnz)) return 1;
+    const uint64_t N = offsets[T];
+    std::vector<uint64_t> colbase(T + 1, 0);
+    for (uint32_t t = 0; t < T; ++t) colbase[t + 1] = colbase[t] + (quant == 4 && columns ? columns[t] : 1);
+    std::vector<std::vector<float>> dec(C);
+    std::vector<const float*> vp(C);
+    for (uint32_t c = 0; c < C; ++c) {
+        dec[c].resize(nnz[c]);
+        for (uint64_t j = 0; j < nnz[c]; ++j) {
+            const uint64_t i = idx[c][j];
+            if (i >= N) return 1;
+            // tensor holding i: the last t with offsets[t] <= i
+            uint32_t t = 0;
+            while (t + 1 < T && offsets[t + 1] <= i) ++t;
+            uint64_t g = t;
+            if (quant == 4) g = colbase[t] + (i - offsets[t]) % (columns ? columns[t] : 1);
+#ifdef GDO_MUTANT_DECODE_BITS_MSB
+            const bool neg = (sign_bits[c][j >> 5] >> (31 - (j & 31))) & 1u;  // mutant: bit order reversed
+#else
+            const bool neg = (sign_bits[c][j >> 5] >> (j & 31)) & 1u;
+#endif
+            dec[c][j] = means[c][2 * g + (neg ? 1 : 0)];
+        }
+        vp[c] = dec[c].data();
+    }
+    return gdo_apply_sparse(params, N, C, idx, vp.data(), nnz, lr);
 }
 
 // R9: output number i of SplitMix64 seeded with seed: the state advances by

@@ -440,6 +440,35 @@ def pin_pull_copy(lib):
     assert np.array_equal(bits(cc), bits(p))
 
 
+def pin_apply_quantised(lib):
+    """Quantised pushes decode to the centres each client subtracted (its error feedback), then sum as R6."""
+    rng = np.random.default_rng(15)
+    offsets = [0, 1200, 1210, 3000]
+    columns = [40, 10, 179]  # each divides its tensor (1790 = 10 * 179)
+    N = offsets[-1]
+    for quant in (1, 2, 3, 4):
+        cols = columns if quant == 4 else None
+        pushes = []
+        for c in range(3):
+            g = (rng.standard_t(3, N) * 1e-2).astype(np.float32)
+            out = oracle.compress(g, np.zeros(N, np.float32), offsets, 0.9, per_tensor=bool(c % 2), quant=quant,
+                                  columns=cols, lib=lib)
+            pushes.append((g, out))
+        decoded = []
+        for g, out in pushes:
+            # one push on p = 0 with lr = -1 leaves exactly the decoded values at the pushed indices
+            d = oracle.apply_quantised(np.zeros(N, np.float32), offsets, [out.idx], [out.sign_bits], [out.means],
+                                       quant, -1.0, columns=cols, lib=lib)[out.idx]
+            # the client kept acc - centre as its residual: the decode must give that centre back
+            assert np.array_equal(bits(out.val - d), bits(out.residual[out.idx])), quant
+            decoded.append(d)
+        p0 = rng.normal(0, 0.1, N).astype(np.float32)
+        got = oracle.apply_quantised(p0, offsets, [o.idx for _, o in pushes], [o.sign_bits for _, o in pushes],
+                                     [o.means for _, o in pushes], quant, 0.5, columns=cols, lib=lib)
+        want = oracle.apply_sparse(p0, [o.idx for _, o in pushes], decoded, 0.5, lib=lib)
+        assert np.array_equal(bits(got), bits(want)), quant
+
+
 def pin_apply_exact(lib):
     rng = np.random.default_rng(5)
     n = 5000
@@ -643,6 +672,7 @@ ALL_PINS = [
     pin_quant_column_limits,
     pin_apply_exact,
     pin_pull_copy,
+    pin_apply_quantised,
     pin_pull_delta,
     pin_splitmix64_reference,
     pin_sample_positions,

@@ -34,6 +34,7 @@ MUTANTS = [
     "GDO_MUTANT_COLUMN_IS_ROW",
     "GDO_MUTANT_PULL_ADDS_ZERO",
     "GDO_MUTANT_PULL_COPY_IS_P",
+    "GDO_MUTANT_DECODE_BITS_MSB",
 ]
 
 
