@@ -215,6 +215,26 @@ gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base,
 gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const uint32_t* const* idx,
                           const float* const* val, const uint64_t* nnz, float lr, void* stream);
 
+/*
+ * gd_apply_quantised - server-side apply of quantised pushes (Section 3 with
+ * Section 5.4): each push is what gd_compress sent under `quant` for the
+ * layout of ctx (the shard is the whole layout: N parameters).
+ *   params (device, N floats, in/out).
+ *   idx, sign_bits, means (host arrays of num_pushes device pointers): push c
+ *     has nnz[c] (host) ascending, unique indices below N, their sign bits
+ *     (bit j % 32 of word j / 32 set for a negative value) and its centre
+ *     pairs (gd_quant_centres(ctx, quant) floats; column-wise centres use the
+ *     columns of ctx, see gd_set_columns).
+ *   Entry j decodes to the negative centre of its tensor's (or column's) pair
+ *   when its bit is set, else the positive one; the decoded pushes are then
+ *   applied exactly as gd_apply_sparse does (sum in push order from +0.0,
+ *   params[i] -= lr * sum).  At most 64 pushes; GD_ERR_ARG for a NULL
+ *   pointer or quant GD_QUANT_NONE.
+ */
+gd_status gd_apply_quantised(gd_ctx* ctx, float* params, uint32_t num_pushes, const uint32_t* const* idx,
+                             const uint32_t* const* sign_bits, const float* const* means, const uint64_t* nnz,
+                             gd_quant quant, float lr, void* stream);
+
 /* Static description of a status code. */
 const char* gd_status_string(gd_status status);
 

@@ -508,6 +508,39 @@ gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const 
     return GD_OK;
 }
 
+gd_status gd_apply_quantised(gd_ctx* ctx, float* params, uint32_t num_pushes, const uint32_t* const* idx,
+                             const uint32_t* const* sign_bits, const float* const* means, const uint64_t* nnz,
+                             gd_quant quant, float lr, void* stream) {
+    if (!ctx || num_pushes > gd::kMaxPushes) return GD_ERR_ARG;
+    if (quant < GD_QUANT_SIGN_MEAN || quant > GD_QUANT_COLUMN_MEAN) return GD_ERR_ARG;
+    if (num_pushes == 0 || ctx->N == 0) return GD_OK;
+    if (!params || !idx || !sign_bits || !means || !nnz) return GD_ERR_ARG;
+    gd::ApplyArgs a{};
+    a.p = params;
+    a.n = (uint32_t)ctx->N;
+    a.C = num_pushes;
+    a.lr = lr;
+    a.qkind = (uint32_t)quant;
+    a.tensor_off = ctx->tab.tensor_off;
+    a.T = ctx->T;
+    a.columns = ctx->cols.columns;
+    a.colbase = ctx->cols.colbase;
+    uint32_t max_nnz = 0;
+    for (uint32_t c = 0; c < num_pushes; ++c) {
+        if (nnz[c] >= 0xFFFFFFFFull) return GD_ERR_ARG;
+        if (nnz[c] && (!idx[c] || !sign_bits[c] || !means[c])) return GD_ERR_ARG;
+        a.idx[c] = idx[c];
+        a.bits[c] = sign_bits[c];
+        a.means[c] = means[c];
+        a.nnz[c] = (uint32_t)nnz[c];
+        max_nnz = std::max(max_nnz, a.nnz[c]);
+    }
+    DeviceGuard guard(ctx->device);
+    if (!guard.ok) return GD_ERR_HIP;
+    if (gd::launch_apply(a, max_nnz, static_cast<hipStream_t>(stream)) != hipSuccess) return GD_ERR_HIP;
+    return GD_OK;
+}
+
 gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode) {
     if (!ctx || mode < 0 || mode > 4) return GD_ERR_ARG;
     ctx->debug_bracket = (uint32_t)mode;

@@ -12,6 +12,8 @@
 // those entries in LDS, and then gives every index to the lowest client
 // holding it, which sums all clients' values for it in client order and
 // writes p once.  The parameter writes of a block stay inside its bucket.
+// Quantised pushes (indices, sign bits, centre pairs; Section 5.4) are decoded
+// entry by entry where their values are read.
 
 #include "gd_kernels.h"
 
@@ -53,6 +55,21 @@ __device__ __forceinline__ uint32_t find_u32(const uint32_t* list, uint32_t lo, 
     return a < hi && list[a] == x ? a : hi;
 }
 
+// Value of entry pos (index i) of push c: sent as is, or a quantised push's
+// centre, chosen by the entry's sign bit from the pair of its tensor or column.
+__device__ __forceinline__ float push_val(const ApplyArgs& a, uint32_t c, uint32_t pos, uint32_t i) {
+    if (a.qkind == 0) return a.val[c][pos];
+    uint32_t lo = 0, hi = a.T;  // tensor holding i: the last t with tensor_off[t] <= i
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (a.tensor_off[mid] <= i) lo = mid;
+        else hi = mid;
+    }
+    const uint32_t g = a.qkind == kQuantColumnMean ? a.colbase[lo] + (i - a.tensor_off[lo]) % a.columns[lo] : lo;
+    const uint32_t neg = (a.bits[c][pos >> 5] >> (pos & 31)) & 1u;
+    return a.means[c][2 * g + neg];
+}
+
 __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
     __shared__ uint32_t rng[kMaxPushes][2];  // bucket's [begin, end) in each client's list
     __shared__ uint32_t base[kMaxPushes + 1];  // first staged entry of each client
@@ -89,8 +106,9 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
         for (uint32_t c = 0; c < a.C; ++c) {
             const uint32_t r0 = rng[c][0], cnt = rng[c][1] - r0, o = base[c];
             for (uint32_t q = tid; q < cnt; q += kBlock) {
-                sidx[o + q] = a.idx[c][r0 + q];
-                sval[o + q] = a.val[c][r0 + q];
+                const uint32_t ii = a.idx[c][r0 + q];
+                sidx[o + q] = ii;
+                sval[o + q] = push_val(a, c, r0 + q, ii);
             }
         }
         __syncthreads();
@@ -113,7 +131,7 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
         for (uint32_t cc = 0; cc < a.C; ++cc) {
             if (cc < c) continue;
             if (cc == c) {
-                s = s + (staged ? sval[e] : a.val[c][rng[c][0] + q]);
+                s = s + (staged ? sval[e] : push_val(a, c, rng[c][0] + q, i));
                 continue;
             }
             if (staged) {
@@ -121,7 +139,7 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
                 if (hit != base[cc + 1]) s = s + sval[hit];
             } else {
                 const uint32_t hit = find_u32(a.idx[cc], rng[cc][0], rng[cc][1], i);
-                if (hit != rng[cc][1]) s = s + a.val[cc][hit];
+                if (hit != rng[cc][1]) s = s + push_val(a, cc, hit, i);
             }
         }
         const float step = a.lr * s;

@@ -162,6 +162,15 @@ struct ApplyArgs {
     const uint32_t* idx[kMaxPushes];
     const float* val[kMaxPushes];
     uint32_t nnz[kMaxPushes];
+    // quantised pushes (qkind 1..4): values decoded from sign bits and centre
+    // pairs per tensor or per column of the layout below
+    uint32_t qkind;
+    const uint32_t* bits[kMaxPushes];
+    const float* means[kMaxPushes];
+    const uint32_t* tensor_off;  // [T + 1]
+    uint32_t T;
+    const uint32_t* columns;     // [T]
+    const uint32_t* colbase;     // [T + 1]
 };
 
 hipError_t launch_sample(const SampleArgs& a, bool has_base, hipStream_t st);

@@ -38,6 +38,7 @@ EXPORTS = [
     "gd_compress_sampled",
     "gd_set_columns",
     "gd_compress_pull",
+    "gd_apply_quantised",
     "gd_quant_centres",
     "gd_apply_sparse",
     "gd_status_string",
@@ -89,6 +90,8 @@ def _lib() -> ctypes.CDLL:
     lib.gd_compress.restype = i32
     lib.gd_compress_sampled.argtypes = [vp, vp, vp, vp, dbl, i32, u32, u64, ctypes.POINTER(_Sparse), vp]
     lib.gd_compress_sampled.restype = i32
+    lib.gd_apply_quantised.argtypes = [vp, vp, u32, vp, vp, vp, vp, i32, ctypes.c_float, vp]
+    lib.gd_apply_quantised.restype = i32
     lib.gd_compress_pull.argtypes = [vp, vp, vp, dbl, i32, ctypes.POINTER(_Sparse), vp]
     lib.gd_compress_pull.restype = i32
     lib.gd_set_columns.argtypes = [vp, vp]
@@ -239,6 +242,28 @@ class Compressor:
             raise GDError(st, "gd_compress_pull")
         out.k = self.keep_total(drop_ratio, per_tensor)
         return out
+
+    def apply_quantised(self, params: torch.Tensor, idx, sign_bits, means, quant: int, lr: float = 1.0,
+                        stream: Optional[torch.cuda.Stream] = None) -> None:
+        """gd_apply_quantised: decode quantised pushes of this layout and apply them to params."""
+        _check_f32(params, "params", self.N)
+        C = len(idx)
+        if not (len(sign_bits) == len(means) == C):
+            raise ValueError("idx, sign_bits and means must have one entry per push")
+        for a, b, m in zip(idx, sign_bits, means):
+            if a.dtype != torch.int32 or b.dtype != torch.int32 or m.dtype != torch.float32:
+                raise TypeError("a push is int32 (uint32 bits) indices and sign words and float32 centres")
+            if not (a.is_cuda and b.is_cuda and m.is_cuda and a.is_contiguous() and b.is_contiguous()
+                    and m.is_contiguous()):
+                raise TypeError("push tensors must be contiguous GPU tensors")
+        arr = lambda xs: (ctypes.c_void_p * max(C, 1))(*[x.data_ptr() for x in xs])
+        ip, bp, mp = arr(idx), arr(sign_bits), arr(means)
+        nz = (ctypes.c_uint64 * max(C, 1))(*[a.numel() for a in idx])
+        st = _lib().gd_apply_quantised(self._h, params.data_ptr(), C, ctypes.cast(ip, ctypes.c_void_p),
+                                       ctypes.cast(bp, ctypes.c_void_p), ctypes.cast(mp, ctypes.c_void_p),
+                                       ctypes.cast(nz, ctypes.c_void_p), int(quant), float(lr), _stream_handle(stream))
+        if st != 0:
+            raise GDError(st, "gd_apply_quantised")
 
     def set_columns(self, columns) -> None:
         """Matrix view of every tensor for the column-wise centres (gd_set_columns)."""
