@@ -48,8 +48,11 @@ __device__ __forceinline__ uint32_t tensor_of(const uint32_t* off, uint32_t T, u
 // MODE 0: acc = grad + residual; 1: (grad - base) + residual (a pull with a
 // residual); 2: grad - base with no residual at all (a pull from the last
 // pulled copy, which keeps the unsent difference itself).
+constexpr int kDenseThreads = kUnitLen / 4;  // one 16-byte vector per lane and input array
+constexpr int kDenseWaves = kDenseThreads / kWave;
+
 template <int MODE>
-__global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
+__global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
     constexpr bool BASE = MODE >= 1, NORES = MODE == 2;
     const uint32_t u = blockIdx.x;
     const int tid = threadIdx.x, w = tid >> 6, lane = lane_id();
@@ -118,12 +121,12 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
     // the four elements of a lane, into one contiguous list per unit (fewer
     // partially written cache lines than a list per wave)
     const uint64_t m0 = ballot(cand[0]), m1 = ballot(cand[1]), m2 = ballot(cand[2]), m3 = ballot(cand[3]);
-    __shared__ uint32_t qc[kWavesPerBlock];
+    __shared__ uint32_t qc[kDenseWaves];
     if (lane == 0) qc[w] = popc64(m0) + popc64(m1) + popc64(m2) + popc64(m3);
     __syncthreads();
     uint32_t base = 0, total = 0;
 #pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i) {
+    for (int i = 0; i < kDenseWaves; ++i) {
         base += i < w ? qc[i] : 0u;
         total += qc[i];
     }
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
     if (tid == 0) a.cnt[u] = total;
     if (boundary) {
         // candidates before each tensor start strictly inside the unit
-        __shared__ uint32_t red[kWavesPerBlock];
+        __shared__ uint32_t red[kDenseWaves];
         for (uint32_t t = (info & 0x7FFFFFFFu) + 1; t < a.T && a.tensor_off[t] < uend; ++t) {
             const uint32_t x = a.tensor_off[t];
             if (x <= ustart) continue;
@@ -158,7 +161,12 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
             __syncthreads();
             if (lane == 0) red[w] = c;
             __syncthreads();
-            if (tid == 0) a.split[t] = red[0] + red[1] + red[2] + red[3];
+            if (tid == 0) {
+                uint32_t sum = 0;
+#pragma unroll
+                for (int i = 0; i < kDenseWaves; ++i) sum += red[i];
+                a.split[t] = sum;
+            }
         }
     }
 }
@@ -166,9 +174,9 @@ __global__ __launch_bounds__(kBlock) void k_dense(DenseArgs a) {
 hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st) {
     if (a.num_units == 0) return hipSuccess;
     const dim3 grid(a.num_units);
-    if (has_base && a.res == nullptr) hipLaunchKernelGGL(k_dense<2>, grid, dim3(kBlock), 0, st, a);
-    else if (has_base) hipLaunchKernelGGL(k_dense<1>, grid, dim3(kBlock), 0, st, a);
-    else hipLaunchKernelGGL(k_dense<0>, grid, dim3(kBlock), 0, st, a);
+    if (has_base && a.res == nullptr) hipLaunchKernelGGL(k_dense<2>, grid, dim3(kDenseThreads), 0, st, a);
+    else if (has_base) hipLaunchKernelGGL(k_dense<1>, grid, dim3(kDenseThreads), 0, st, a);
+    else hipLaunchKernelGGL(k_dense<0>, grid, dim3(kDenseThreads), 0, st, a);
     return hipGetLastError();
 }
 

@@ -21,7 +21,7 @@
 
 namespace gd {
 
-constexpr uint32_t kMaxScanBlocks = 4096;  // 2^32 elements / 1024 per unit / 1024 units per block
+constexpr uint32_t kMaxScanBlocks = (uint32_t)((1ull << 32) / kUnitLen / kScanUnits);  // for 2^32 elements
 
 // Candidates (dense-pass order) before element offset x, x a tensor start.
 __device__ __forceinline__ uint32_t raw_start(const CandArgs& a, const uint32_t* boff, uint32_t grand, uint32_t t) {
