@@ -9,9 +9,9 @@
 // finds where the bucket starts and ends in every client's (ascending) index
 // list by a 32-way search per half-wave (four rounds of loads for a list of a
 // few hundred thousand entries, instead of a binary search's twenty), stages
-// those entries in LDS, and then gives every index to the lowest client
-// holding it, which sums all clients' values for it in client order and
-// writes p once.  The parameter writes of a block stay inside its bucket.
+// those entries in LDS, marking the indices pushed more than once, and then
+// gives every index to the lowest client holding it, which sums all clients'
+// values for it in client order and writes p once.  The parameter writes of a block stay inside its bucket.
 // Quantised pushes (indices, sign bits, centre pairs; Section 5.4) are decoded
 // entry by entry where their values are read.
 
@@ -20,7 +20,8 @@
 namespace gd {
 
 constexpr int kApplyBucketShift = 15;
-constexpr int kApplyLds = 4096;  // entries of all clients staged per bucket
+constexpr int kApplyLds = 2048;                              // entries of all clients staged per bucket
+constexpr int kBucketWords = (1 << kApplyBucketShift) / 32;  // one bit per index of a bucket
 
 // First position in list[lo, hi) whose value is >= x, found by the 32 lanes of
 // one half-wave together (g: lane within the half, mask: the half's lanes).
@@ -75,6 +76,7 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
     __shared__ uint32_t base[kMaxPushes + 1];  // first staged entry of each client
     __shared__ uint32_t sidx[kApplyLds];
     __shared__ float sval[kApplyLds];
+    __shared__ uint32_t seen[2][kBucketWords];  // [0]: index pushed at least once, [1]: more than once
     const int tid = threadIdx.x, w = tid >> 6, lane = lane_id();
     const uint32_t b = blockIdx.x;
     const uint32_t i_lo = b << kApplyBucketShift;
@@ -101,20 +103,68 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
     const uint32_t total = base[a.C];
     if (total == 0) return;
     const bool staged = total <= (uint32_t)kApplyLds;
-    // 2. stage the bucket's entries (index, value) of every client
+    // 2. stage the bucket's entries (index, value) of every client, and mark
+    //    the indices pushed more than once
     if (staged) {
+        for (uint32_t q = tid; q < 2u * kBucketWords; q += kBlock) (&seen[0][0])[q] = 0;
+        __syncthreads();
         for (uint32_t c = 0; c < a.C; ++c) {
             const uint32_t r0 = rng[c][0], cnt = rng[c][1] - r0, o = base[c];
             for (uint32_t q = tid; q < cnt; q += kBlock) {
                 const uint32_t ii = a.idx[c][r0 + q];
                 sidx[o + q] = ii;
                 sval[o + q] = push_val(a, c, r0 + q, ii);
+                const uint32_t off = ii - i_lo, bit = 1u << (off & 31);
+                if (atomicOr(&seen[0][off >> 5], bit) & bit) atomicOr(&seen[1][off >> 5], bit);
             }
         }
         __syncthreads();
     }
     // 3. each entry: skip it if a lower client holds the same index, else sum
-    //    every client's value for it in client order and update p once
+    //    every client's value for it in client order and update p once (an
+    //    index pushed once needs no search).  When staged, a thread settles all
+    //    its entries first and then reads all its parameters at once, so their
+    //    latencies overlap instead of adding up.
+    if (staged) {
+        constexpr int kPer = kApplyLds / kBlock;
+        uint32_t pi[kPer];
+        float pstep[kPer];
+        bool pv[kPer];
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) {
+            const uint32_t e = tid + t * kBlock;
+            pv[t] = false;
+            pi[t] = i_lo;  // a valid parameter index for the unconditional load below
+            pstep[t] = 0.0f;
+            if (e < total) {
+                uint32_t c = 0;
+                while (base[c + 1] <= e) ++c;  // client of staged entry e
+                const uint32_t i = sidx[e];
+                const uint32_t off = i - i_lo;
+                const bool once = (seen[1][off >> 5] & (1u << (off & 31))) == 0;
+                bool owner = true;
+                for (uint32_t cc = 0; cc < c && owner && !once; ++cc)
+                    owner = find_u32(sidx, base[cc], base[cc + 1], i) == base[cc + 1];
+                if (owner) {
+                    float sum = 0.0f + sval[e];
+                    for (uint32_t cc = c + 1; cc < a.C && !once; ++cc) {
+                        const uint32_t hit = find_u32(sidx, base[cc], base[cc + 1], i);
+                        if (hit != base[cc + 1]) sum = sum + sval[hit];
+                    }
+                    pv[t] = true;
+                    pi[t] = i;
+                    pstep[t] = a.lr * sum;
+                }
+            }
+        }
+        float pold[kPer];
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) pold[t] = a.p[pi[t]];
+#pragma unroll
+        for (int t = 0; t < kPer; ++t)
+            if (pv[t]) a.p[pi[t]] = pold[t] - pstep[t];
+        return;
+    }
     for (uint32_t e = tid; e < total; e += kBlock) {
         uint32_t c = 0;
         while (base[c + 1] <= e) ++c;  // client of staged entry e
