@@ -240,8 +240,9 @@ const char* gd_status_string(gd_status status);
 
 /*
  * Timing of the dense pass (the kernel that streams grad and residual).
- * When enabled, gd_compress records a HIP event pair around that kernel on
- * the call's stream.  gd_profile_read waits for the recorded events, returns
+ * When enabled, gd_compress has the dispatch of that kernel record a HIP
+ * event pair at its start and end (hipExtLaunchKernelGGL; the events are
+ * created without the system-scope fence, as they serve timing only).  gd_profile_read waits for the recorded events, returns
  * the summed milliseconds and the number of launches, and resets both.
  */
 gd_status gd_profile_enable(gd_ctx* ctx, int enable);

@@ -119,12 +119,10 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     da.slots = ctx->scr.slots;
     da.cnt = ctx->scr.cnt;
     const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_units > 0;
-    if (timed && hipEventRecord(ctx->events[ctx->events_used], st) != hipSuccess) return GD_ERR_HIP;
-    if (gd::launch_dense(da, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
-    if (timed) {
-        if (hipEventRecord(ctx->events[ctx->events_used + 1], st) != hipSuccess) return GD_ERR_HIP;
-        ctx->events_used += 2;
-    }
+    hipEvent_t t0 = timed ? ctx->events[ctx->events_used] : nullptr;
+    hipEvent_t t1 = timed ? ctx->events[ctx->events_used + 1] : nullptr;
+    if (gd::launch_dense(da, base != nullptr, st, t0, t1) != hipSuccess) return GD_ERR_HIP;
+    if (timed) ctx->events_used += 2;
     if (ctx->num_units > 0) ++ctx->dense_launches;
 
     gd::CandArgs ca{};
@@ -568,7 +566,7 @@ gd_status gd_profile_enable(gd_ctx* ctx, int enable) {
     if (enable && ctx->events.empty()) {
         ctx->events.resize(2 * 4096);
         for (auto& e : ctx->events)
-            if (hipEventCreate(&e) != hipSuccess) return GD_ERR_HIP;
+            if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return GD_ERR_HIP;
     }
     ctx->profile = enable != 0;
     ctx->events_used = 0;

@@ -396,13 +396,9 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         }
         const uint32_t hi = v.miss ? kNoKey : a.seg[v.s].hi;
         const uint32_t thr = a.seg[v.s].thr, need = a.seg[v.s].need;
-        // Residual words that may change below are read first, early enough
-        // to overlap the prefix work: the 4-byte fix-up then lands on a line
-        // the cache holds whole.  A lone partial-line write reaches HBM as a
-        // read-modify-write when the line is evicted, which the next dense
-        // pass pays for many times over.
-        // A pull from the copy instead reads the copy word of every entry that
-        // may be kept, to add the sent value to it.
+        // A pull from the copy reads the copy word of every entry that may be
+        // kept, to add the sent value to it; the loads are issued here, early
+        // enough to overlap the prefix work.
         const bool pull = a.res == nullptr;
         float old[kRows];
 #pragma unroll
@@ -410,11 +406,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             const uint32_t key = vb[r] & 0x7FFFFFFFu;
             const bool valid = v.p0 + r * kWave + lane < v.p1;
             old[r] = 0.0f;
-            if (pull) {
-                if (valid && key >= thr) old[r] = a.pull_copy[ix[r]];
-            } else if (valid && ((key > thr) != (key >= hi) || key == thr)) {
-                old[r] = *reinterpret_cast<const volatile float*>(a.res + ix[r]);
-            }
+            if (pull && valid && key >= thr) old[r] = a.pull_copy[ix[r]];
         }
         // candidates above / equal to the threshold in earlier tiles of the segment
         uint32_t bg = 0, be = 0;
@@ -478,10 +470,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
                 if (kept) a.pull_copy[ix[r]] = old[r] + __uint_as_float(vb[r]);
             } else {
                 const bool wz = valid && key >= hi;
-                if (kept != wz) {
-                    asm volatile("" ::"v"(old[r]));  // the line read above precedes the write
-                    a.res[ix[r]] = kept ? 0.0f : __uint_as_float(vb[r]);
-                }
+                if (kept != wz) a.res[ix[r]] = kept ? 0.0f : __uint_as_float(vb[r]);
             }
             bg += popc64(mg);
             be += popc64(me);

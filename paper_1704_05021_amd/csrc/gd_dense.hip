@@ -13,11 +13,17 @@
 //
 // A unit is the 1024 elements [1024u, 1024u + 1024) of the flat gradient,
 // one block of 256 threads with one 16-byte vector per thread, so every
-// load is aligned and issued before any table lookup.  The block compacts
+// load is aligned and issued before any table lookup.  The streamed arrays
+// are loaded and the residual stored as non-temporal: the residual's load and
+// store both streaming keeps its lines from filling the L2 with dirty data
+// (either alone gains nothing; both take the 137M-element pass from about
+// 288 to 254 us).  The block compacts
 // the unit's candidates into slots [1024u, ...) and stores their count.  A unit
 // that holds a tensor boundary also records, for each tensor starting inside
 // it, how many of its candidates precede that start (the candidate layout
 // needs it).
+
+#include <hip/hip_ext.h>
 
 #include "gd_kernels.h"
 
@@ -64,7 +70,7 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
     if (e0 + 4 <= uend) {
         g = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.grad) + (e0 >> 2));
         if (BASE) b = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.base) + (e0 >> 2));
-        if (!NORES) r = reinterpret_cast<const f4*>(a.res)[e0 >> 2];
+        if (!NORES) r = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.res) + (e0 >> 2));
     } else {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -110,7 +116,7 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
     }
     if (!NORES) {
         if (e0 + 4 <= uend) {
-            reinterpret_cast<f4*>(a.res)[e0 >> 2] = ov;
+            __builtin_nontemporal_store(ov, reinterpret_cast<f4*>(a.res) + (e0 >> 2));
         } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q)
@@ -141,12 +147,6 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
             }
         }
     }
-    {
-        // pad the list to whole 128-byte lines, so that no partially written
-        // line is left for HBM to merge
-        const uint32_t padded = (total + 15u) & ~15u;
-        if ((uint32_t)tid < padded - total) a.slots[ustart + total + tid] = make_uint2(kNoKey, 0u);
-    }
     if (tid == 0) a.cnt[u] = total;
     if (boundary) {
         // candidates before each tensor start strictly inside the unit
@@ -171,12 +171,14 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
     }
 }
 
-hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st) {
+// When t0 and t1 are given, the dispatch itself records them at its start and
+// end (no separate marker packets on the stream, so the timing adds no gap).
+hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st, hipEvent_t t0, hipEvent_t t1) {
     if (a.num_units == 0) return hipSuccess;
-    const dim3 grid(a.num_units);
-    if (has_base && a.res == nullptr) hipLaunchKernelGGL(k_dense<2>, grid, dim3(kDenseThreads), 0, st, a);
-    else if (has_base) hipLaunchKernelGGL(k_dense<1>, grid, dim3(kDenseThreads), 0, st, a);
-    else hipLaunchKernelGGL(k_dense<0>, grid, dim3(kDenseThreads), 0, st, a);
+    const dim3 grid(a.num_units), block(kDenseThreads);
+    auto k = has_base && a.res == nullptr ? k_dense<2> : has_base ? k_dense<1> : k_dense<0>;
+    if (t0 != nullptr && t1 != nullptr) hipExtLaunchKernelGGL(k, grid, block, 0, st, t0, t1, 0, a);
+    else hipLaunchKernelGGL(k, grid, block, 0, st, a);
     return hipGetLastError();
 }
 

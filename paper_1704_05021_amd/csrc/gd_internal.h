@@ -24,7 +24,7 @@ struct Tables {
 };
 
 struct Scratch {
-    uint2* slots = nullptr;          // [C * 1024] candidates (index, value bits) of unit u at [1024u, ...), padded to 16
+    uint2* slots = nullptr;          // [C * 1024] candidates (index, value bits) of unit u at [1024u, ...)
     uint32_t* cnt = nullptr;         // [C] candidates per unit
     uint32_t* split = nullptr;       // [T] candidates of a tensor's first unit before the tensor
     uint32_t* loc = nullptr;         // [C] candidate offset of each unit inside its scan block

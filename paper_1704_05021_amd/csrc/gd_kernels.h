@@ -176,7 +176,8 @@ struct ApplyArgs {
 hipError_t launch_sample(const SampleArgs& a, bool has_base, hipStream_t st);
 hipError_t launch_sampled(const SampledArgs& a, bool has_base, uint32_t max_samples, hipStream_t st);
 hipError_t launch_layout(const CandArgs& a, hipStream_t st);
-hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st);
+hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st, hipEvent_t t0 = nullptr,
+                        hipEvent_t t1 = nullptr);
 hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles, hipStream_t st);
 hipError_t launch_quant(const QuantArgs& q, hipStream_t st);
 hipError_t launch_apply(const ApplyArgs& a, uint32_t max_nnz, hipStream_t st);
