@@ -56,6 +56,7 @@ __host__ __device__ constexpr uint32_t sample_unit_count(uint32_t n16) {
 constexpr uint32_t kNoKey16 = 0xFFFFu;
 constexpr int kK16Shift = 15;           // key16 = key >> 15
 constexpr int kS0Shift = 6, kSNB1 = 64;
+constexpr int kBracketWin = 4;  // coarse digits whose fine histograms one bracket pass builds
 constexpr int kSHistWords = 1024 + 2;  // per segment: digit histogram of the sample, valid and zero counts  // key16 digits: bits 15..6 (= key digit 0), bits 5..0
 
 // Sampled-threshold mode: sampler blocks of 256 threads with 4 sample

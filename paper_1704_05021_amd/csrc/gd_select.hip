@@ -19,11 +19,13 @@
 //               Neighbours are strongly correlated in sparse embedding
 //               gradients (a nonzero row), so spread groups carry far more
 //               information per sample than one run of 16.
-//   k_bracket : one block per segment holds its sample keys in registers,
-//               estimates the threshold's 16-bit key prefix P from the
-//               sample rank k * m / n, and measures the spread of the
-//               per-unit counts of keys >= P (neighbouring elements can be
-//               strongly correlated, so the spread is not assumed binomial).
+//   k_bracket : one block per segment holds its sample keys in registers
+//               and, in one pass over them, estimates the threshold's 16-bit
+//               key prefix P from the sample rank k * m / n and measures the
+//               spread of the per-unit counts of keys in or above P's
+//               coarse digit (neighbouring elements can be strongly
+//               correlated, so the spread is not assumed binomial: its
+//               dispersion index scales the binomial standard deviation).
 //               hi is just above P: the dense pass zeroes the residual of
 //               keys >= hi, and every key between hi and the exact threshold
 //               costs one fix-up write later, so hi is a point estimate.  lo
@@ -226,6 +228,7 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
     const uint32_t k = keep_of(n, a.keep_ppm);
     __shared__ uint32_t hA[kNB0];
     __shared__ uint32_t hB[kSNB1];
+    __shared__ uint32_t hW[kBracketWin * kSNB1];
     __shared__ uint32_t par[4];
     __shared__ uint32_t sums[4];
     uint32_t n16, U;
@@ -277,34 +280,80 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
             hi = kNoKey;
             lo = (full && k > mnz) ? 0u : 1u;
         } else {
-            const uint32_t P = pick16(hA, hB, par, rq, kw);
-            hi = (P + 1u) << kK16Shift;
-            if (full) {
-                lo = P << kK16Shift;
-            } else {
-                // Pass 2: spread of the per-unit counts of keys >= P
+            // One pass over the sample keys: the fine (low 6-bit) histograms of
+            // the kBracketWin coarse digits from dq, the digit holding rank rq,
+            // downwards; and per unit, the count of keys at or above dq's floor.
+            if (tid < kWave) {
+                uint32_t d, ab;
+                wave_pick<kNB0>(hA, rq, d, ab);
+                if (tid == 0) {
+                    par[0] = d;
+                    par[1] = rq - ab;
+                }
+            }
+            for (int i = tid; i < kBracketWin * kSNB1; i += kBracketThreads) hW[i] = 0;
+            __syncthreads();
+            const uint32_t dq = par[0], rf = par[1], floor16 = dq << kS0Shift;
 #pragma unroll
-                for (int j = 0; j < kBracketUnits; ++j) {
-                    uint32_t c = 0;
+            for (int j = 0; j < kBracketUnits; ++j) {
+                uint32_t c = 0;
 #pragma unroll
-                    for (int i = 0; i < kUnit; ++i) {
-                        const uint32_t key = (kw[j][i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
-                        c += key != kNoKey16 && key >= P;
-                    }
+                for (int i = 0; i < kUnit; ++i) {
+                    const uint32_t key = (kw[j][i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
+                    const bool valid = key != kNoKey16;
+                    const uint32_t dd = dq - (key >> kS0Shift);  // wraps above dq
+                    lds_hist_add(hW, dd * kSNB1 + (key & (kSNB1 - 1)), valid && key != 0 && dd < (uint32_t)kBracketWin);
+                    c += valid && key >= floor16;
+                }
+                if (!full) {
                     const uint32_t s1 = wave_sum(c), s2 = wave_sum(c * c);
                     if (lane_id() == 0) {
                         atomicAdd(&sums[2], s1);
                         atomicAdd(&sums[3], s2);
                     }
                 }
-                __syncthreads();
-                const double mean = (double)sums[2] / U, var = (double)sums[3] / U - mean * mean;
-                const double sd = sqrt(fmax(q, U * fmax(var, 0.0)));
+            }
+            __syncthreads();
+            // P: the fine bin of rank rf within digit dq
+            if (tid < kWave) {
+                uint32_t f, ab;
+                wave_pick<kSNB1>(hW, rf, f, ab);
+                if (tid == 0) par[2] = floor16 | f;
+            }
+            __syncthreads();
+            const uint32_t P = par[2];
+            hi = (P + 1u) << kK16Shift;
+            if (full) {
+                lo = P << kK16Shift;
+            } else {
+                // The spread of the per-unit counts at dq's floor, as a
+                // dispersion index (variance over mean), carried over to the
+                // count at the estimate: sd = sqrt(q * max(1, index)).
+                const double mean = (double)sums[2] / U;
+                const double var = fmax((double)sums[3] / U - mean * mean, 0.0);
+                const double disp = mean > 0.0 ? var / mean : 1.0;
+                const double sd = sqrt(q * fmax(1.0, disp));
                 const double fl = ceil(q + 5.0 * sd + 4.0);
                 if (fl > (double)mnz) {
                     lo = 1u;  // the margin reaches the zero keys
                 } else {
-                    lo = pick16(hA, hB, par, (uint32_t)fl, kw) << kK16Shift;
+                    // rank fl lies in digit dl <= dq: within the window, or
+                    // (rarely) one more pass over the keys
+                    if (tid < kWave) {
+                        uint32_t dl, abl, lo16 = kNoKey;
+                        wave_pick<kNB0>(hA, (uint32_t)fl, dl, abl);
+                        if (dq - dl < (uint32_t)kBracketWin) {
+                            uint32_t f, ab;
+                            wave_pick<kSNB1>(hW + (dq - dl) * kSNB1, (uint32_t)fl - abl, f, ab);
+                            lo16 = (dl << kS0Shift) | f;
+                        }
+                        if (tid == 0) par[3] = lo16;
+                    }
+                    __syncthreads();
+                    uint32_t lo16 = par[3];
+                    __syncthreads();
+                    if (lo16 == kNoKey) lo16 = pick16(hA, hB, par, (uint32_t)fl, kw);
+                    lo = lo16 << kK16Shift;
                     if (lo == 0) lo = 1;
                 }
             }
