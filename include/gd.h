@@ -240,12 +240,18 @@ const char* gd_status_string(gd_status status);
 
 /*
  * Timing of the dense pass (the kernel that streams grad and residual).
- * When enabled, gd_compress has the dispatch of that kernel record a HIP
- * event pair at its start and end (hipExtLaunchKernelGGL; the events are
- * created without the system-scope fence, as they serve timing only).  gd_profile_read waits for the recorded events, returns
- * the summed milliseconds and the number of launches, and resets both.
+ * gd_profile_enable(ctx, every) with every >= 1 times the dense launches
+ * numbered 0, every, 2 * every, ... from this call on (every = 1: all of
+ * them); every = 0 turns timing off; a negative value is GD_ERR_ARG.  A
+ * timed dispatch records a HIP event pair at its own start and end
+ * (hipExtLaunchKernelGGL; the events are created without the system-scope
+ * fence, as they serve timing only).  Each timed launch still delays the
+ * next kernel by a few microseconds, which is why a caller may time only
+ * every n-th one.  Up to 4096 launches are timed between reads.
+ * gd_profile_read waits for the recorded events, returns the summed
+ * milliseconds and the number of timed launches, and resets both.
  */
-gd_status gd_profile_enable(gd_ctx* ctx, int enable);
+gd_status gd_profile_enable(gd_ctx* ctx, int every);
 gd_status gd_profile_read(gd_ctx* ctx, double* dense_ms, uint64_t* dense_launches);
 
 /*

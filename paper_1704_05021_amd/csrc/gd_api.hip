@@ -118,7 +118,8 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     da.seg = ctx->scr.seg;
     da.slots = ctx->scr.slots;
     da.cnt = ctx->scr.cnt;
-    const bool timed = ctx->profile && ctx->events_used + 2 <= ctx->events.size() && ctx->num_units > 0;
+    const bool timed = ctx->profile_every != 0 && ctx->dense_launches % ctx->profile_every == 0 &&
+                       ctx->events_used + 2 <= ctx->events.size() && ctx->num_units > 0;
     hipEvent_t t0 = timed ? ctx->events[ctx->events_used] : nullptr;
     hipEvent_t t1 = timed ? ctx->events[ctx->events_used + 1] : nullptr;
     if (gd::launch_dense(da, base != nullptr, st, t0, t1) != hipSuccess) return GD_ERR_HIP;
@@ -560,15 +561,15 @@ gd_status gd_debug_state(gd_ctx* ctx, uint32_t* seg_words, uint32_t max_segments
     return GD_OK;
 }
 
-gd_status gd_profile_enable(gd_ctx* ctx, int enable) {
-    if (!ctx) return GD_ERR_ARG;
+gd_status gd_profile_enable(gd_ctx* ctx, int every) {
+    if (!ctx || every < 0) return GD_ERR_ARG;
     DeviceGuard guard(ctx->device);
-    if (enable && ctx->events.empty()) {
+    if (every && ctx->events.empty()) {
         ctx->events.resize(2 * 4096);
         for (auto& e : ctx->events)
             if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return GD_ERR_HIP;
     }
-    ctx->profile = enable != 0;
+    ctx->profile_every = (uint32_t)every;
     ctx->events_used = 0;
     ctx->dense_launches = 0;
     return GD_OK;

@@ -81,7 +81,7 @@ struct gd_ctx {
     gd::ColumnTables cols;
     std::vector<void*> allocations;
     uint32_t debug_bracket = 0;
-    bool profile = false;
+    uint32_t profile_every = 0;  // time dense launches 0, every, 2 * every, ... (0: off)
     std::vector<hipEvent_t> events;  // pairs
     size_t events_used = 0;
     uint64_t dense_launches = 0;

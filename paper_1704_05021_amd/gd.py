@@ -326,8 +326,9 @@ class Compressor:
         keys = ("unit_len", "units", "tile", "max_tiles")
         return segs, dict(zip(keys, (int(x) for x in info)))
 
-    def profile_enable(self, on: bool = True) -> None:
-        st = _lib().gd_profile_enable(self._h, int(on))
+    def profile_enable(self, every: int = 1) -> None:
+        """Time dense launches 0, every, 2 * every, ... from now on (0: off)."""
+        st = _lib().gd_profile_enable(self._h, int(every))
         if st != 0:
             raise GDError(st, "gd_profile_enable")
 

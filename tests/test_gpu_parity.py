@@ -286,3 +286,26 @@ def test_non_default_stream():
     s.synchronize()
     assert np.array_equal(out.idx[:out.k].cpu().numpy().view(np.uint32), o.idx)
     assert np.array_equal(bits(rt.cpu().numpy()), bits(o.residual))
+
+
+def test_dense_timing_every_nth_launch():
+    """Timing every third dense launch over seven calls times launches 0, 3 and 6; results are unchanged."""
+    w = wl.workload("nmt_small_per_tensor")
+    off = w.layout.offsets.astype(np.int64).tolist()
+    comp = gd.Compressor(off)
+    grad = w.grad(0)
+    o = oracle_compress(grad, np.zeros_like(grad), off, 0.99, True, False)
+    gt = torch.from_numpy(grad).cuda()
+    comp.profile_enable(3)
+    for _ in range(7):
+        rt = torch.zeros_like(gt)
+        out = comp.compress(gt, rt, 0.99, per_tensor=True)
+    ms, n = comp.profile_read()
+    assert n == 3 and ms > 0.0
+    assert np.array_equal(out.idx[:out.k].cpu().numpy().view(np.uint32), o.idx)
+    assert np.array_equal(bits(rt.cpu().numpy()), bits(o.residual))
+    comp.profile_enable(0)
+    comp.compress(gt, torch.zeros_like(gt), 0.99, per_tensor=True)
+    assert comp.profile_read() == (0.0, 0)
+    with pytest.raises(gd.GDError):
+        comp.profile_enable(-1)
