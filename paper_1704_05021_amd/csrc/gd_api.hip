@@ -174,10 +174,6 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     ea.capacity = out->capacity;
     const bool q = quant != GD_QUANT_NONE;
     ea.qkind = (uint32_t)quant;
-    ea.columns = ctx->cols.columns;
-    ea.colbase = ctx->cols.colbase;
-    ea.csum = ctx->cols.csum;
-    ea.ccnt = ctx->cols.ccnt;
     if (gd::launch_layout(ca, st) != hipSuccess) return GD_ERR_HIP;
     if (gd::launch_candidates(ca, ea, q, ctx->max_tiles, st) != hipSuccess) return GD_ERR_HIP;
 

@@ -447,16 +447,9 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             if (kept) {
                 o.idx[pos] = ix[r];
                 o.val[pos] = __uint_as_float(vb[r]);
-                if (QUANT) {
+                if (QUANT && o.qkind != kQuantColumnMean) {  // column sums come from the sent entries later
                     const float x = __uint_as_float(vb[r]);
-                    if (o.qkind == kQuantColumnMean) {
-                        // column of this entry in its tensor's row-major matrix view
-                        const uint32_t c = o.colbase[v.t] + (ix[r] - a.tensor_off[v.t]) % o.columns[v.t];
-                        const uint32_t slot = 2 * c + (x < 0.0f ? 1u : 0u);
-                        // native fp64 add in the L2 (device memory), not a compare-and-swap loop
-                        unsafeAtomicAdd(&o.csum[slot], (double)x);
-                        atomicAdd(&o.ccnt[slot], 1u);
-                    } else if (x < 0.0f) {
+                    if (x < 0.0f) {
                         sn += (double)x;
                         ++nn;
                     } else {

@@ -120,10 +120,6 @@ struct EmitArgs {
     uint32_t* tensor_counts;
     uint64_t capacity;
     uint32_t qkind;             // 0 or a kQuant* kind
-    const uint32_t* columns;    // [T] columns of each tensor's matrix view (column-wise centres)
-    const uint32_t* colbase;    // [T + 1] first column group of each tensor
-    double* csum;               // [2 * groups] column sums (positive, negative), zero on entry
-    uint32_t* ccnt;             // [2 * groups] column counts, zero on entry
 };
 
 struct QuantArgs {
@@ -148,8 +144,8 @@ struct QuantArgs {
     const uint32_t* columns;
     const uint32_t* colbase;
     uint32_t groups;            // column groups (column-wise centres)
-    double* csum;               // cleared again after use
-    uint32_t* ccnt;
+    double* csum;               // [2 * groups] column sums (positive, negative), zero on entry, cleared after use
+    uint32_t* ccnt;             // [2 * groups] column counts, likewise
 };
 
 constexpr uint32_t kMaxPushes = 64;

@@ -13,12 +13,16 @@
 //   column mean  : per column of each tensor's row-major matrix view.
 // Per-tensor and global sums are taken in fp64 in a fixed order (per
 // candidate tile, then tiles in order), so they are deterministic; column
-// sums are fp64 atomics.  The sent bits are packed LSB-first, 32 per word,
+// sums are fp64 atomics over the sent entries (in LDS per slice, then once
+// per touched column).  The sent bits are packed LSB-first, 32 per word,
 // and residual[idx] becomes acc - centre.
 
 #include "gd_kernels.h"
 
 namespace gd {
+
+constexpr uint32_t kColSlice = 4096;  // sent entries per column-sum block
+constexpr int kColLds = 2048;         // most columns a block sums in LDS (48 KB)
 
 // Centres per tensor (every kind but the column mean) and the first output
 // slot of each tensor.  One wave per tensor.
@@ -62,6 +66,63 @@ __global__ __launch_bounds__(kBlock) void k_means(QuantArgs q) {
     if (lane == 0) {
         q.means[2 * t + 0] = pos;
         q.means[2 * t + 1] = neg;
+    }
+}
+
+// Column sums of the sent entries, per sign.  Each block takes a slice of
+// kColSlice consecutive output slots and walks the tensors it touches; for a
+// tensor of at most kColLds columns it sums the slice in LDS first (fp64 LDS
+// atomics) and then adds each touched column to the global sums once, so a
+// column's global atomics number its tensor's slices rather than its entries.
+// Wider tensors spread their entries over many columns and add directly.
+__global__ __launch_bounds__(kBlock) void k_colsum(QuantArgs q) {
+    __shared__ double ls[2 * kColLds];
+    __shared__ uint32_t lc[2 * kColLds];
+    const int tid = threadIdx.x;
+    const uint32_t total = q.qbase[q.T];
+    const uint64_t j0 = (uint64_t)blockIdx.x * kColSlice;
+    if (j0 >= total) return;
+    const uint32_t j1 = j0 + kColSlice < total ? (uint32_t)j0 + kColSlice : total;
+    uint32_t lo = 0, hi = q.T;  // tensor of slot j0: the last t with qbase[t] <= j0
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (q.qbase[mid] <= j0) lo = mid;
+        else hi = mid;
+    }
+    uint32_t t = lo;
+    for (uint32_t j = (uint32_t)j0; j < j1;) {  // block-uniform walk over the tensors of the slice
+        while (q.qbase[t + 1] <= j) ++t;
+        const uint32_t e = q.qbase[t + 1] < j1 ? q.qbase[t + 1] : j1;
+        const uint32_t C = q.columns[t], cb = 2 * q.colbase[t], off = q.tensor_off[t];
+        const bool local = C <= (uint32_t)kColLds;
+        if (local) {
+            for (uint32_t i = tid; i < 2 * C; i += kBlock) {
+                ls[i] = 0.0;
+                lc[i] = 0;
+            }
+            __syncthreads();
+        }
+        for (uint32_t x = j + tid; x < e; x += kBlock) {
+            const float v = q.val[x];
+            const uint32_t sl = 2 * ((q.idx[x] - off) % C) + (v < 0.0f ? 1u : 0u);
+            if (local) {
+                unsafeAtomicAdd(&ls[sl], (double)v);
+                atomicAdd(&lc[sl], 1u);
+            } else {
+                unsafeAtomicAdd(&q.csum[cb + sl], (double)v);
+                atomicAdd(&q.ccnt[cb + sl], 1u);
+            }
+        }
+        if (local) {
+            __syncthreads();
+            for (uint32_t i = tid; i < 2 * C; i += kBlock)
+                if (lc[i]) {
+                    unsafeAtomicAdd(&q.csum[cb + i], ls[i]);
+                    atomicAdd(&q.ccnt[cb + i], lc[i]);
+                }
+            __syncthreads();
+        }
+        j = e;
     }
 }
 
@@ -109,8 +170,12 @@ static inline uint32_t blocks_for_waves(uint32_t waves) { return (waves + kWaves
 
 hipError_t launch_quant(const QuantArgs& q, hipStream_t st) {
     hipLaunchKernelGGL(k_means, dim3(blocks_for_waves(q.T)), dim3(kBlock), 0, st, q);
-    if (q.qkind == kQuantColumnMean && q.groups > 0)
+    if (q.qkind == kQuantColumnMean && q.groups > 0) {
+        if (q.k_total > 0)
+            hipLaunchKernelGGL(k_colsum, dim3((uint32_t)((q.k_total + kColSlice - 1) / kColSlice)), dim3(kBlock), 0, st,
+                               q);
         hipLaunchKernelGGL(k_colmeans, dim3((q.groups + kBlock - 1) / kBlock), dim3(kBlock), 0, st, q);
+    }
     if (q.k_total > 0) {
         const uint64_t blocks = (q.k_total + kBlock - 1) / kBlock;
         hipLaunchKernelGGL(k_quant, dim3((uint32_t)blocks), dim3(kBlock), 0, st, q);
