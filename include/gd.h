@@ -77,8 +77,9 @@ typedef struct gd_ctx gd_ctx;
  *     [tensor_offsets[t], tensor_offsets[t+1]); tensor_offsets[0] must be 0,
  *     the sequence non-decreasing (empty tensors are allowed) and
  *     N = tensor_offsets[T] below 2^32 (indices are sent as uint32).
- *   Allocates all device scratch on the current HIP device (about 8 bytes per
- *   element plus small tables); gd_compress never allocates.
+ *   Allocates all device scratch on the current HIP device (about 16 bytes
+ *   per element plus about 109 KB per tensor for the per-tensor histograms);
+ *   gd_compress never allocates.  Any number of tensors is accepted.
  *   Returns GD_ERR_LAYOUT for a bad layout, GD_ERR_OOM when allocation fails.
  */
 gd_status gd_create(gd_ctx** out, const uint64_t* tensor_offsets, uint32_t num_tensors);

@@ -51,11 +51,12 @@ __device__ __forceinline__ uint32_t sample_count(uint32_t n, uint32_t sample_ppm
 }
 
 template <bool BASE>
-__global__ __launch_bounds__(kSsThreads) void k_ssample(SampledArgs a) {
-    const uint32_t s = blockIdx.y;
+__global__ __launch_bounds__(kSsThreads) void k_ssample(SampledArgs a, uint32_t bps) {
+    // a 1-D grid of bps blocks per segment (no limit on segments)
+    const uint32_t s = blockIdx.x / bps, bx = blockIdx.x % bps;
     const int tid = threadIdx.x;
     const uint32_t seg_a = a.seg_off[s], n = a.seg_off[s + 1] - seg_a;
-    if (blockIdx.x == 0) {
+    if (bx == 0) {
         if (tid == 0) {
             a.seg[s].clo = 0;
             a.seg[s].miss = 0;
@@ -69,7 +70,7 @@ __global__ __launch_bounds__(kSsThreads) void k_ssample(SampledArgs a) {
         }
     }
     const uint32_t m = sample_count(n, a.sample_ppm);
-    const uint32_t j0 = blockIdx.x * (kSsThreads * kSsPerThread);
+    const uint32_t j0 = bx * (kSsThreads * kSsPerThread);
     if (j0 >= m) return;  // block-uniform
     __shared__ uint32_t h[kSsNB0];
     for (int i = tid; i < kSsNB0; i += kSsThreads) h[i] = 0;
@@ -92,7 +93,7 @@ __global__ __launch_bounds__(kSsThreads) void k_ssample(SampledArgs a) {
         lds_hist_add(h, key[q] >> kSsD0Shift, ok[q]);
     }
     __syncthreads();
-    uint32_t* gh = a.sshist + ((size_t)s * kSsCopies + blockIdx.x % kSsCopies) * kSsNB0;
+    uint32_t* gh = a.sshist + ((size_t)s * kSsCopies + bx % kSsCopies) * kSsNB0;
     for (int i = tid; i < kSsNB0; i += kSsThreads)
         if (h[i]) atomicAdd(&gh[i], h[i]);
 }
@@ -228,9 +229,11 @@ __global__ __launch_bounds__(kSsSelThreads) void k_sselect(SampledArgs a) {
 
 hipError_t launch_sampled(const SampledArgs& a, bool has_base, uint32_t max_samples, hipStream_t st) {
     constexpr uint32_t per_block = kSsThreads * kSsPerThread;
-    const dim3 grid(max_samples > 0 ? (max_samples + per_block - 1) / per_block : 1u, a.S);
-    if (has_base) hipLaunchKernelGGL(k_ssample<true>, grid, dim3(kSsThreads), 0, st, a);
-    else hipLaunchKernelGGL(k_ssample<false>, grid, dim3(kSsThreads), 0, st, a);
+    const uint32_t bps = max_samples > 0 ? (max_samples + per_block - 1) / per_block : 1u;
+    if ((uint64_t)bps * a.S > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+    const dim3 grid(bps * a.S);
+    if (has_base) hipLaunchKernelGGL(k_ssample<true>, grid, dim3(kSsThreads), 0, st, a, bps);
+    else hipLaunchKernelGGL(k_ssample<false>, grid, dim3(kSsThreads), 0, st, a, bps);
     hipLaunchKernelGGL(k_sselect, dim3(a.S), dim3(kSsSelThreads), 0, st, a);
     return hipGetLastError();
 }

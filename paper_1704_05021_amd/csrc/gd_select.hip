@@ -60,20 +60,21 @@ __device__ __forceinline__ void sample_units(uint32_t seg_a, uint32_t seg_b, uin
 
 template <bool BASE>
 __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
-    const uint32_t s = blockIdx.y;
+    // a 1-D grid of kSampleBlocks blocks per segment (no limit on segments)
+    const uint32_t s = blockIdx.x / kSampleBlocks, bx = blockIdx.x % kSampleBlocks;
     const int tid = threadIdx.x;
     const uint32_t seg_a = a.seg_off[s], seg_b = a.seg_off[s + 1];
     __shared__ uint32_t lds[kSampleThreads / kWave + 1];
 
     // Clear this segment's histograms and state for the passes that follow.
     uint32_t* h = a.hist + (size_t)s * kHistWords;
-    for (uint32_t i = blockIdx.x * kSampleThreads + tid; i < (uint32_t)kHistWords; i += gridDim.x * kSampleThreads)
+    for (uint32_t i = bx * kSampleThreads + tid; i < (uint32_t)kHistWords; i += kSampleBlocks * kSampleThreads)
         h[i] = 0;
-    if (blockIdx.x == 0 && tid == 0) {
+    if (bx == 0 && tid == 0) {
         a.seg[s].clo = 0;
         a.seg[s].miss = 0;
     }
-    if (s == 0 && blockIdx.x == 0) {
+    if (s == 0 && bx == 0) {
         for (uint32_t t = tid; t < a.T; t += kSampleThreads) a.tensor_counts[t] = 0;
         // First output slot of each segment: exclusive prefix of k_s.
         uint64_t carry = 0;
@@ -89,8 +90,8 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
 
     uint32_t n16, U;
     sample_units(seg_a, seg_b, n16, U);
-    const uint32_t j = blockIdx.x * kSampleThreads + tid;
-    if (blockIdx.x * kSampleThreads >= U) return;  // whole block idle (block-uniform)
+    const uint32_t j = bx * kSampleThreads + tid;
+    if (bx * kSampleThreads >= U) return;  // whole block idle (block-uniform)
     __shared__ uint32_t hs[kNB0];
     __shared__ uint32_t cnt[2];
     for (int i = tid; i < kNB0; i += kSampleThreads) hs[i] = 0;
@@ -376,7 +377,8 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
 }
 
 hipError_t launch_sample(const SampleArgs& a, bool has_base, hipStream_t st) {
-    const dim3 grid(kSampleBlocks, a.S);
+    if ((uint64_t)kSampleBlocks * a.S > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+    const dim3 grid(kSampleBlocks * a.S);
     if (has_base) hipLaunchKernelGGL(k_sample<true>, grid, dim3(kSampleThreads), 0, st, a);
     else hipLaunchKernelGGL(k_sample<false>, grid, dim3(kSampleThreads), 0, st, a);
     hipLaunchKernelGGL(k_bracket, dim3(a.S), dim3(kBracketThreads), 0, st, a);

@@ -309,3 +309,19 @@ def test_dense_timing_every_nth_launch():
     assert comp.profile_read() == (0.0, 0)
     with pytest.raises(gd.GDError):
         comp.profile_enable(-1)
+
+
+@pytest.mark.parametrize("T", [3000, 70_000])
+def test_many_tensors(T):
+    """Thousands of small tensors (empty ones among them): every per-segment loop and grid runs past one block."""
+    rng = np.random.default_rng(T)
+    sizes = rng.integers(0, 40, T)
+    sizes[rng.random(T) < 0.1] = 0
+    sizes[rng.integers(0, T, 3)] = [5000, 1025, 4096]
+    offsets = [0] + np.cumsum(sizes).tolist()
+    N = offsets[-1]
+    g = (rng.standard_t(3, N) * 1e-3).astype(np.float32)
+    r = rng.normal(0, 1e-3, N).astype(np.float32)
+    comp = gd.Compressor(offsets)
+    for per, quant, drop in ((True, False, 0.9), (False, False, 0.99), (True, True, 0.5)):
+        check_case(g, r, offsets, drop, per, quant, comp=comp, what=f"T={T} per={per} quant={quant}")

@@ -173,3 +173,17 @@ def test_errors():
         comp.compress_sampled(g, r, 1.5)
     with pytest.raises(gd.GDError):
         comp.compress_sampled(torch.zeros(1001, device="cuda")[1:], r)  # not 16-byte aligned
+
+
+def test_many_tensors():
+    """70,000 small tensors under a per-tensor sampled threshold (one sampler block row per tensor)."""
+    rng = np.random.default_rng(70)
+    T = 70_000
+    sizes = rng.integers(0, 40, T)
+    sizes[rng.integers(0, T, 2)] = [30_000, 5_000]
+    offsets = [0] + np.cumsum(sizes).tolist()
+    N = offsets[-1]
+    g, r = _values(rng, N, "heavy"), _values(rng, N, "gauss")
+    comp = gd.Compressor(offsets)
+    for per in (True, False):
+        check(g, r, offsets, 0.9, per, 50_000, 4, comp=comp, what=f"T={T} per={per}")
