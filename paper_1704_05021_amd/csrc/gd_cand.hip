@@ -491,7 +491,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
                     const uint32_t before = run_e + ie - e8[j];
                     const uint32_t ties = need > before ? (need - before < e8[j] ? need - before : e8[j]) : 0u;
                     cnt += wave_sum(g8[j] + ties);
-                    run_e += __shfl(ie, kWave - 1, kWave);
+                    run_e += lane_value(ie, kWave - 1);
                 }
             }
             // entries past the capacity are not sent

@@ -115,21 +115,29 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Value of v in lane `src` of the wave (src the same in every lane).
+__device__ __forceinline__ uint32_t lane_value(uint32_t v, int src) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, src);
+}
+
+// Inclusive prefix sum over the 64 lanes, in registers: DPP shifts by 1, 2, 4
+// and 8 within each 16-lane row, then the last lane of row 0 (row 2) added
+// to row 1 (row 3) and the last lane of row 1 to rows 2 and 3.  A lane whose
+// DPP source lies outside its row, or whose row is masked off, adds the
+// `old` operand, 0.  (Cross-lane shuffles would go through the LDS crossbar,
+// one round trip per step.)  Every lane of the wave must be active.
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        uint32_t t = __shfl_up(v, d, kWave);
-        if (lane >= d) v += t;
-    }
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);  // row_shr:1
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);  // row_shr:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);  // row_shr:4
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);  // row_shr:8
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast:15, rows 1 and 3
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast:31, rows 2 and 3
     return v;
 }
 
-__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
-#pragma unroll
-    for (int d = kWave / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, kWave);
-    return v;
-}
+// Sum over the 64 lanes, in every lane.  Every lane must be active.
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) { return lane_value(wave_incl_scan(v), kWave - 1); }
 
 __device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
@@ -159,7 +167,7 @@ __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uin
     const uint64_t m = ballot(mine);
     if (m == 0) {
         digit = 0;
-        above = __shfl(incl, kWave - 1, kWave);
+        above = lane_value(incl, kWave - 1);
         return false;
     }
     const int src = __ffsll((unsigned long long)m) - 1;
@@ -177,8 +185,8 @@ __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uin
             acc += c[i];
         }
     }
-    digit = __shfl(d, src, kWave);
-    above = __shfl(ab, src, kWave);
+    digit = lane_value(d, src);
+    above = lane_value(ab, src);
     return true;
 }
 

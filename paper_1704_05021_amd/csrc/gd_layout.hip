@@ -205,7 +205,7 @@ __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
     while (todo) {
         const int src = __ffsll((unsigned long long)todo) - 1;
         todo &= todo - 1;
-        const uint32_t uu = __shfl(u, src, kWave), nn = __shfl(cnt, src, kWave);
+        const uint32_t uu = lane_value(u, src), nn = lane_value(cnt, src);
         for (uint32_t i = lane_id(); i < nn; i += kWave) {
             const uint2 e = a.slots[(size_t)uu * kUnitLen + i];
             uint32_t s = 0;

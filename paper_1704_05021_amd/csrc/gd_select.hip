@@ -295,6 +295,7 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
             for (int i = tid; i < kBracketWin * kSNB1; i += kBracketThreads) hW[i] = 0;
             __syncthreads();
             const uint32_t dq = par[0], rf = par[1], floor16 = dq << kS0Shift;
+            uint32_t s1 = 0, s2 = 0;  // this thread's units: sum of counts and of squared counts
 #pragma unroll
             for (int j = 0; j < kBracketUnits; ++j) {
                 uint32_t c = 0;
@@ -306,12 +307,15 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
                     lds_hist_add(hW, dd * kSNB1 + (key & (kSNB1 - 1)), valid && key != 0 && dd < (uint32_t)kBracketWin);
                     c += valid && key >= floor16;
                 }
-                if (!full) {
-                    const uint32_t s1 = wave_sum(c), s2 = wave_sum(c * c);
-                    if (lane_id() == 0) {
-                        atomicAdd(&sums[2], s1);
-                        atomicAdd(&sums[3], s2);
-                    }
+                s1 += c;
+                s2 += c * c;
+            }
+            if (!full) {
+                s1 = wave_sum(s1);
+                s2 = wave_sum(s2);
+                if (lane_id() == 0) {
+                    atomicAdd(&sums[2], s1);
+                    atomicAdd(&sums[3], s2);
                 }
             }
             __syncthreads();
