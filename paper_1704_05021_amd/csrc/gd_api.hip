@@ -155,8 +155,7 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     ca.cand_val = ctx->scr.cand_val;
     ca.ten_cbase = ctx->scr.ten_cbase;
     ca.tile_base = ctx->scr.tile_base;
-    ca.tile_ne0 = ctx->scr.tile_ne0;
-    ca.tile_tensor = ctx->scr.tile_tensor;
+    ca.tile_desc = ctx->scr.tile_desc;
     ca.flags = ctx->scr.flags;
     ca.tile_gt = ctx->scr.tile_gt;
     ca.tile_eq = ctx->scr.tile_eq;
@@ -302,8 +301,8 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
          dev_alloc(ctx, &ctx->scr.ne_off, C + 1) && dev_alloc(ctx, &ctx->scr.num_ne, 1) &&
          dev_alloc(ctx, &ctx->scr.raw_tbase, T + 1) && dev_alloc(ctx, &ctx->scr.cand_idx, N) &&
          dev_alloc(ctx, &ctx->scr.cand_val, N) && dev_alloc(ctx, &ctx->scr.ten_cbase, T + 1) &&
-         dev_alloc(ctx, &ctx->scr.tile_base, T + 1) && dev_alloc(ctx, &ctx->scr.tile_ne0, MT) &&
-         dev_alloc(ctx, &ctx->scr.tile_tensor, MT) && dev_alloc(ctx, &ctx->scr.tile_gt, MT) &&
+         dev_alloc(ctx, &ctx->scr.tile_base, T + 1) && dev_alloc(ctx, &ctx->scr.tile_desc, (size_t)MT * gd::kTileDescWords) &&
+          dev_alloc(ctx, &ctx->scr.tile_gt, MT) &&
          dev_alloc(ctx, &ctx->scr.tile_eq, MT) && dev_alloc(ctx, &ctx->scr.tile_q, 4 * (size_t)MT) &&
          dev_alloc(ctx, &ctx->scr.flags, 4) && dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) &&
          dev_alloc(ctx, &ctx->scr.seg, S_max) && dev_alloc(ctx, &ctx->scr.out_base, S_max) &&

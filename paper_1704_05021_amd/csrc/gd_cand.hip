@@ -38,22 +38,28 @@
 
 namespace gd {
 
+// A tile as its descriptor (written by the layout pass) describes it: tensor
+// t and segment s, the segment's k, the compact candidates [p0, p1), the
+// segment's first tile, the tensor's tiles [tfirst, tend), the non-empty
+// unit ne0 holding the first candidate, and whether the bracket missed.
 struct TileView {
-    uint32_t t, s, k, p0, p1, first_tile;
+    uint32_t t, s, k, p0, p1, first_tile, tfirst, tend, ne0;
     bool miss;
 };
 
 __device__ __forceinline__ void tile_setup(const CandArgs& a, uint32_t tile, TileView& v) {
-    const uint32_t t = a.tile_tensor[tile];
-    v.t = t;
-    v.s = a.per_tensor ? t : 0u;
-    v.k = keep_of(a.seg_off[v.s + 1] - a.seg_off[v.s], a.keep_ppm);
-    v.miss = a.seg[v.s].miss != 0;
-    const uint32_t tb = a.tile_base[t];
-    v.p0 = a.ten_cbase[t] + (tile - tb) * kTile;
-    const uint32_t end = a.ten_cbase[t + 1];
-    v.p1 = v.p0 + kTile < end ? v.p0 + kTile : end;
-    v.first_tile = a.per_tensor ? tb : 0u;
+    const uint4* d = reinterpret_cast<const uint4*>(a.tile_desc + (size_t)tile * kTileDescWords);
+    const uint4 d0 = d[0], d1 = d[1];
+    v.t = d0.x & 0x7FFFFFFFu;
+    v.miss = (d0.x >> 31) != 0;
+    v.ne0 = d0.y;
+    v.p0 = d0.z;
+    v.p1 = d0.w;
+    v.first_tile = d1.x;
+    v.k = d1.y;
+    v.tfirst = d1.z;
+    v.tend = d1.w;
+    v.s = a.per_tensor ? v.t : 0u;
 }
 
 __device__ __forceinline__ uint32_t* seg_hist(const CandArgs& a, uint32_t s, int which) {
@@ -145,7 +151,7 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
         } else {
             // compact position p <-> dense-pass offset p + shift
             const uint32_t shift = a.raw_tbase[v.t] - a.ten_cbase[v.t];
-            const uint32_t j0 = a.tile_ne0[tile];
+            const uint32_t j0 = v.ne0;
             const uint32_t nne = a.num_ne[0];
             {
                 constexpr int NW = (kWin + kWave) / kWave;
@@ -468,12 +474,12 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             bg += popc64(mg);
             be += popc64(me);
         }
-        if (tile == a.tile_base[v.t]) {
+        if (tile == v.tfirst) {
             // The first tile of a tensor writes the tensor's kept count: per
             // tile, every candidate above T plus the ties still needed (in
             // ascending tile order within the segment).  No atomics: a few
             // hundred tiles adding to one counter serialise badly.
-            const uint32_t tend = a.tile_base[v.t + 1];
+            const uint32_t tend = v.tend;
             uint32_t cnt = 0, run_e = be0;
             for (uint32_t b0 = tile; b0 < tend; b0 += 8 * kWave) {
                 uint32_t g8[8], e8[8];

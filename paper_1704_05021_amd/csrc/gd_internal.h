@@ -41,8 +41,7 @@ struct Scratch {
     uint32_t* cand_val = nullptr;    // [max(N,1)] their value bits
     uint32_t* ten_cbase = nullptr;   // [T + 1] first compact candidate of each tensor
     uint32_t* tile_base = nullptr;   // [T + 1] first tile of each tensor
-    uint32_t* tile_ne0 = nullptr;    // [max_tiles]
-    uint32_t* tile_tensor = nullptr; // [max_tiles]
+    uint32_t* tile_desc = nullptr;   // [max_tiles * kTileDescWords]
     uint32_t* tile_gt = nullptr;     // [max_tiles]
     uint32_t* tile_eq = nullptr;     // [max_tiles]
     double* tile_q = nullptr;        // [max_tiles * 4] kept positive sum, negative sum, counts

@@ -67,6 +67,7 @@ struct DenseArgs {
 };
 
 constexpr uint32_t kTile = 1024;        // candidates per tile of the candidate passes
+constexpr uint32_t kTileDescWords = 8;  // words of a tile descriptor (two 16-byte loads)
 constexpr uint32_t kTileBlocks = 512;   // most blocks a candidate pass launches (4 waves each)
 
 struct CandArgs {
@@ -98,8 +99,7 @@ struct CandArgs {
     uint32_t* cand_val;   // [N] their value bits
     uint32_t* ten_cbase;  // [T + 1] first compact candidate of each tensor
     uint32_t* tile_base;  // [T + 1] first tile of each tensor
-    uint32_t* tile_ne0;   // [max tiles] non-empty unit holding each tile's first candidate
-    uint32_t* tile_tensor; // [max tiles] tensor of each tile
+    uint32_t* tile_desc;  // [max tiles * kTileDescWords] per tile, written by the layout pass: see TileView
     uint32_t* tile_gt;    // [max tiles]
     uint32_t* tile_eq;
     double* tile_q;       // [max tiles * 4]

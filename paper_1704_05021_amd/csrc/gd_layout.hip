@@ -156,14 +156,23 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
 }
 
 // Tiles of tensor t whose first candidate lies in [p, q) (dense-pass order
-// for a regular tensor, element order for a missed one): record t and the
-// non-empty unit index ne.
+// for a regular tensor, element order for a missed one): write each one's
+// descriptor, so that the candidate passes find all they need about a tile
+// in one load.  Words: tensor | miss << 31, the non-empty unit ne holding
+// the tile's first candidate, its compact candidates [p0, p1), the
+// segment's first tile, the segment's k, and the tensor's tiles [first, end).
 __device__ __forceinline__ void mark_tiles(const CandArgs& a, uint32_t t, uint32_t base, uint32_t p, uint32_t q,
                                            uint32_t ne) {
-    const uint32_t t0 = a.tile_base[t];
+    const uint32_t t0 = a.tile_base[t], t1 = a.tile_base[t + 1];
+    const uint32_t s = a.per_tensor ? t : 0u;
+    const uint32_t miss = a.seg[s].miss != 0 ? 0x80000000u : 0u;
+    const uint32_t k = keep_of(a.seg_off[s + 1] - a.seg_off[s], a.keep_ppm);
+    const uint32_t c0 = a.ten_cbase[t], c1 = a.ten_cbase[t + 1];
     for (uint32_t j = p > base ? (p - base + kTile - 1) / kTile : 0u; base + j * kTile < q; ++j) {
-        a.tile_tensor[t0 + j] = t;
-        a.tile_ne0[t0 + j] = ne;
+        const uint32_t p0 = c0 + j * kTile, p1 = p0 + kTile < c1 ? p0 + kTile : c1;
+        uint4* d = reinterpret_cast<uint4*>(a.tile_desc + (size_t)(t0 + j) * kTileDescWords);
+        d[0] = make_uint4(t | miss, ne, p0, p1);
+        d[1] = make_uint4(a.per_tensor ? t0 : 0u, k, t0, t1);
     }
 }
 
