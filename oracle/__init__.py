@@ -58,8 +58,8 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.gdo_splitmix64.restype = u64
     lib.gdo_sample_position.argtypes = [u64, u32, u64, u64, u64, u64]
     lib.gdo_sample_position.restype = u64
-    lib.gdo_compress_sampled.argtypes = [vp, vp, vp, vp, u32, dbl, i32, u32, u64, vp, vp, vp, u64,
-                                         ctypes.POINTER(u64)]
+    lib.gdo_compress_sampled.argtypes = [vp, vp, vp, vp, u32, dbl, i32, u32, u64, i32, vp, vp, vp, vp, vp, u64,
+                                         ctypes.POINTER(u64), vp]
     lib.gdo_compress_sampled.restype = i32
     return lib
 
@@ -193,8 +193,12 @@ def compress_sampled(
     base: Optional[np.ndarray] = None,
     capacity: Optional[int] = None,
     lib: Optional[ctypes.CDLL] = None,
+    quant=False,
+    columns: Optional[Sequence[int]] = None,
 ) -> Compressed:
-    """Algorithm 1 with the threshold selected on a sample (Section 4); inputs are not modified."""
+    """Algorithm 1 with the threshold selected on a sample (Section 4), optionally with the 1-bit
+    quantisation of Section 5.4 over the entries sent (quant and columns as ``compress``); inputs are
+    not modified."""
     lib = lib or load()
     g = np.ascontiguousarray(grad, dtype=np.float32)
     r = np.array(residual, dtype=np.float32, copy=True)
@@ -206,14 +210,20 @@ def compress_sampled(
     idx = np.zeros(max(cap, 1), np.uint32)
     val = np.zeros(max(cap, 1), np.float32)
     counts = np.zeros(T, np.uint32)
+    quant = int(quant)
+    cols = None if columns is None else np.ascontiguousarray(columns, dtype=np.uint32)
+    groups = int(cols.astype(np.int64).sum()) if (quant == 4 and cols is not None) else T
+    bits = np.zeros(max((cap + 31) // 32, 1), np.uint32) if quant else None
+    means = np.zeros(2 * groups, np.float32) if quant else None
     k = ctypes.c_uint64(0)
     rc = lib.gdo_compress_sampled(_ptr(g), _ptr(b), _ptr(r), _ptr(off), T, float(drop_ratio), int(per_tensor),
-                                  int(sample_ppm), int(seed), _ptr(idx), _ptr(val), _ptr(counts), cap,
-                                  ctypes.byref(k))
+                                  int(sample_ppm), int(seed), quant, _ptr(idx), _ptr(val), _ptr(bits), _ptr(means),
+                                  _ptr(counts), cap, ctypes.byref(k), _ptr(cols))
     if rc != 0:
         raise ValueError(f"gdo_compress_sampled failed with status {rc}")
-    k = int(k.value)
-    return Compressed(idx[:k].copy(), val[:k].copy(), r, counts, None, None)
+    k = min(int(k.value), cap)
+    return Compressed(idx[:k].copy(), val[:k].copy(), r, counts,
+                      None if bits is None else bits[:(k + 31) // 32].copy(), means)
 
 
 def apply_sparse(params: np.ndarray, idx: List[np.ndarray], val: List[np.ndarray], lr: float = 1.0,

@@ -144,6 +144,142 @@ std::vector<uint8_t> exact_keep(const std::vector<float>& acc, const std::vector
 
 }  // namespace
 
+// Section 5.4, 1-bit quantisation with error feedback (R5, R10, R13): each
+// of the k entries sent (idx, val, in tensor order as tensor_counts gives
+// them) is sent as the centre of its group and sign, and acc minus that
+// centre goes back into the residual.  Centres are taken over the entries
+// sent; the threshold centre is the smallest sent magnitude of the threshold
+// segment (one segment, or one per tensor when per_tensor).
+static void quantise_sent(const uint64_t* offsets, uint32_t T, bool per_tensor, int quant, const uint32_t* columns,
+                          const uint32_t* idx, const float* val, const uint32_t* tensor_counts, uint64_t k,
+                          uint32_t* sign_bits, float* means, float* residual) {
+    const size_t nseg = per_tensor ? T : 1u;
+    const uint64_t words = (k + 31) / 32;
+    for (uint64_t w = 0; w < words; ++w) sign_bits[w] = 0;
+    // group of every output slot: its tensor, or its column for quant 4
+    std::vector<uint64_t> colbase(T + 1, 0);
+    for (uint32_t t = 0; t < T; ++t) colbase[t + 1] = colbase[t] + (quant == 4 && columns ? columns[t] : 1);
+    std::vector<uint64_t> group(k);
+    {
+        uint64_t q = 0;
+        for (uint32_t t = 0; t < T; ++t) {
+            for (uint32_t c = 0; c < tensor_counts[t] && q < k; ++c, ++q) {
+                uint64_t g = t;
+                if (quant == 4) {
+                    const uint64_t cols = columns ? columns[t] : 1;
+#ifdef GDO_MUTANT_COLUMN_IS_ROW
+                    g = colbase[t] + ((idx[q] - offsets[t]) / cols) % cols;  // mutant: rows, not columns
+#else
+                    g = colbase[t] + (idx[q] - offsets[t]) % cols;
+#endif
+                }
+                group[q] = g;
+            }
+        }
+    }
+    const uint64_t G = quant == 4 ? colbase[T] : T;
+    std::vector<float> pos_c(G, 0.0f), neg_c(G, 0.0f);
+    if (quant == 1 || quant == 4) {
+        // averages per group, summed in double in ascending index
+        std::vector<double> ps(G, 0.0), ns(G, 0.0);
+        std::vector<uint64_t> pn(G, 0), nn(G, 0);
+        for (uint64_t q = 0; q < k; ++q) {
+            if (val[q] < 0.0f) {
+                ns[group[q]] += (double)val[q];
+                ++nn[group[q]];
+            } else {
+                ps[group[q]] += (double)val[q];
+                ++pn[group[q]];
+            }
+        }
+        for (uint64_t g = 0; g < G; ++g) {
+            pos_c[g] = pn[g] ? (float)(ps[g] / (double)pn[g]) : 0.0f;
+            neg_c[g] = nn[g] ? (float)(ns[g] / (double)nn[g]) : 0.0f;
+        }
+    } else if (quant == 3) {
+        // one average of each sign over the whole call
+        double ps = 0.0, ns = 0.0;
+        uint64_t pn = 0, nn = 0;
+        for (uint64_t q = 0; q < k; ++q) {
+            if (val[q] < 0.0f) {
+                ns += (double)val[q];
+                ++nn;
+            } else {
+                ps += (double)val[q];
+                ++pn;
+            }
+        }
+        const float pc = pn ? (float)(ps / (double)pn) : 0.0f;
+        const float nc = nn ? (float)(ns / (double)nn) : 0.0f;
+        for (uint64_t g = 0; g < G; ++g) {
+#ifdef GDO_MUTANT_GLOBAL_MEAN_PER_TENSOR
+            (void)pc;
+            (void)nc;
+#else
+            pos_c[g] = pc;
+            neg_c[g] = nc;
+#endif
+        }
+#ifdef GDO_MUTANT_GLOBAL_MEAN_PER_TENSOR
+        // mutant: per-tensor averages instead of one over the call
+        std::vector<double> ps2(G, 0.0), ns2(G, 0.0);
+        std::vector<uint64_t> pn2(G, 0), nn2(G, 0);
+        for (uint64_t q = 0; q < k; ++q) {
+            if (val[q] < 0.0f) { ns2[group[q]] += val[q]; ++nn2[group[q]]; }
+            else { ps2[group[q]] += val[q]; ++pn2[group[q]]; }
+        }
+        for (uint64_t g = 0; g < G; ++g) {
+            pos_c[g] = pn2[g] ? (float)(ps2[g] / (double)pn2[g]) : 0.0f;
+            neg_c[g] = nn2[g] ? (float)(ns2[g] / (double)nn2[g]) : 0.0f;
+        }
+#endif
+    } else {
+        // quant 2: the smallest kept magnitude of each threshold segment
+        std::vector<uint32_t> seg_min(nseg, 0xFFFFFFFFu);
+        std::vector<uint8_t> seg_any(nseg, 0);
+        uint64_t q = 0;
+        for (uint32_t t = 0; t < T; ++t) {
+            const uint32_t sg = per_tensor ? t : 0u;
+            for (uint32_t c = 0; c < tensor_counts[t]; ++c, ++q) {
+                const uint32_t kk = key_of(val[q]);
+#ifdef GDO_MUTANT_THRESHOLD_MAX
+                if (!seg_any[sg] || kk > seg_min[sg]) seg_min[sg] = kk;  // mutant: the largest instead
+#else
+                if (!seg_any[sg] || kk < seg_min[sg]) seg_min[sg] = kk;
+#endif
+                seg_any[sg] = 1;
+            }
+        }
+        for (uint32_t t = 0; t < T; ++t) {
+            const uint32_t sg = per_tensor ? t : 0u;
+            if (!seg_any[sg]) continue;
+            float mag;
+            std::memcpy(&mag, &seg_min[sg], sizeof mag);
+            pos_c[t] = mag;
+            neg_c[t] = -mag;
+        }
+    }
+    for (uint64_t g = 0; g < G; ++g) {
+#ifdef GDO_MUTANT_SWAP_CENTRES
+        means[2 * g + 0] = neg_c[g];
+        means[2 * g + 1] = pos_c[g];
+#else
+        means[2 * g + 0] = pos_c[g];
+        means[2 * g + 1] = neg_c[g];
+#endif
+    }
+    for (uint64_t q = 0; q < k; ++q) {
+        const bool neg = val[q] < 0.0f;
+#ifdef GDO_MUTANT_BITS_MSB_FIRST
+        if (neg) sign_bits[q >> 5] |= 1u << (31 - (q & 31));
+#else
+        if (neg) sign_bits[q >> 5] |= 1u << (q & 31);
+#endif
+        const float sent = neg ? means[2 * group[q] + 1] : means[2 * group[q] + 0];
+        residual[idx[q]] = val[q] - sent;
+    }
+}
+
 extern "C" {
 
 // R1: the keep fraction in parts per million.
@@ -244,135 +380,8 @@ int gdo_compress(const float* grad, const float* base, float* residual, const ui
 #endif
     }
 
-    // Section 5.4, 1-bit quantisation with error feedback (R5, R10): each
-    // kept entry is sent as the centre of its group and sign, and acc minus
-    // that centre goes back into the residual.
-    if (quant) {
-        const uint64_t words = (k_total + 31) / 32;
-        for (uint64_t w = 0; w < words; ++w) sign_bits[w] = 0;
-        // group of every output slot: its tensor, or its column for quant 4
-        std::vector<uint64_t> colbase(T + 1, 0);
-        for (uint32_t t = 0; t < T; ++t) colbase[t + 1] = colbase[t] + (quant == 4 && columns ? columns[t] : 1);
-        std::vector<uint64_t> group(k_total);
-        {
-            uint64_t q = 0;
-            for (uint32_t t = 0; t < T; ++t) {
-                for (uint32_t c = 0; c < tensor_counts[t]; ++c, ++q) {
-                    uint64_t g = t;
-                    if (quant == 4) {
-                        const uint64_t cols = columns ? columns[t] : 1;
-#ifdef GDO_MUTANT_COLUMN_IS_ROW
-                        g = colbase[t] + ((idx[q] - offsets[t]) / cols) % cols;  // mutant: rows, not columns
-#else
-                        g = colbase[t] + (idx[q] - offsets[t]) % cols;
-#endif
-                    }
-                    group[q] = g;
-                }
-            }
-        }
-        const uint64_t G = quant == 4 ? colbase[T] : T;
-        std::vector<float> pos_c(G, 0.0f), neg_c(G, 0.0f);
-        if (quant == 1 || quant == 4) {
-            // averages per group, summed in double in ascending index
-            std::vector<double> ps(G, 0.0), ns(G, 0.0);
-            std::vector<uint64_t> pn(G, 0), nn(G, 0);
-            for (uint64_t q = 0; q < k_total; ++q) {
-                if (val[q] < 0.0f) {
-                    ns[group[q]] += (double)val[q];
-                    ++nn[group[q]];
-                } else {
-                    ps[group[q]] += (double)val[q];
-                    ++pn[group[q]];
-                }
-            }
-            for (uint64_t g = 0; g < G; ++g) {
-                pos_c[g] = pn[g] ? (float)(ps[g] / (double)pn[g]) : 0.0f;
-                neg_c[g] = nn[g] ? (float)(ns[g] / (double)nn[g]) : 0.0f;
-            }
-        } else if (quant == 3) {
-            // one average of each sign over the whole call
-            double ps = 0.0, ns = 0.0;
-            uint64_t pn = 0, nn = 0;
-            for (uint64_t q = 0; q < k_total; ++q) {
-                if (val[q] < 0.0f) {
-                    ns += (double)val[q];
-                    ++nn;
-                } else {
-                    ps += (double)val[q];
-                    ++pn;
-                }
-            }
-            const float pc = pn ? (float)(ps / (double)pn) : 0.0f;
-            const float nc = nn ? (float)(ns / (double)nn) : 0.0f;
-            for (uint64_t g = 0; g < G; ++g) {
-#ifdef GDO_MUTANT_GLOBAL_MEAN_PER_TENSOR
-                (void)pc;
-                (void)nc;
-#else
-                pos_c[g] = pc;
-                neg_c[g] = nc;
-#endif
-            }
-#ifdef GDO_MUTANT_GLOBAL_MEAN_PER_TENSOR
-            // mutant: per-tensor averages instead of one over the call
-            std::vector<double> ps2(G, 0.0), ns2(G, 0.0);
-            std::vector<uint64_t> pn2(G, 0), nn2(G, 0);
-            for (uint64_t q = 0; q < k_total; ++q) {
-                if (val[q] < 0.0f) { ns2[group[q]] += val[q]; ++nn2[group[q]]; }
-                else { ps2[group[q]] += val[q]; ++pn2[group[q]]; }
-            }
-            for (uint64_t g = 0; g < G; ++g) {
-                pos_c[g] = pn2[g] ? (float)(ps2[g] / (double)pn2[g]) : 0.0f;
-                neg_c[g] = nn2[g] ? (float)(ns2[g] / (double)nn2[g]) : 0.0f;
-            }
-#endif
-        } else {
-            // quant 2: the smallest kept magnitude of each threshold segment
-            std::vector<uint32_t> seg_min(seg.size(), 0xFFFFFFFFu);
-            std::vector<uint8_t> seg_any(seg.size(), 0);
-            uint64_t q = 0;
-            for (uint32_t t = 0; t < T; ++t) {
-                const uint32_t sg = per_tensor ? t : 0u;
-                for (uint32_t c = 0; c < tensor_counts[t]; ++c, ++q) {
-                    const uint32_t kk = key_of(val[q]);
-#ifdef GDO_MUTANT_THRESHOLD_MAX
-                    if (!seg_any[sg] || kk > seg_min[sg]) seg_min[sg] = kk;  // mutant: the largest instead
-#else
-                    if (!seg_any[sg] || kk < seg_min[sg]) seg_min[sg] = kk;
-#endif
-                    seg_any[sg] = 1;
-                }
-            }
-            for (uint32_t t = 0; t < T; ++t) {
-                const uint32_t sg = per_tensor ? t : 0u;
-                if (!seg_any[sg]) continue;
-                float mag;
-                std::memcpy(&mag, &seg_min[sg], sizeof mag);
-                pos_c[t] = mag;
-                neg_c[t] = -mag;
-            }
-        }
-        for (uint64_t g = 0; g < G; ++g) {
-#ifdef GDO_MUTANT_SWAP_CENTRES
-            means[2 * g + 0] = neg_c[g];
-            means[2 * g + 1] = pos_c[g];
-#else
-            means[2 * g + 0] = pos_c[g];
-            means[2 * g + 1] = neg_c[g];
-#endif
-        }
-        for (uint64_t q = 0; q < k_total; ++q) {
-            const bool neg = val[q] < 0.0f;
-#ifdef GDO_MUTANT_BITS_MSB_FIRST
-            if (neg) sign_bits[q >> 5] |= 1u << (31 - (q & 31));
-#else
-            if (neg) sign_bits[q >> 5] |= 1u << (q & 31);
-#endif
-            const float sent = neg ? means[2 * group[q] + 1] : means[2 * group[q] + 0];
-            residual[idx[q]] = val[q] - sent;
-        }
-    }
+    if (quant) quantise_sent(offsets, T, per_tensor != 0, quant, columns, idx, val, tensor_counts, k_total, sign_bits,
+                             means, residual);
     return 0;
 }
 
@@ -489,21 +498,30 @@ uint64_t gdo_sample_position(uint64_t seed, uint32_t s, uint64_t a, uint64_t n, 
 #endif
 }
 
-// Algorithm 1 with the threshold selected on a sample (Section 4, R9).
-// Arguments as gdo_compress, without quantisation, plus sample_ppm (1..1e6)
-// and seed.  idx/val may be null when capacity is 0.  *out_k receives the
-// number of entries sent.  Returns 0 on success, 1 on bad arguments.
+// Algorithm 1 with the threshold selected on a sample (Section 4, R9), and
+// optionally the 1-bit quantisation of Section 5.4 over the entries sent
+// (R13).  Arguments as gdo_compress plus sample_ppm (1..1e6) and seed;
+// idx/val (and sign_bits when quant != 0) may be null when capacity is 0.
+// *out_k receives the number of entries sent.  Returns 0 on success, 1 on
+// bad arguments.
 int gdo_compress_sampled(const float* grad, const float* base, float* residual, const uint64_t* offsets,
                          uint32_t T, double drop_ratio, int per_tensor, uint32_t sample_ppm, uint64_t seed,
-                         uint32_t* idx, float* val, uint32_t* tensor_counts, uint64_t capacity, uint64_t* out_k) {
+                         int quant, uint32_t* idx, float* val, uint32_t* sign_bits, float* means,
+                         uint32_t* tensor_counts, uint64_t capacity, uint64_t* out_k, const uint32_t* columns) {
     if (!grad || !residual || !offsets || T == 0 || !tensor_counts) return 1;
     if (capacity && (!idx || !val)) return 1;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return 1;
     if (sample_ppm == 0 || sample_ppm > 1000000u) return 1;
+    if (quant < 0 || quant > 4) return 1;
+    if (quant && (!means || (capacity && !sign_bits))) return 1;
     const uint64_t N = offsets[T];
     if (offsets[0] != 0 || N > 0xFFFFFFFFull) return 1;
     for (uint32_t t = 0; t < T; ++t)
         if (offsets[t + 1] < offsets[t]) return 1;
+    if (quant == 4 && columns) {
+        for (uint32_t t = 0; t < T; ++t)
+            if (columns[t] == 0 || (offsets[t + 1] - offsets[t]) % columns[t] != 0) return 1;
+    }
     const uint64_t keep_ppm = gdo_keep_ppm(drop_ratio);
 
     // Algorithm 1, first line: add the carried residual (pulls: delta first, R7).
@@ -574,6 +592,9 @@ int gdo_compress_sampled(const float* grad, const float* base, float* residual, 
     }
     if (out_k) *out_k = j;
     for (uint64_t i = 0; i < N; ++i) residual[i] = keep[i] ? 0.0f : acc[i];
+    if (quant)
+        quantise_sent(offsets, T, per_tensor != 0, quant, columns, idx, val, tensor_counts, std::min(j, capacity),
+                      sign_bits, means, residual);
     return 0;
 }
 

@@ -638,6 +638,78 @@ def pin_sampled_capacity(lib):
         assert np.array_equal(bits(out.residual), bits(np.where(sent, np.float32(0), acc)))
 
 
+def pin_sampled_quant_full_sample_is_exact(lib):
+    """Every entry sampled and distinct magnitudes: each 1-bit form under the sampled threshold is the exact one."""
+    rng = np.random.default_rng(24)
+    offsets = [0, 3000, 3001, 7000, 7000, 10_000]
+    columns = [30, 1, 43, 9, 100]  # 3999 = 3 * 31 * 43
+    g = rng.permutation(np.arange(1, 10_001, dtype=np.float32)) * np.where(rng.random(10_000) < 0.5, -1, 1)
+    g = (g * np.float32(1e-3)).astype(np.float32)
+    r = np.zeros(10_000, np.float32)
+    for per in (False, True):
+        for quant in (1, 2, 3, 4):
+            cols = columns if quant == 4 else None
+            a = oracle.compress_sampled(g, r, offsets, 0.9, per_tensor=per, sample_ppm=1_000_000, seed=2, lib=lib,
+                                        quant=quant, columns=cols)
+            b = oracle.compress(g, r, offsets, 0.9, per_tensor=per, quant=quant, columns=cols, lib=lib)
+            assert np.array_equal(a.idx, b.idx) and np.array_equal(bits(a.val), bits(b.val)), (per, quant)
+            assert np.array_equal(bits(a.means), bits(b.means)), (per, quant)
+            assert np.array_equal(a.sign_bits, b.sign_bits), (per, quant)
+            assert np.array_equal(bits(a.residual), bits(b.residual)), (per, quant)
+
+
+def pin_sampled_quant_sent_entries(lib):
+    """Under the sampled threshold and a short output buffer, centres, sign bits and error feedback cover exactly
+    the entries sent (exact arithmetic); the threshold centre is the smallest sent magnitude."""
+    rng = np.random.default_rng(25)
+    offsets = [0, 2000, 2001, 5001]
+    columns = [40, 1, 60]
+    T, N = len(offsets) - 1, offsets[-1]
+    tensor_of = np.searchsorted(np.array(offsets[1:]), np.arange(N), side="right")
+    g = (rng.standard_t(3, N) * 1e-3).astype(np.float32)
+    r = rng.normal(0, 1e-3, N).astype(np.float32)
+    acc = g + r
+    for per in (False, True):
+        full = oracle.compress_sampled(g, r, offsets, 0.95, per_tensor=per, sample_ppm=100_000, seed=9, lib=lib)
+        K = full.idx.size
+        assert K > 40
+        cap = K * 2 // 3
+        for quant in (1, 2, 3, 4):
+            out = oracle.compress_sampled(g, r, offsets, 0.95, per_tensor=per, sample_ppm=100_000, seed=9,
+                                          capacity=cap, lib=lib, quant=quant, columns=columns if quant == 4 else None)
+            k = out.idx.size
+            assert k == cap and np.array_equal(out.idx, full.idx[:cap])
+            _check_sign_bits(out, k)
+            kt = tensor_of[out.idx]
+            if quant == 4:
+                colbase = np.concatenate([[0], np.cumsum(columns)])
+                grp = np.array([colbase[t] + (int(i) - offsets[t]) % columns[t] for i, t in zip(out.idx, kt)])
+                G = int(colbase[-1])
+            elif quant == 3:
+                grp, G = np.zeros(k, np.int64), 1
+            else:
+                grp, G = kt.astype(np.int64), T
+            for q in range(k):
+                c = out.means[2 * (kt[q] if quant == 3 else grp[q]) + int(out.val[q] < 0)]
+                assert within_half_ulp(out.residual[out.idx[q]], Fraction(float(out.val[q])) - Fraction(float(c)))
+            if quant == 2:
+                for t in range(T):
+                    seg = (kt == t) if per else np.ones(k, bool)
+                    if seg.any():
+                        assert bits([out.means[2 * t]])[0] == bits([np.min(np.abs(out.val[seg]))])[0]
+            else:
+                for gi in range(G):
+                    v = out.val[grp == gi]
+                    pos = [x for x in v if not (x < 0)]
+                    neg = [x for x in v if x < 0]
+                    mp, mn = out.means[2 * gi], out.means[2 * gi + 1]
+                    assert within_half_ulp(mp, _exact_avg(pos)) if pos else bits([mp])[0] == 0
+                    assert within_half_ulp(mn, _exact_avg(neg)) if neg else bits([mn])[0] == 0
+            unsent = np.ones(N, bool)
+            unsent[out.idx] = False
+            assert np.array_equal(bits(out.residual[unsent]), bits(acc[unsent])), (per, quant)
+
+
 def pin_sampled_statistics(lib):
     """On iid data the kept fraction tracks 1 - R; entries above the sample maximum when k_m = 0."""
     rng = np.random.default_rng(24)
@@ -680,4 +752,6 @@ ALL_PINS = [
     pin_sampled_brute,
     pin_sampled_capacity,
     pin_sampled_statistics,
+    pin_sampled_quant_full_sample_is_exact,
+    pin_sampled_quant_sent_entries,
 ]
