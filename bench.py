@@ -73,7 +73,8 @@ def cpu_baseline(w, grads_host, budget_s, sample_ppm=0, quant=0):
         g = grads_host[done % len(grads_host)]
         if sample_ppm:
             o = oracle.compress_sampled(g, residual, off, w.drop, per_tensor=w.per_tensor, sample_ppm=sample_ppm,
-                                        seed=done, capacity=SAMPLED_CAPACITY_PCT * w.layout.numel // 100, lib=lib)
+                                        seed=done, capacity=SAMPLED_CAPACITY_PCT * w.layout.numel // 100, lib=lib,
+                                        quant=quant, columns=w.layout.columns if quant == 4 else None)
         else:
             o = oracle.compress(g, residual, off, w.drop, per_tensor=w.per_tensor, quant=quant, lib=lib,
                                 columns=w.layout.columns if quant == 4 else None)
@@ -299,15 +300,12 @@ def main():
     if quant == 4:
         comp.set_columns(w.layout.columns)
     if sampled:
-        if quant:
-            print("the sampled selection has no quantised form", file=sys.stderr)
-            sys.exit(2)
         cap = SAMPLED_CAPACITY_PCT * N // 100
-        out = comp.alloc_out(1.0, w.per_tensor, capacity=cap)
+        out = comp.alloc_out(1.0, w.per_tensor, quant, capacity=cap)
 
         def step(i):
             comp.compress_sampled(grads[i % len(grads)], residual, w.drop, per_tensor=w.per_tensor,
-                                  sample_ppm=args.sample_ppm, seed=i, out=out, capacity=cap)
+                                  sample_ppm=args.sample_ppm, seed=i, out=out, capacity=cap, quant=quant)
 
         def kept_now():
             return int(out.tensor_counts[:comp.T].cpu().numpy().view(np.uint32).astype(np.int64).sum())

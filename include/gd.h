@@ -191,15 +191,21 @@ uint64_t gd_quant_centres(const gd_ctx* ctx, gd_quant quant);
  *     out->capacity of them (idx and val may be NULL when capacity is 0);
  *     kept entries past the capacity are not sent and keep acc in the
  *     residual.  tensor_counts[t] receives the entries of tensor t actually
- *     sent; their sum is the output length.  sign_bits and means are ignored:
- *     no quantisation in this mode.
- *   residual (in/out): +0.0 at sent entries, acc elsewhere.
- *   Returns GD_ERR_ARG for a bad sample_ppm or drop ratio, a NULL pointer or
- *   a bad mode, GD_ERR_ALIGN as gd_compress; never GD_ERR_CAPACITY.
+ *     sent; their sum is the output length.
+ *   quant: as gd_compress (Section 5.4 on what this dropping sends).  The
+ *     centres are taken over the entries sent.  The threshold centre is the
+ *     smallest sent magnitude of the segment, which is above the sample
+ *     threshold.  Sign bits are written for the entries sent; means needs
+ *     gd_quant_centres() floats, and sign_bits ceil(capacity/32) words.
+ *   residual (in/out): +0.0 at sent entries (acc minus the sent centre under
+ *     a quantised form), acc elsewhere.
+ *   Returns GD_ERR_ARG for a bad sample_ppm, drop ratio or quant, a NULL
+ *   pointer or a bad mode, GD_ERR_ALIGN as gd_compress; never
+ *   GD_ERR_CAPACITY.
  */
 gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base, float* residual,
                               double drop_ratio, gd_threshold mode, uint32_t sample_ppm, uint64_t seed,
-                              const gd_sparse* out, void* stream);
+                              gd_quant quant, const gd_sparse* out, void* stream);
 
 /*
  * gd_apply_sparse - server-side apply of sparse pushes to a parameter shard

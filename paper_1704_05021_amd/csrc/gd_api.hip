@@ -198,6 +198,7 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
         qa.seg = ctx->scr.seg;
         qa.columns = ctx->cols.columns;
         qa.colbase = ctx->cols.colbase;
+        qa.sampled = sampled ? 1u : 0u;
         qa.groups = ctx->cols.groups;
         qa.csum = ctx->cols.csum;
         qa.ccnt = ctx->cols.ccnt;
@@ -437,9 +438,11 @@ uint64_t gd_quant_centres(const gd_ctx* ctx, gd_quant quant) {
 
 gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base, float* residual,
                               double drop_ratio, gd_threshold mode, uint32_t sample_ppm, uint64_t seed,
-                              const gd_sparse* out, void* stream) {
+                              gd_quant quant, const gd_sparse* out, void* stream) {
     if (!ctx || !grad || !residual || !out) return GD_ERR_ARG;
     if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
+    if (quant < GD_QUANT_NONE || quant > GD_QUANT_COLUMN_MEAN) return GD_ERR_ARG;
+    if (quant != GD_QUANT_NONE && (!out->means || (out->capacity && !out->sign_bits))) return GD_ERR_ARG;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
     if (sample_ppm == 0 || sample_ppm > 1000000u) return GD_ERR_ARG;
     if (!out->tensor_counts || (out->capacity && (!out->idx || !out->val))) return GD_ERR_ARG;
@@ -475,7 +478,8 @@ gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base,
     sa.tensor_counts = out->tensor_counts;
     if (gd::launch_sampled(sa, base != nullptr, (uint32_t)max_samples, st) != hipSuccess) return GD_ERR_HIP;
 
-    return run_after_bracket(ctx, grad, base, residual, per, ppm, true, GD_QUANT_NONE, 0, out, st);
+    // the number sent is only known on the device: quantisation covers up to the capacity
+    return run_after_bracket(ctx, grad, base, residual, per, ppm, true, quant, out->capacity, out, st);
 }
 
 gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const uint32_t* const* idx,

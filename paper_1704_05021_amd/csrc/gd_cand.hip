@@ -438,6 +438,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         const uint64_t ob = a.out_base[v.s];
         double sp = 0.0, sn = 0.0;
         uint32_t np = 0, nn = 0;
+        uint32_t kmin = kNoKey;  // sampled threshold, threshold centre: smallest key sent by this lane
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
             const bool valid = v.p0 + r * kWave + lane < v.p1;
@@ -453,6 +454,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             if (kept) {
                 o.idx[pos] = ix[r];
                 o.val[pos] = __uint_as_float(vb[r]);
+                if (QUANT && a.sampled && o.qkind == kQuantThreshold) kmin = key < kmin ? key : kmin;
                 if (QUANT && o.qkind != kQuantColumnMean) {  // column sums come from the sent entries later
                     const float x = __uint_as_float(vb[r]);
                     if (x < 0.0f) {
@@ -506,10 +508,15 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             if (lane == 0) o.tensor_counts[v.t] = (uint64_t)cnt < room ? cnt : (uint32_t)room;
         }
         if (QUANT) {
-            sp = wave_sum(sp);
-            sn = wave_sum(sn);
-            np = wave_sum(np);
-            nn = wave_sum(nn);
+            if (a.sampled && o.qkind == kQuantThreshold) {
+                // the tile's smallest sent key (kNoKey if none) in place of its positive sum
+                sp = (double)wave_min(kmin);
+            } else {
+                sp = wave_sum(sp);
+                sn = wave_sum(sn);
+                np = wave_sum(np);
+                nn = wave_sum(nn);
+            }
             if (lane == 0) {
                 a.tile_q[4 * (size_t)tile + 0] = sp;
                 a.tile_q[4 * (size_t)tile + 1] = sn;

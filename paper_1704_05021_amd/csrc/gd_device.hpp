@@ -139,6 +139,19 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
 // Sum over the 64 lanes, in every lane.  Every lane must be active.
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) { return lane_value(wave_incl_scan(v), kWave - 1); }
 
+// Minimum over the 64 lanes, in every lane, by the same DPP steps (`old` is
+// then the identity of min).  Every lane must be active.
+__device__ __forceinline__ uint32_t wave_min(uint32_t v) {
+    constexpr int kId = -1;  // 0xFFFFFFFF
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)v, 0x111, 0xF, 0xF, false));  // row_shr:1
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)v, 0x112, 0xF, 0xF, false));  // row_shr:2
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)v, 0x114, 0xF, 0xF, false));  // row_shr:4
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)v, 0x118, 0xF, 0xF, false));  // row_shr:8
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)v, 0x142, 0xA, 0xF, false));  // row_bcast:15
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)v, 0x143, 0xC, 0xF, false));  // row_bcast:31
+    return lane_value(v, kWave - 1);
+}
+
 __device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
     for (int d = kWave / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, kWave);

@@ -143,6 +143,7 @@ struct QuantArgs {
     const SegState* seg;
     const uint32_t* columns;
     const uint32_t* colbase;
+    uint32_t sampled;           // 1 under a sampled threshold: the count is k_total at most, qbase[T] exactly
     uint32_t groups;            // column groups (column-wise centres)
     double* csum;               // [2 * groups] column sums (positive, negative), zero on entry, cleared after use
     uint32_t* ccnt;             // [2 * groups] column counts, likewise

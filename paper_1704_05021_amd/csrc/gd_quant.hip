@@ -40,11 +40,24 @@ __global__ __launch_bounds__(kBlock) void k_means(QuantArgs q) {
     if (q.qkind == kQuantColumnMean) return;
     float pos = 0.0f, neg = 0.0f;
     if (q.qkind == kQuantThreshold) {
-        // the exact threshold key is the smallest kept magnitude
+        // the smallest kept magnitude of the segment: the exact threshold key,
+        // or under a sampled threshold the smallest key sent, the minimum over
+        // the segment's tiles
         const uint32_t s = q.per_tensor ? t : 0u;
-        if (keep_of(q.seg_off[s + 1] - q.seg_off[s], q.keep_ppm) > 0) {
-            pos = __uint_as_float(q.seg[s].thr);
-            neg = __uint_as_float(q.seg[s].thr | 0x80000000u);
+        uint32_t key = kNoKey;
+        if (q.sampled) {
+            const uint32_t g0 = q.per_tensor ? q.tile_base[t] : 0u, g1 = q.per_tensor ? q.tile_base[t + 1] : q.tile_base[q.T];
+            for (uint32_t g = g0 + lane; g < g1; g += kWave) {
+                const uint32_t x = (uint32_t)q.tile_q[4 * (size_t)g + 0];
+                key = x < key ? x : key;
+            }
+            key = wave_min(key);
+        } else if (keep_of(q.seg_off[s + 1] - q.seg_off[s], q.keep_ppm) > 0) {
+            key = q.seg[s].thr;
+        }
+        if (key != kNoKey) {
+            pos = __uint_as_float(key);
+            neg = __uint_as_float(key | 0x80000000u);
         }
     } else {
         const bool global = q.qkind == kQuantGlobalMean;
@@ -142,7 +155,8 @@ __global__ __launch_bounds__(kBlock) void k_colmeans(QuantArgs q) {
 
 __global__ __launch_bounds__(kBlock) void k_quant(QuantArgs q) {
     const uint64_t j = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    const bool valid = j < q.k_total;
+    const uint64_t total = q.qbase[q.T];  // entries sent (the grid covers k_total >= total)
+    const bool valid = j < total;
     bool neg = false;
     if (valid) {
         // tensor of output slot j: the last t with qbase[t] <= j
@@ -161,7 +175,7 @@ __global__ __launch_bounds__(kBlock) void k_quant(QuantArgs q) {
     }
     const uint64_t m = ballot(valid && neg);
     const uint64_t jw = j - lane_id();  // first slot of this wave, a multiple of 64
-    const uint64_t words = (q.k_total + 31) / 32;
+    const uint64_t words = (total + 31) / 32;
     if (lane_id() == 0 && jw / 32 < words) q.sign_bits[jw / 32] = (uint32_t)m;
     if (lane_id() == 1 && jw / 32 + 1 < words) q.sign_bits[jw / 32 + 1] = (uint32_t)(m >> 32);
 }

@@ -88,7 +88,7 @@ def _lib() -> ctypes.CDLL:
     lib.gd_keep_total.restype = u64
     lib.gd_compress.argtypes = [vp, vp, vp, vp, dbl, i32, i32, ctypes.POINTER(_Sparse), vp]
     lib.gd_compress.restype = i32
-    lib.gd_compress_sampled.argtypes = [vp, vp, vp, vp, dbl, i32, u32, u64, ctypes.POINTER(_Sparse), vp]
+    lib.gd_compress_sampled.argtypes = [vp, vp, vp, vp, dbl, i32, u32, u64, i32, ctypes.POINTER(_Sparse), vp]
     lib.gd_compress_sampled.restype = i32
     lib.gd_apply_quantised.argtypes = [vp, vp, u32, vp, vp, vp, vp, i32, ctypes.c_float, vp]
     lib.gd_apply_quantised.restype = i32
@@ -282,25 +282,29 @@ class Compressor:
     def compress_sampled(self, grad: torch.Tensor, residual: torch.Tensor, drop_ratio: float = 0.99,
                          per_tensor: bool = False, sample_ppm: int = 1000, seed: int = 0,
                          base: Optional[torch.Tensor] = None, out: Optional[SparseOut] = None,
-                         capacity: Optional[int] = None,
+                         capacity: Optional[int] = None, quant=False,
                          stream: Optional[torch.cuda.Stream] = None) -> SparseOut:
         """One gd_compress_sampled call; ``residual`` is updated in place.
 
         The number sent is data dependent: it is ``out.tensor_counts.sum()``
         (read it after the stream has run).  ``out.k`` is left as None.
+        quant: as ``compress``, over the entries sent.
         """
         _check_f32(grad, "grad", self.N)
         _check_f32(residual, "residual", self.N)
         if base is not None:
             _check_f32(base, "base", self.N)
         if out is None:
-            out = self.alloc_out(1.0, per_tensor, capacity=self.N if capacity is None else capacity)
-        sp = _Sparse(out.idx.data_ptr(), out.val.data_ptr(), None, None, out.tensor_counts.data_ptr(),
+            out = self.alloc_out(1.0, per_tensor, quant, capacity=self.N if capacity is None else capacity)
+        sp = _Sparse(out.idx.data_ptr(), out.val.data_ptr(),
+                     out.sign_bits.data_ptr() if (quant and out.sign_bits is not None) else None,
+                     out.means.data_ptr() if (quant and out.means is not None) else None,
+                     out.tensor_counts.data_ptr(),
                      out.idx.numel() if capacity is None else min(int(capacity), out.idx.numel()))
         st = _lib().gd_compress_sampled(
             self._h, grad.data_ptr(), None if base is None else base.data_ptr(), residual.data_ptr(),
             float(drop_ratio), GD_PER_TENSOR if per_tensor else GD_GLOBAL, int(sample_ppm), int(seed),
-            ctypes.byref(sp), _stream_handle(stream))
+            int(quant), ctypes.byref(sp), _stream_handle(stream))
         if st != 0:
             raise GDError(st, "gd_compress_sampled")
         out.k = None

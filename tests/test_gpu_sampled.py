@@ -23,31 +23,42 @@ def _gpu():
     torch.cuda.set_device(0)
 
 
-def gpu_sampled(comp, grad, residual, drop, per_tensor, sample_ppm, seed, base=None, capacity=None) -> Result:
+def gpu_sampled(comp, grad, residual, drop, per_tensor, sample_ppm, seed, base=None, capacity=None,
+                quant=0) -> Result:
     dev = comp.device
     g = torch.from_numpy(np.ascontiguousarray(grad, np.float32)).to(dev)
     r = torch.from_numpy(np.ascontiguousarray(residual, np.float32)).to(dev)
     b = None if base is None else torch.from_numpy(np.ascontiguousarray(base, np.float32)).to(dev)
     o = comp.compress_sampled(g, r, drop, per_tensor=per_tensor, sample_ppm=sample_ppm, seed=seed, base=b,
-                              capacity=capacity)
+                              capacity=capacity, quant=quant)
     torch.cuda.synchronize()
     counts = o.tensor_counts[:comp.T].cpu().numpy().view(np.uint32).copy()
     k = int(counts.astype(np.int64).sum())
-    return Result(idx=o.idx[:k].cpu().numpy().view(np.uint32).copy(), val=o.val[:k].cpu().numpy().copy(),
-                  residual=r.cpu().numpy(), tensor_counts=counts)
+    res = Result(idx=o.idx[:k].cpu().numpy().view(np.uint32).copy(), val=o.val[:k].cpu().numpy().copy(),
+                 residual=r.cpu().numpy(), tensor_counts=counts)
+    if quant:
+        res.sign_bits = o.sign_bits[:(k + 31) // 32].cpu().numpy().view(np.uint32).copy()
+        res.means = o.means[:comp.quant_centres(quant)].cpu().numpy().copy()
+    return res
 
 
-def oracle_sampled(grad, residual, offsets, drop, per_tensor, sample_ppm, seed, base=None, capacity=None):
+def oracle_sampled(grad, residual, offsets, drop, per_tensor, sample_ppm, seed, base=None, capacity=None, quant=0,
+                   columns=None):
     o = oracle.compress_sampled(grad, residual, offsets, drop, per_tensor=per_tensor, sample_ppm=sample_ppm,
-                                seed=seed, base=base, capacity=capacity)
-    return Result(o.idx, o.val, o.residual, o.tensor_counts)
+                                seed=seed, base=base, capacity=capacity, quant=quant, columns=columns)
+    return Result(o.idx, o.val, o.residual, o.tensor_counts, o.sign_bits, o.means)
 
 
-def check(grad, residual, offsets, drop, per, ppm, seed, base=None, capacity=None, comp=None, what=""):
-    comp = comp or gd.Compressor(offsets)
-    g = gpu_sampled(comp, grad, residual, drop, per, ppm, seed, base, capacity)
-    o = oracle_sampled(grad, residual, offsets, drop, per, ppm, seed, base, capacity)
-    assert_parity(g, o, False, what)
+def check(grad, residual, offsets, drop, per, ppm, seed, base=None, capacity=None, comp=None, what="", quant=0,
+          columns=None):
+    """comp must already have ``columns`` set when it is passed in with quant 4."""
+    if comp is None:
+        comp = gd.Compressor(offsets)
+        if columns is not None:
+            comp.set_columns(columns)
+    g = gpu_sampled(comp, grad, residual, drop, per, ppm, seed, base, capacity, quant)
+    o = oracle_sampled(grad, residual, offsets, drop, per, ppm, seed, base, capacity, quant, columns)
+    assert_parity(g, o, quant, what)
     return o
 
 
@@ -187,3 +198,69 @@ def test_many_tensors():
     comp = gd.Compressor(offsets)
     for per in (True, False):
         check(g, r, offsets, 0.9, per, 50_000, 4, comp=comp, what=f"T={T} per={per}")
+
+
+QUANT = {"sign_mean": gd.GD_QUANT_SIGN_MEAN, "threshold": gd.GD_QUANT_THRESHOLD,
+         "global_mean": gd.GD_QUANT_GLOBAL_MEAN, "column_mean": gd.GD_QUANT_COLUMN_MEAN}
+
+
+def _divisor_columns(rng, sizes):
+    cols = []
+    for n in sizes:
+        divs = [d for d in range(1, min(int(n), 2048) + 1) if n % d == 0] if n else [1, 5]
+        cols.append(int(rng.choice(divs)))
+    return cols
+
+
+@pytest.mark.parametrize("kind", list(QUANT))
+@pytest.mark.parametrize("seed", range(3))
+def test_quantised(kind, seed):
+    """Each 1-bit form of Section 5.4 over what the sampled threshold sends, short output buffers included."""
+    rng = np.random.default_rng(2000 + seed)
+    T = int(rng.integers(1, 7))
+    sizes = rng.integers(0, 120_000, T)
+    sizes[rng.random(T) < 0.2] = 0
+    offsets = [0] + np.cumsum(sizes).tolist()
+    if offsets[-1] == 0:
+        offsets[-1] = 1
+        sizes[-1] = 1
+    N = offsets[-1]
+    g, r = _values(rng, N, ["gauss", "ties", "heavy"][seed % 3]), _values(rng, N, "gauss")
+    q = QUANT[kind]
+    cols = _divisor_columns(rng, sizes) if q == gd.GD_QUANT_COLUMN_MEAN else None
+    comp = gd.Compressor(offsets)
+    if cols is not None:
+        comp.set_columns(cols)
+    for per in (False, True):
+        full = oracle_sampled(g, r, offsets, 0.99, per, 20_000, seed)
+        K = full.idx.size
+        for ppm, cap in ((1000, None), (20_000, None), (20_000, K // 2), (20_000, 0)):
+            check(g, r, offsets, 0.99, per, ppm, seed, capacity=cap, comp=comp, quant=q, columns=cols,
+                  what=f"{kind} per={per} ppm={ppm} cap={cap}")
+
+
+@pytest.mark.parametrize("kind", list(QUANT))
+def test_quantised_full_size_nmt(kind):
+    """The 136,875,744-element NMT-shaped set, global threshold on a 0.1% sample, each 1-bit form."""
+    w = wl.workload("nmt_85k_global_signmean")
+    offsets = w.layout.offsets.astype(np.int64).tolist()
+    q = QUANT[kind]
+    cols = [int(c) for c in w.layout.columns] if q == gd.GD_QUANT_COLUMN_MEAN else None
+    comp = gd.Compressor(offsets)
+    if cols is not None:
+        comp.set_columns(cols)
+    g = w.grad(0)
+    r = (w.grad(1) * np.float32(0.5)).astype(np.float32)
+    check(g, r, offsets, 0.99, False, 1000, 3, capacity=4 * w.layout.numel // 100, comp=comp, quant=q, columns=cols,
+          what=f"nmt {kind}")
+
+
+def test_quantised_errors():
+    comp = gd.Compressor([0, 1000])
+    g = torch.zeros(1000, device="cuda")
+    r = torch.zeros(1000, device="cuda")
+    with pytest.raises(gd.GDError):
+        comp.compress_sampled(g, r, 0.99, quant=7)
+    out = comp.alloc_out(1.0, capacity=100)  # no sign_bits or means
+    with pytest.raises(gd.GDError):
+        comp.compress_sampled(g, r, 0.99, quant=gd.GD_QUANT_SIGN_MEAN, out=out, capacity=100)
