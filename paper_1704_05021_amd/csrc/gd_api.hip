@@ -323,7 +323,9 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
     if (hipMemset(ctx->scr.seg, 0, S_max * sizeof(gd::SegState)) != hipSuccess ||
         hipMemset(ctx->scr.shist, 0, (size_t)S_max * gd::kSHistWords * sizeof(uint32_t)) != hipSuccess ||
         hipMemset(ctx->scr.sshist, 0, (size_t)S_max * gd::kSsCopies * gd::kSsNB0 * sizeof(uint32_t)) != hipSuccess ||
-        hipDeviceSynchronize() != hipSuccess) {
+        hipMemset(ctx->scr.ten_cbase, 0, (T + 1) * sizeof(uint32_t)) != hipSuccess ||
+        hipMemset(ctx->scr.tile_base, 0, (T + 1) * sizeof(uint32_t)) != hipSuccess ||
+        hipMemset(ctx->scr.qbase, 0, (T + 1) * sizeof(uint32_t)) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
         free_all(ctx);
         delete ctx;
         return GD_ERR_HIP;
@@ -341,7 +343,7 @@ void gd_destroy(gd_ctx* ctx) {
 
 gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* residual, double drop_ratio,
                       gd_threshold mode, gd_quant quant, const gd_sparse* out, void* stream) {
-    if (!ctx || !grad || !residual || !out) return GD_ERR_ARG;
+    if (!ctx || !out || (ctx->N > 0 && (!grad || !residual))) return GD_ERR_ARG;  // an empty layout needs no data
     if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
     if (quant < GD_QUANT_NONE || quant > GD_QUANT_COLUMN_MEAN) return GD_ERR_ARG;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
@@ -382,7 +384,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
 
 gd_status gd_compress_pull(gd_ctx* ctx, const float* params, float* copy, double drop_ratio, gd_threshold mode,
                            const gd_sparse* out, void* stream) {
-    if (!ctx || !params || !copy || !out) return GD_ERR_ARG;
+    if (!ctx || !out || (ctx->N > 0 && (!params || !copy))) return GD_ERR_ARG;  // an empty layout needs no data
     if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
     if (!out->idx || !out->val || !out->tensor_counts) return GD_ERR_ARG;
@@ -439,7 +441,7 @@ uint64_t gd_quant_centres(const gd_ctx* ctx, gd_quant quant) {
 gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base, float* residual,
                               double drop_ratio, gd_threshold mode, uint32_t sample_ppm, uint64_t seed,
                               gd_quant quant, const gd_sparse* out, void* stream) {
-    if (!ctx || !grad || !residual || !out) return GD_ERR_ARG;
+    if (!ctx || !out || (ctx->N > 0 && (!grad || !residual))) return GD_ERR_ARG;  // an empty layout needs no data
     if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
     if (quant < GD_QUANT_NONE || quant > GD_QUANT_COLUMN_MEAN) return GD_ERR_ARG;
     if (quant != GD_QUANT_NONE && (!out->means || (out->capacity && !out->sign_bits))) return GD_ERR_ARG;

@@ -233,7 +233,12 @@ __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
 }
 
 hipError_t launch_layout(const CandArgs& a, hipStream_t st) {
-    if (a.num_units == 0) return hipSuccess;
+    if (a.num_units == 0) {
+        // an empty layout still needs its (zero) candidate and tile bases:
+        // the quantisation pass reads the tiles of every tensor
+        hipLaunchKernelGGL(k_scan_final, dim3(1), dim3(kScanThreads), 0, st, a, 0u);
+        return hipGetLastError();
+    }
     const uint32_t sb = (a.num_units + kScanUnits - 1) / kScanUnits;
     hipLaunchKernelGGL(k_scan, dim3(sb), dim3(kScanThreads), 0, st, a);
     hipLaunchKernelGGL(k_scan_final, dim3(1), dim3(kScanThreads), 0, st, a, sb);

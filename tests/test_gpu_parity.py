@@ -325,3 +325,17 @@ def test_many_tensors(T):
     comp = gd.Compressor(offsets)
     for per, quant, drop in ((True, False, 0.9), (False, False, 0.99), (True, True, 0.5)):
         check_case(g, r, offsets, drop, per, quant, comp=comp, what=f"T={T} per={per} quant={quant}")
+
+
+def test_empty_layout():
+    """Every tensor empty (N = 0): each compress form succeeds and sends nothing."""
+    comp = gd.Compressor([0, 0, 0])
+    e = torch.zeros(0, device="cuda")
+    for quant in (False, True):
+        out = comp.compress(e, e, 0.99, per_tensor=True, quant=quant)
+        torch.cuda.synchronize()
+        assert out.k == 0 and out.tensor_counts[:2].cpu().tolist() == [0, 0]
+    out = comp.compress_pull(e, e, 0.99)
+    s = comp.compress_sampled(e, e, 0.99, per_tensor=True, capacity=4, quant=gd.GD_QUANT_THRESHOLD)
+    torch.cuda.synchronize()
+    assert out.tensor_counts[:2].cpu().tolist() == [0, 0] and s.tensor_counts[:2].cpu().tolist() == [0, 0]
