@@ -1,6 +1,6 @@
 // C ABI of the gradient-dropping compressor: argument checks, layout tables,
 // scratch ownership and the launch sequence.  The operations are defined in
-// include/gd.h; the kernels are in gd_kernels.hip.
+// include/gd.h; the kernels' launchers are declared in gd_kernels.h.
 
 #include <algorithm>
 #include <cmath>
@@ -99,7 +99,8 @@ bool set_columns(gd_ctx* ctx, const std::vector<uint32_t>& columns) {
 
 // The passes after the threshold bracket is set: the dense stream, the
 // candidate layout, exact selection or plain compaction, and quantisation.
-// k_total is the host-known output size (exact threshold) or 0 (sampled).
+// k_total is the host-known output size (exact threshold), or under a sampled
+// threshold the capacity, a bound the device-side count stays within.
 gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, float* residual, bool per,
                             uint32_t ppm, bool sampled, gd_quant quant, uint64_t k_total, const gd_sparse* out,
                             hipStream_t st) {
@@ -302,9 +303,9 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
          dev_alloc(ctx, &ctx->scr.ne_off, C + 1) && dev_alloc(ctx, &ctx->scr.num_ne, 1) &&
          dev_alloc(ctx, &ctx->scr.raw_tbase, T + 1) && dev_alloc(ctx, &ctx->scr.cand_idx, N) &&
          dev_alloc(ctx, &ctx->scr.cand_val, N) && dev_alloc(ctx, &ctx->scr.ten_cbase, T + 1) &&
-         dev_alloc(ctx, &ctx->scr.tile_base, T + 1) && dev_alloc(ctx, &ctx->scr.tile_desc, (size_t)MT * gd::kTileDescWords) &&
-          dev_alloc(ctx, &ctx->scr.tile_gt, MT) &&
-         dev_alloc(ctx, &ctx->scr.tile_eq, MT) && dev_alloc(ctx, &ctx->scr.tile_q, 4 * (size_t)MT) &&
+         dev_alloc(ctx, &ctx->scr.tile_base, T + 1) &&
+         dev_alloc(ctx, &ctx->scr.tile_desc, (size_t)MT * gd::kTileDescWords) &&
+         dev_alloc(ctx, &ctx->scr.tile_gt, MT) && dev_alloc(ctx, &ctx->scr.tile_eq, MT) && dev_alloc(ctx, &ctx->scr.tile_q, 4 * (size_t)MT) &&
          dev_alloc(ctx, &ctx->scr.flags, 4) && dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) &&
          dev_alloc(ctx, &ctx->scr.seg, S_max) && dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
          dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&
@@ -480,8 +481,10 @@ gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base,
     sa.tensor_counts = out->tensor_counts;
     if (gd::launch_sampled(sa, base != nullptr, (uint32_t)max_samples, st) != hipSuccess) return GD_ERR_HIP;
 
-    // the number sent is only known on the device: quantisation covers up to the capacity
-    return run_after_bracket(ctx, grad, base, residual, per, ppm, true, quant, out->capacity, out, st);
+    // the number sent is only known on the device: quantisation covers up to
+    // the capacity, or N, since no more can be sent
+    return run_after_bracket(ctx, grad, base, residual, per, ppm, true, quant, std::min<uint64_t>(out->capacity, ctx->N),
+                             out, st);
 }
 
 gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const uint32_t* const* idx,
