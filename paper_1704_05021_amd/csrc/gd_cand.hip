@@ -17,7 +17,9 @@
 //              coarse bins) instead of block histograms.
 //   count    : the last digit, i.e. the exact threshold key T and the number
 //              of candidates equal to T to keep (lowest index first); per
-//              tile, the candidates above and equal to T.
+//              tile, the candidates above and equal to T.  (A sampled
+//              threshold sends every candidate, so emit derives these counts
+//              from positions and neither radix nor count runs.)
 //   emit     : kept (index, value) pairs in ascending index order, the
 //              residual of every candidate whose fate differs from what the
 //              dense pass assumed, kept counts per tensor (and per-tile sums
@@ -342,18 +344,6 @@ __device__ __forceinline__ void phase_count(const CandArgs& a) {
         tile_setup(a, tile, v);
         uint32_t key[kRows];
         load_keys(a, v, key);
-        if (a.sampled) {
-            // the sampled threshold keeps every candidate
-            uint32_t c = 0;
-#pragma unroll
-            for (int r = 0; r < kRows; ++r) c += v.p0 + r * kWave + lane < v.p1;
-            c = wave_sum(c);
-            if (lane == 0) {
-                a.tile_gt[tile] = c;
-                a.tile_eq[tile] = 0;
-            }
-            continue;
-        }
         if (v.s != cached_s) {
             // digit 2 in two steps: its coarse bin, then the bin among 32
             const uint32_t p18 = a.seg[v.s].p18, r2 = a.seg[v.s].r2;
@@ -416,24 +406,29 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         }
         // candidates above / equal to the threshold in earlier tiles of the segment
         uint32_t bg = 0, be = 0;
-        for (uint32_t b0 = v.first_tile; b0 < tile; b0 += 8 * kWave) {
-            uint32_t g8[8], e8[8];
+        if (a.sampled) {
+            // every candidate is sent: the earlier tiles hold p0 minus the segment's first candidate
+            bg = v.p0 - (a.per_tensor ? a.ten_cbase[v.t] : 0u);
+        } else {
+            for (uint32_t b0 = v.first_tile; b0 < tile; b0 += 8 * kWave) {
+                uint32_t g8[8], e8[8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const uint32_t q = b0 + j * kWave + lane;
-                const uint32_t qc = q < tile ? q : v.first_tile;  // unconditional loads, all in flight
-                const uint32_t x = a.tile_gt[qc], y = a.tile_eq[qc];
-                g8[j] = q < tile ? x : 0u;
-                e8[j] = q < tile ? y : 0u;
-            }
+                for (int j = 0; j < 8; ++j) {
+                    const uint32_t q = b0 + j * kWave + lane;
+                    const uint32_t qc = q < tile ? q : v.first_tile;  // unconditional loads, all in flight
+                    const uint32_t x = a.tile_gt[qc], y = a.tile_eq[qc];
+                    g8[j] = q < tile ? x : 0u;
+                    e8[j] = q < tile ? y : 0u;
+                }
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                bg += g8[j];
-                be += e8[j];
+                for (int j = 0; j < 8; ++j) {
+                    bg += g8[j];
+                    be += e8[j];
+                }
             }
+            bg = wave_sum(bg);
+            be = wave_sum(be);
         }
-        bg = wave_sum(bg);
-        be = wave_sum(be);
         const uint32_t bg0 = bg, be0 = be;
         const uint64_t ob = a.out_base[v.s];
         double sp = 0.0, sn = 0.0;
@@ -483,7 +478,8 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             // hundred tiles adding to one counter serialise badly.
             const uint32_t tend = v.tend;
             uint32_t cnt = 0, run_e = be0;
-            for (uint32_t b0 = tile; b0 < tend; b0 += 8 * kWave) {
+            if (a.sampled) cnt = a.ten_cbase[v.t + 1] - a.ten_cbase[v.t];  // every candidate is sent
+            for (uint32_t b0 = tile; b0 < tend && !a.sampled; b0 += 8 * kWave) {
                 uint32_t g8[8], e8[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
@@ -557,7 +553,7 @@ hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, u
         hipLaunchKernelGGL(k_radix<1>, gt, b, 0, st, a);
         hipLaunchKernelGGL(k_radix<2>, gt, b, 0, st, a);
     }
-    hipLaunchKernelGGL(k_count, gt, b, 0, st, a);
+    if (!a.sampled) hipLaunchKernelGGL(k_count, gt, b, 0, st, a);  // under a sampled threshold every candidate is sent
     if (quant) hipLaunchKernelGGL(k_emit<true>, gt, b, 0, st, a, o);
     else hipLaunchKernelGGL(k_emit<false>, gt, b, 0, st, a, o);
     return hipGetLastError();
