@@ -98,7 +98,6 @@ __device__ __forceinline__ void block_flush(const CandArgs& a, uint32_t* lh, con
                     sg[v] = kNoKey;
                 }
             }
-            if (a.sampled) continue;  // the threshold is already known
             uint32_t* g = seg_hist(a, sg[w], which) + 2 * i;
             if (sum & 0xFFFFu) atomicAdd(g, sum & 0xFFFFu);
             if (sum >> 16) atomicAdd(g + 1, sum >> 16);
@@ -132,7 +131,7 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
         const uint32_t tile = t0 + w;
         if (tile >= ntiles) {
             if (lane == 0) wseg[w] = kNoKey;
-            block_flush<kNB0>(a, lh, wseg, kHistH0);
+            if (!a.sampled) block_flush<kNB0>(a, lh, wseg, kHistH0);  // block-uniform
             continue;
         }
         TileView v;
@@ -218,10 +217,10 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
                 a.cand_idx[pl] = ix[r];
                 a.cand_val[pl] = vb[r];
             }
-            lds_hist_add16(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active);
+            lds_hist_add16(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active && !a.sampled);
         }
         if (lane == 0) wseg[w] = v.s;
-        block_flush<kNB0>(a, lh, wseg, kHistH0);
+        if (!a.sampled) block_flush<kNB0>(a, lh, wseg, kHistH0);  // a sampled threshold needs no histogram
     }
 }
 
