@@ -72,6 +72,10 @@
 //       nothing.  The count is data dependent; kept entries past the output
 //       capacity (in ascending index) are not sent and keep acc in the
 //       residual.
+//   R13 1-bit quantisation under the sampled threshold (Section 5.4 on what
+//       the Section 4 dropping sends): the centres of R5 and R10 over the
+//       entries actually sent, the threshold centre being the smallest sent
+//       magnitude of the segment; sent entries get acc - centre.
 //
 // Build: g++ -O2 -ffp-contract=off -fPIC -shared (no fast-math).
 
