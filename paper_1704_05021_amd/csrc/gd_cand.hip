@@ -44,6 +44,8 @@ namespace gd {
 // t and segment s, the segment's k, the compact candidates [p0, p1), the
 // segment's first tile, the tensor's tiles [tfirst, tend), the non-empty
 // unit ne0 holding the first candidate, and whether the bracket missed.
+// Lane positions in a tile are tested as offsets, (pos - p0) < (p1 - p0), so
+// that a tile near 2^32 candidate positions cannot wrap around.
 struct TileView {
     uint32_t t, s, k, p0, p1, first_tile, tfirst, tend, ne0;
     bool miss;
@@ -144,10 +146,10 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
             for (int r = 0; r < kRows; ++r) {
                 const uint32_t pl = v.p0 + r * kWave + lane;
                 ix[r] = e_base + pl;
-                const uint32_t e = e_base + (pl < v.p1 ? pl : v.p0);
+                const uint32_t e = e_base + (pl - v.p0 < v.p1 - v.p0 ? pl : v.p0);
                 // acc is the restored residual, or for a pull from the copy p - copy
                 const uint32_t x = __float_as_uint(a.res ? a.res[e] : a.pull_p[e] - a.pull_copy[e]);
-                vb[r] = pl < v.p1 ? x : 0u;
+                vb[r] = pl - v.p0 < v.p1 - v.p0 ? x : 0u;
             }
         } else {
             // compact position p <-> dense-pass offset p + shift
@@ -212,7 +214,7 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
             const uint32_t pl = v.p0 + r * kWave + lane;
-            const bool active = pl < v.p1;
+            const bool active = pl - v.p0 < v.p1 - v.p0;
             if (active) {
                 a.cand_idx[pl] = ix[r];
                 a.cand_val[pl] = vb[r];
@@ -229,8 +231,8 @@ __device__ __forceinline__ void load_keys(const CandArgs& a, const TileView& v, 
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
         const uint32_t pl = v.p0 + r * kWave + lane_id();
-        const uint32_t x = a.cand_val[pl < v.p1 ? pl : v.p0];  // unconditional: all rows in flight
-        key[r] = pl < v.p1 ? (x & 0x7FFFFFFFu) : 0u;
+        const uint32_t x = a.cand_val[pl - v.p0 < v.p1 - v.p0 ? pl : v.p0];  // unconditional: all rows in flight
+        key[r] = pl - v.p0 < v.p1 - v.p0 ? (x & 0x7FFFFFFFu) : 0u;
     }
 }
 
@@ -309,7 +311,7 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
             if (kBlockHist) {
 #pragma unroll
                 for (int r = 0; r < kRows; ++r) {
-                    const bool active = v.p0 + r * kWave + lane < v.p1;
+                    const bool active = (uint32_t)(r * kWave + lane) < v.p1 - v.p0;
                     lds_hist_add16(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
                                    active && (key[r] >> Lv::kPrefixShift) == prefix);
                 }
@@ -319,7 +321,7 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
                 uint32_t* hc = seg_hist(a, v.s, kHistH2c);
 #pragma unroll
                 for (int r = 0; r < kRows; ++r) {
-                    const bool active = v.p0 + r * kWave + lane < v.p1;
+                    const bool active = (uint32_t)(r * kWave + lane) < v.p1 - v.p0;
                     if (active && (key[r] >> Lv::kPrefixShift) == prefix) {
                         const uint32_t d = key[r] & (Lv::kNB - 1);
                         atomicAdd(hf + d, 1u);
@@ -360,7 +362,7 @@ __device__ __forceinline__ void phase_count(const CandArgs& a) {
         uint32_t gt = 0, eq = 0;
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
-            const bool active = v.p0 + r * kWave + lane < v.p1;
+            const bool active = (uint32_t)(r * kWave + lane) < v.p1 - v.p0;
             gt += active && key[r] > thr;
             eq += active && key[r] == thr;
         }
@@ -384,10 +386,10 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
             const uint32_t pl = v.p0 + r * kWave + lane;
-            const uint32_t pc = pl < v.p1 ? pl : v.p0;
+            const uint32_t pc = pl - v.p0 < v.p1 - v.p0 ? pl : v.p0;
             const uint32_t x = a.cand_idx[pc], y = a.cand_val[pc];
-            ix[r] = pl < v.p1 ? x : 0u;
-            vb[r] = pl < v.p1 ? y : 0u;
+            ix[r] = pl - v.p0 < v.p1 - v.p0 ? x : 0u;
+            vb[r] = pl - v.p0 < v.p1 - v.p0 ? y : 0u;
         }
         const uint32_t hi = v.miss ? kNoKey : a.seg[v.s].hi;
         const uint32_t thr = a.seg[v.s].thr, need = a.seg[v.s].need;
@@ -399,7 +401,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
             const uint32_t key = vb[r] & 0x7FFFFFFFu;
-            const bool valid = v.p0 + r * kWave + lane < v.p1;
+            const bool valid = (uint32_t)(r * kWave + lane) < v.p1 - v.p0;
             old[r] = 0.0f;
             if (pull && valid && key >= thr) old[r] = a.pull_copy[ix[r]];
         }
@@ -435,7 +437,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         uint32_t kmin = kNoKey;  // sampled threshold, threshold centre: smallest key sent by this lane
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
-            const bool valid = v.p0 + r * kWave + lane < v.p1;
+            const bool valid = (uint32_t)(r * kWave + lane) < v.p1 - v.p0;
             const uint32_t key = vb[r] & 0x7FFFFFFFu;
             const bool isgt = valid && (a.sampled || key > thr);
             const bool iseq = valid && !a.sampled && key == thr;

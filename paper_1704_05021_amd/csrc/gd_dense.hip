@@ -63,11 +63,13 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
     const uint32_t u = blockIdx.x;
     const int tid = threadIdx.x, w = tid >> 6, lane = lane_id();
     const uint32_t ustart = u * kUnitLen;
-    const uint32_t uend = ustart + kUnitLen < a.N ? ustart + kUnitLen : a.N;
+    // ends and vector tests without 32-bit wrap-around (N may come within a unit of 2^32)
+    const uint32_t uend = a.N - ustart > kUnitLen ? ustart + kUnitLen : a.N;
     const uint32_t e0 = ustart + 4 * tid;
 
     f4 g = {0.f, 0.f, 0.f, 0.f}, b = g, r = g;
-    if (e0 + 4 <= uend) {
+    const bool whole = e0 < uend && uend - e0 >= 4;  // all four elements of this lane exist
+    if (whole) {
         g = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.grad) + (e0 >> 2));
         if (BASE) b = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.base) + (e0 >> 2));
         if (!NORES) r = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.res) + (e0 >> 2));
@@ -115,7 +117,7 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
         ov[q] = (valid && key >= hi[q]) ? 0.0f : acc[q];
     }
     if (!NORES) {
-        if (e0 + 4 <= uend) {
+        if (whole) {
             __builtin_nontemporal_store(ov, reinterpret_cast<f4*>(a.res) + (e0 >> 2));
         } else {
 #pragma unroll

@@ -136,7 +136,7 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
         if (t < a.T) {
             const uint32_t s = a.per_tensor ? t : 0u;
             cc = a.seg[s].miss ? a.tensor_off[t + 1] - a.tensor_off[t] : a.raw_tbase[t + 1] - a.raw_tbase[t];
-            tiles = (cc + kTile - 1) / kTile;
+            tiles = (uint32_t)(((uint64_t)cc + kTile - 1) / kTile);
         }
         uint32_t ctot, ttot;
         const uint32_t ce = block_excl_scan<kScanThreads>(cc, lds, &ctot);
@@ -168,7 +168,8 @@ __device__ __forceinline__ void mark_tiles(const CandArgs& a, uint32_t t, uint32
     const uint32_t miss = a.seg[s].miss != 0 ? 0x80000000u : 0u;
     const uint32_t k = keep_of(a.seg_off[s + 1] - a.seg_off[s], a.keep_ppm);
     const uint32_t c0 = a.ten_cbase[t], c1 = a.ten_cbase[t + 1];
-    for (uint32_t j = p > base ? (p - base + kTile - 1) / kTile : 0u; base + j * kTile < q; ++j) {
+    // (64-bit positions: a tile start past 2^32 must end the loop, not wrap)
+    for (uint32_t j = p > base ? (p - base + kTile - 1) / kTile : 0u; (uint64_t)base + (uint64_t)j * kTile < q; ++j) {
         const uint32_t p0 = c0 + j * kTile, p1 = p0 + kTile < c1 ? p0 + kTile : c1;
         uint4* d = reinterpret_cast<uint4*>(a.tile_desc + (size_t)(t0 + j) * kTileDescWords);
         d[0] = make_uint4(t | miss, ne, p0, p1);
@@ -190,7 +191,7 @@ __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
             a.ne_off[ne] = raw;
         }
         info = a.unit_info[u];
-        const uint32_t ustart = u * kUnitLen, uend = ustart + kUnitLen < a.N ? ustart + kUnitLen : a.N;
+        const uint32_t ustart = u * kUnitLen, uend = a.N - ustart > kUnitLen ? ustart + kUnitLen : a.N;
         // every tensor overlapping the unit (one, unless it holds a boundary)
         for (uint32_t t = info & 0x7FFFFFFFu; t < a.T && a.tensor_off[t] < uend; ++t) {
             const uint32_t ta = a.tensor_off[t], tb = a.tensor_off[t + 1];

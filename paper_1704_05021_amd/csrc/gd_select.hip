@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
         const uint32_t s0 = ((seg_a >> 4) + lo_j) * kUnit;
         if (U == n16) {
             // every block sampled: its 16 neighbours
-            if (s0 >= seg_a && s0 + kUnit <= seg_b) {
+            if (s0 >= seg_a && s0 < seg_b && seg_b - s0 >= (uint32_t)kUnit) {
                 const f4* g4 = reinterpret_cast<const f4*>(a.grad + s0);
                 const f4* r4 = reinterpret_cast<const f4*>(nores ? a.grad + s0 : a.res + s0);
                 const f4* b4 = reinterpret_cast<const f4*>(BASE ? a.base + s0 : a.grad + s0);
@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
             for (int q = 0; q < 4; ++q) {
                 const uint32_t h = mix32((j * 4u + q) * 0x9E3779B9u ^ (s + 1u) * 0x85EBCA6Bu);
                 const uint32_t e = s0 + q * sub + (h % (sub / 4)) * 4;
-                if (e >= seg_a && e + 4 <= seg_b) {
+                if (e >= seg_a && e < seg_b && seg_b - e >= 4u) {
                     const f4 g = *reinterpret_cast<const f4*>(a.grad + e);
                     const f4 r = nores ? f4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<const f4*>(a.res + e);
                     const f4 b = BASE ? *reinterpret_cast<const f4*>(a.base + e) : g;
