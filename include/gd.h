@@ -36,7 +36,7 @@ extern "C" {
 typedef enum {
     GD_OK = 0,
     GD_ERR_ARG = 1,      /* null pointer, drop ratio outside [0,1], bad enum */
-    GD_ERR_LAYOUT = 2,   /* offsets not starting at 0, decreasing, or N >= 2^32 */
+    GD_ERR_LAYOUT = 2,   /* offsets not starting at 0, decreasing, or N > 2^32 - 2 */
     GD_ERR_CAPACITY = 3, /* output capacity below the number of kept entries */
     GD_ERR_ALIGN = 4,    /* grad, base or residual not 16-byte aligned */
     GD_ERR_OOM = 5,      /* device scratch allocation failed (gd_create only) */
@@ -76,7 +76,7 @@ typedef struct gd_ctx gd_ctx;
  *   tensor_offsets (host, T+1 entries): tensor t occupies flat indices
  *     [tensor_offsets[t], tensor_offsets[t+1]); tensor_offsets[0] must be 0,
  *     the sequence non-decreasing (empty tensors are allowed) and
- *     N = tensor_offsets[T] below 2^32 (indices are sent as uint32).
+ *     N = tensor_offsets[T] at most 2^32 - 2 (indices are sent as uint32).
  *   Allocates all device scratch on the current HIP device (about 16 bytes
  *   per element plus about 109 KB per tensor for the per-tensor histograms);
  *   gd_compress never allocates.  Any number of tensors is accepted.
