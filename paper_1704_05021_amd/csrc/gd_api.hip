@@ -160,6 +160,8 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     ca.flags = ctx->scr.flags;
     ca.tile_gt = ctx->scr.tile_gt;
     ca.tile_eq = ctx->scr.tile_eq;
+    ca.grp_gt = ctx->scr.grp_gt;
+    ca.grp_eq = ctx->scr.grp_eq;
     ca.tile_q = ctx->scr.tile_q;
     ca.out_base = ctx->scr.out_base;
     ca.sampled = sampled ? 1u : 0u;
@@ -305,7 +307,9 @@ gd_status gd_create(gd_ctx** out, const uint64_t* off, uint32_t T) {
          dev_alloc(ctx, &ctx->scr.cand_val, N) && dev_alloc(ctx, &ctx->scr.ten_cbase, T + 1) &&
          dev_alloc(ctx, &ctx->scr.tile_base, T + 1) &&
          dev_alloc(ctx, &ctx->scr.tile_desc, (size_t)MT * gd::kTileDescWords) &&
-         dev_alloc(ctx, &ctx->scr.tile_gt, MT) && dev_alloc(ctx, &ctx->scr.tile_eq, MT) && dev_alloc(ctx, &ctx->scr.tile_q, 4 * (size_t)MT) &&
+         dev_alloc(ctx, &ctx->scr.tile_gt, MT) && dev_alloc(ctx, &ctx->scr.tile_eq, MT) &&
+         dev_alloc(ctx, &ctx->scr.grp_gt, MT / gd::kGroupTiles + 1) && dev_alloc(ctx, &ctx->scr.grp_eq, MT / gd::kGroupTiles + 1) &&
+         dev_alloc(ctx, &ctx->scr.tile_q, 4 * (size_t)MT) &&
          dev_alloc(ctx, &ctx->scr.flags, 4) && dev_alloc(ctx, &ctx->scr.hist, (size_t)S_max * gd::kHistWords) &&
          dev_alloc(ctx, &ctx->scr.seg, S_max) && dev_alloc(ctx, &ctx->scr.out_base, S_max) &&
          dev_alloc(ctx, &ctx->scr.skeys, std::max(ctx->skeys_tensor, ctx->skeys_global)) &&

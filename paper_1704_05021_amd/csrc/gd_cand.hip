@@ -14,7 +14,8 @@
 //              share the prefix found so far (L = 1, 2; digits of 10, 8 and
 //              13 key bits).  Few candidates share the first 18 bits, so
 //              digit 2 is counted with direct global atomics (fine and
-//              coarse bins) instead of block histograms.
+//              coarse bins) instead of block histograms, a repeated bin
+//              once per run.
 //   count    : the last digit, i.e. the exact threshold key T and the number
 //              of candidates equal to T to keep (lowest index first); per
 //              tile, the candidates above and equal to T.  (A sampled
@@ -68,6 +69,12 @@ __device__ __forceinline__ void tile_setup(const CandArgs& a, uint32_t tile, Til
 
 __device__ __forceinline__ uint32_t* seg_hist(const CandArgs& a, uint32_t s, int which) {
     return a.hist + (size_t)s * kHistWords + which;
+}
+
+// Whether the tile's segment keeps group sums of its tile counts (its tiles
+// are the tensor's under a per-tensor threshold, else all of them).
+__device__ __forceinline__ bool seg_grouped(const CandArgs& a, const TileView& v, uint32_t ntiles) {
+    return (a.per_tensor ? v.tend - v.tfirst : ntiles) > kBigSegTiles;
 }
 
 // Adds the block's four per-wave histograms (16-bit counters, two bins per
@@ -219,7 +226,7 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
                 a.cand_idx[pl] = ix[r];
                 a.cand_val[pl] = vb[r];
             }
-            lds_hist_add16(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active && !a.sampled);
+            lds_hist_add16_wave(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active && !a.sampled);
         }
         if (lane == 0) wseg[w] = v.s;
         if (!a.sampled) block_flush<kNB0>(a, lh, wseg, kHistH0);  // a sampled threshold needs no histogram
@@ -278,6 +285,19 @@ constexpr int radix_lds() {
     return L == 1 ? kWavesPerBlock * (Level<L>::kNB / 2) + kWavesPerBlock : 1;
 }
 
+// Digit 2 is counted with global atomics, since few candidates share the
+// first 18 bits of the threshold.  Many equal keys (exact zeros, values of a
+// narrower float type) would put thousands of atomics on one bin, so each
+// wave keeps a run: the first bin it meets and how many of its candidates
+// fell in it, added once when the wave moves to another segment or ends.
+// Candidates in other bins are added one by one.
+__device__ __forceinline__ void run_flush(const CandArgs& a, uint32_t s, uint32_t d, uint32_t c) {
+    if (c != 0 && lane_id() == 0) {
+        atomicAdd(seg_hist(a, s, kHistH2) + d, c);
+        atomicAdd(seg_hist(a, s, kHistH2c) + (d >> kD2cShift), c);
+    }
+}
+
 template <int L>
 __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
     using Lv = Level<L>;
@@ -292,6 +312,7 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
     }
     const uint32_t ntiles = a.tile_base[a.T];
     uint32_t cached_s = kNoKey, prefix = 0, rank = 0;
+    uint32_t run_s = kNoKey, run_d = 0, run_c = 0;  // digit 2: this wave's run of one bin
     for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += gridDim.x * kWavesPerBlock) {
         const uint32_t tile = t0 + w;
         if (tile < ntiles) {
@@ -312,18 +333,28 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
 #pragma unroll
                 for (int r = 0; r < kRows; ++r) {
                     const bool active = (uint32_t)(r * kWave + lane) < v.p1 - v.p0;
-                    lds_hist_add16(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
+                    lds_hist_add16_wave(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
                                    active && (key[r] >> Lv::kPrefixShift) == prefix);
                 }
                 if (lane == 0) wseg[w] = v.s;
             } else {
+                if (v.s != run_s) {
+                    run_flush(a, run_s, run_d, run_c);
+                    run_s = v.s;
+                    run_c = 0;
+                }
                 uint32_t* hf = seg_hist(a, v.s, kHistH2);
                 uint32_t* hc = seg_hist(a, v.s, kHistH2c);
 #pragma unroll
                 for (int r = 0; r < kRows; ++r) {
-                    const bool active = (uint32_t)(r * kWave + lane) < v.p1 - v.p0;
-                    if (active && (key[r] >> Lv::kPrefixShift) == prefix) {
-                        const uint32_t d = key[r] & (Lv::kNB - 1);
+                    const bool in = (uint32_t)(r * kWave + lane) < v.p1 - v.p0 && (key[r] >> Lv::kPrefixShift) == prefix;
+                    const uint64_t m = ballot(in);
+                    if (m == 0) continue;
+                    const uint32_t d = key[r] & (Lv::kNB - 1);
+                    if (run_c == 0) run_d = lane_value(d, __ffsll((unsigned long long)m) - 1);
+                    const bool same = in && d == run_d;
+                    run_c += popc64(ballot(same));
+                    if (in && !same) {
                         atomicAdd(hf + d, 1u);
                         atomicAdd(hc + (d >> kD2cShift), 1u);
                     }
@@ -334,6 +365,7 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
         }
         if (kBlockHist) block_flush<Lv::kNB>(a, lh, wseg, Lv::kHist);
     }
+    if (!kBlockHist) run_flush(a, run_s, run_d, run_c);
 }
 
 __device__ __forceinline__ void phase_count(const CandArgs& a) {
@@ -371,7 +403,48 @@ __device__ __forceinline__ void phase_count(const CandArgs& a) {
         if (lane == 0) {
             a.tile_gt[tile] = gt;
             a.tile_eq[tile] = eq;
+            if (seg_grouped(a, v, ntiles)) {
+                if (gt) atomicAdd(&a.grp_gt[tile / kGroupTiles], gt);
+                if (eq) atomicAdd(&a.grp_eq[tile / kGroupTiles], eq);
+            }
         }
+    }
+}
+
+// This lane's part of the sums of x and y over [lo, hi) (wave_sum gives the
+// totals).
+__device__ __forceinline__ void sum_span(const uint32_t* x, const uint32_t* y, uint32_t lo, uint32_t hi, uint32_t& g,
+                                         uint32_t& e) {
+    for (uint32_t b0 = lo; b0 < hi; b0 += 8 * kWave) {
+        uint32_t g8[8], e8[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t q = b0 + j * kWave + lane_id();
+            const uint32_t qc = q < hi ? q : lo;  // unconditional loads, all in flight
+            const uint32_t xv = x[qc], yv = y[qc];
+            g8[j] = q < hi ? xv : 0u;
+            e8[j] = q < hi ? yv : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            g += g8[j];
+            e += e8[j];
+        }
+    }
+}
+
+// Candidates above and equal to the threshold in tiles [lo, hi) of one
+// segment (this lane's part): whole groups of a grouped segment come from
+// the group sums, the tiles at either end one by one.
+__device__ __forceinline__ void sum_tiles(const CandArgs& a, bool grouped, uint32_t lo, uint32_t hi, uint32_t& g,
+                                          uint32_t& e) {
+    const uint32_t glo = (lo + kGroupTiles - 1) / kGroupTiles, ghi = hi / kGroupTiles;
+    if (grouped && glo < ghi) {
+        sum_span(a.tile_gt, a.tile_eq, lo, glo * kGroupTiles, g, e);
+        sum_span(a.grp_gt, a.grp_eq, glo, ghi, g, e);
+        sum_span(a.tile_gt, a.tile_eq, ghi * kGroupTiles, hi, g, e);
+    } else {
+        sum_span(a.tile_gt, a.tile_eq, lo, hi, g, e);
     }
 }
 
@@ -411,22 +484,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             // every candidate is sent: the earlier tiles hold p0 minus the segment's first candidate
             bg = v.p0 - (a.per_tensor ? a.ten_cbase[v.t] : 0u);
         } else {
-            for (uint32_t b0 = v.first_tile; b0 < tile; b0 += 8 * kWave) {
-                uint32_t g8[8], e8[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const uint32_t q = b0 + j * kWave + lane;
-                    const uint32_t qc = q < tile ? q : v.first_tile;  // unconditional loads, all in flight
-                    const uint32_t x = a.tile_gt[qc], y = a.tile_eq[qc];
-                    g8[j] = q < tile ? x : 0u;
-                    e8[j] = q < tile ? y : 0u;
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    bg += g8[j];
-                    be += e8[j];
-                }
-            }
+            sum_tiles(a, seg_grouped(a, v, ntiles), v.first_tile, tile, bg, be);
             bg = wave_sum(bg);
             be = wave_sum(be);
         }
@@ -473,31 +531,21 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             be += popc64(me);
         }
         if (tile == v.tfirst) {
-            // The first tile of a tensor writes the tensor's kept count: per
-            // tile, every candidate above T plus the ties still needed (in
-            // ascending tile order within the segment).  No atomics: a few
-            // hundred tiles adding to one counter serialise badly.
-            const uint32_t tend = v.tend;
-            uint32_t cnt = 0, run_e = be0;
-            if (a.sampled) cnt = a.ten_cbase[v.t + 1] - a.ten_cbase[v.t];  // every candidate is sent
-            for (uint32_t b0 = tile; b0 < tend && !a.sampled; b0 += 8 * kWave) {
-                uint32_t g8[8], e8[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const uint32_t q = b0 + j * kWave + lane;
-                    const uint32_t qc = q < tend ? q : tile;
-                    const uint32_t x = a.tile_gt[qc], y = a.tile_eq[qc];
-                    g8[j] = q < tend ? x : 0u;
-                    e8[j] = q < tend ? y : 0u;
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const uint32_t ie = wave_incl_scan(e8[j]);
-                    const uint32_t before = run_e + ie - e8[j];
-                    const uint32_t ties = need > before ? (need - before < e8[j] ? need - before : e8[j]) : 0u;
-                    cnt += wave_sum(g8[j] + ties);
-                    run_e += lane_value(ie, kWave - 1);
-                }
+            // The first tile of a tensor writes the tensor's kept count: every
+            // candidate of the tensor above T, plus as many of its candidates
+            // equal to T as the segment still needs at this tile (ties go to
+            // the lowest index, and a tensor's tiles are consecutive).  No
+            // atomics: a few hundred tiles adding to one counter serialise badly.
+            uint32_t cnt;
+            if (a.sampled) {
+                cnt = a.ten_cbase[v.t + 1] - a.ten_cbase[v.t];  // every candidate is sent
+            } else {
+                uint32_t gt_t = 0, eq_t = 0;
+                sum_tiles(a, seg_grouped(a, v, ntiles), tile, v.tend, gt_t, eq_t);
+                gt_t = wave_sum(gt_t);
+                eq_t = wave_sum(eq_t);
+                const uint32_t left = need > be0 ? need - be0 : 0u;
+                cnt = gt_t + (eq_t < left ? eq_t : left);
             }
             // entries past the capacity are not sent
             const uint64_t start = ob + bg0 + (be0 < need ? be0 : need);

@@ -216,6 +216,22 @@ __device__ __forceinline__ void lds_hist_add16(uint32_t* h, uint32_t bin, bool a
     if (active) atomicAdd(&h[bin >> 1], 1u << ((bin & 1u) << 4));
 }
 
+// lds_hist_add16 for a whole wave (every lane calls it): when all active
+// lanes hold one bin (many equal keys, such as exact zeros or values of a
+// narrower float type), one lane adds their count, instead of 64 atomics on
+// one LDS word that the LDS would serialise.
+__device__ __forceinline__ void lds_hist_add16_wave(uint32_t* h, uint32_t bin, bool active) {
+    const uint64_t m = ballot(active);
+    if (m == 0) return;
+    const int first = __ffsll((unsigned long long)m) - 1;
+    const uint32_t b0 = lane_value(bin, first);
+    if (ballot(active && bin == b0) == m) {
+        if (lane_id() == first) atomicAdd(&h[b0 >> 1], popc64(m) << ((b0 & 1u) << 4));
+    } else if (active) {
+        atomicAdd(&h[bin >> 1], 1u << ((bin & 1u) << 4));
+    }
+}
+
 // Exclusive prefix over a block of NT threads; *total receives the block sum.
 // lds must hold NT / 64 + 1 words.  Every thread of the block must call it.
 template <int NT>

@@ -44,6 +44,8 @@ struct Scratch {
     uint32_t* tile_desc = nullptr;   // [max_tiles * kTileDescWords]
     uint32_t* tile_gt = nullptr;     // [max_tiles]
     uint32_t* tile_eq = nullptr;     // [max_tiles]
+    uint32_t* grp_gt = nullptr;      // [max_tiles / kGroupTiles + 1]
+    uint32_t* grp_eq = nullptr;
     double* tile_q = nullptr;        // [max_tiles * 4] kept positive sum, negative sum, counts
     uint32_t* flags = nullptr;       // [4] device flags (0: some bracket missed)
     uint32_t* hist = nullptr;        // [S_max * kHistWords]

@@ -69,6 +69,12 @@ struct DenseArgs {
 constexpr uint32_t kTile = 1024;        // candidates per tile of the candidate passes
 constexpr uint32_t kTileDescWords = 8;  // words of a tile descriptor (two 16-byte loads)
 constexpr uint32_t kTileBlocks = 512;   // most blocks a candidate pass launches (4 waves each)
+// A segment of more than kBigSegTiles tiles also keeps per-group sums of its
+// tiles' counts (groups of kGroupTiles consecutive tiles), so that a tile's
+// prefix over the earlier tiles of its segment costs about
+// tiles / kGroupTiles + kGroupTiles loads instead of one per earlier tile.
+constexpr uint32_t kGroupTiles = 256;
+constexpr uint32_t kBigSegTiles = 4096;
 
 struct CandArgs {
     float* res;
@@ -102,6 +108,8 @@ struct CandArgs {
     uint32_t* tile_desc;  // [max tiles * kTileDescWords] per tile, written by the layout pass: see TileView
     uint32_t* tile_gt;    // [max tiles]
     uint32_t* tile_eq;
+    uint32_t* grp_gt;     // [max tiles / kGroupTiles + 1] sums of tile_gt per group (segments of many tiles)
+    uint32_t* grp_eq;     //   and of tile_eq; cleared by the layout pass
     double* tile_q;       // [max tiles * 4]
     uint64_t* out_base;   // [S] first output slot of each segment (the sampled mode writes it here)
     uint32_t* flags;      // [0]: some segment missed its bracket

@@ -148,6 +148,11 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
         ccarry += ctot;
         tcarry += ttot;
     }
+    // the group sums of the candidate passes start from zero
+    for (uint32_t i = tid; i < tcarry / kGroupTiles + 1; i += kScanThreads) {
+        a.grp_gt[i] = 0;
+        a.grp_eq[i] = 0;
+    }
     if (tid == 0) {
         a.ten_cbase[a.T] = ccarry;
         a.tile_base[a.T] = tcarry;
@@ -201,7 +206,8 @@ __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
                 // direct tiles start at element offsets ta + j * kTile
                 const uint32_t lo_e = ta > ustart ? ta : ustart, hi_e = tb < uend ? tb : uend;
                 mark_tiles(a, t, ta, lo_e, hi_e, ne);
-                restore = restore || (cnt > 0 && a.res != nullptr);  // a pull from the copy zeroed nothing
+                // nothing to restore after a pull from the copy, or where no key reached hi
+                restore = restore || (cnt > 0 && a.res != nullptr && a.seg[s].hi != kNoKey);
             } else {
                 const uint32_t rb = a.raw_tbase[t], re = a.raw_tbase[t + 1];
                 const uint32_t p = raw > rb ? raw : rb, q = raw + cnt < re ? raw + cnt : re;
