@@ -278,7 +278,8 @@ gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode);
  * Test hook: waits for the device, then copies the per-segment state of the
  * last gd_compress call (16 uint32 words per threshold segment: candidate
  * bracket lo and hi, candidate count, bracket-miss flag, radix digits and
- * ranks, threshold key, ties kept) for up to max_segments segments into
+ * ranks, threshold key, ties kept, zero-mode flag: fewer nonzero keys than
+ * k, so the threshold is key 0) for up to max_segments segments into
  * seg_words (host), and the decomposition into info (host, 4 entries:
  * elements per dense-pass unit, units, candidates per tile, most tiles).
  * Synchronises the host.

@@ -20,7 +20,11 @@
 //              of candidates equal to T to keep (lowest index first); per
 //              tile, the candidates above and equal to T.  (A sampled
 //              threshold sends every candidate, so emit derives these counts
-//              from positions and neither radix nor count runs.)
+//              from positions and neither radix nor count runs.)  For a
+//              segment with fewer nonzero keys than k (the zero mode: T is
+//              key 0, every candidate is nonzero and sent), it also sends the
+//              zeros kept, the segment's lowest-index ones, and writes the
+//              segment's tensor counts; radix skips such segments.
 //   emit     : kept (index, value) pairs in ascending index order, the
 //              residual of every candidate whose fate differs from what the
 //              dense pass assumed, kept counts per tensor (and per-tile sums
@@ -321,14 +325,18 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
             uint32_t key[kRows];
             load_keys(a, v, key);
             if (v.s != cached_s) {
-                uint32_t p0, r0, d, ab;
-                read_level<L>(a.seg[v.s], v.k, p0, r0);
-                wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
-                prefix = (p0 << Lv::kPrevBits) | d;
-                rank = r0 - ab;
+                if (a.seg[v.s].zero) {
+                    prefix = kNoKey;  // the zero mode knows its threshold: no key matches, nothing counted
+                } else {
+                    uint32_t p0, r0, d, ab;
+                    read_level<L>(a.seg[v.s], v.k, p0, r0);
+                    wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
+                    prefix = (p0 << Lv::kPrevBits) | d;
+                    rank = r0 - ab;
+                }
                 cached_s = v.s;
             }
-            if (tile == v.first_tile && lane == 0) write_level<L>(a.seg[v.s], prefix, rank);
+            if (tile == v.first_tile && lane == 0 && prefix != kNoKey) write_level<L>(a.seg[v.s], prefix, rank);
             if (kBlockHist) {
 #pragma unroll
                 for (int r = 0; r < kRows; ++r) {
@@ -368,7 +376,90 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
     if (!kBlockHist) run_flush(a, run_s, run_d, run_c);
 }
 
-__device__ __forceinline__ void phase_count(const CandArgs& a) {
+// Zero mode, elements [xs, xe) of one segment (segment start seg_a, zb of its
+// zeros before xs, output slots from ob): the zeros whose rank among the
+// segment's zeros is below need are kept.  Every element before such a zero
+// is kept too, so it goes to slot ob + (e - seg_a); its residual becomes +0.
+// The residual holds acc here (nothing was zeroed early).  Whole wave.
+__device__ __forceinline__ void fill_zeros(const CandArgs& a, const EmitArgs& o, uint32_t xs, uint32_t xe,
+                                           uint32_t seg_a, uint32_t zb, uint32_t need, uint64_t ob) {
+    for (uint32_t d0 = 0; d0 < xe - xs && zb < need; d0 += kWave) {
+        const uint32_t d = d0 + lane_id();
+        const bool valid = d < xe - xs;
+        const uint32_t e = xs + (valid ? d : 0u);
+        const float x = a.res[e];
+        const bool z = valid && (__float_as_uint(x) & 0x7FFFFFFFu) == 0u;
+        const uint64_t m = ballot(z);
+        if (z && zb + lanes_below(m) < need) {
+            const uint64_t pos = ob + (e - seg_a);
+            o.idx[pos] = e;
+            o.val[pos] = x;  // +0 or -0, as acc is
+            a.res[e] = 0.0f;
+        }
+        zb += popc64(m);
+    }
+}
+
+// Zero-mode segments of unit u, or with fill = false only whether one of
+// them keeps zeros in the unit (any lane may call it so); with fill = true
+// the whole wave fills them.
+__device__ __forceinline__ bool zero_unit(const CandArgs& a, const EmitArgs& o, uint32_t u, bool fill) {
+    const uint32_t ustart = u * kUnitLen, uend = a.N - ustart > kUnitLen ? ustart + kUnitLen : a.N;
+    const uint32_t raw = a.loc[u] + a.boff[u / kScanUnits];  // candidates before ustart
+    if (!a.per_tensor) {
+        const SegState& g = a.seg[0];
+        if (!g.zero) return false;
+        const uint32_t need = keep_of(a.N, a.keep_ppm) - g.clo, zb = ustart - raw;
+        if (fill && zb < need) fill_zeros(a, o, ustart, uend, 0u, zb, need, a.out_base[0]);
+        return zb < need;
+    }
+    bool any = false;
+    for (uint32_t t = a.unit_info[u] & 0x7FFFFFFFu; t < a.T && a.tensor_off[t] < uend; ++t) {
+        const uint32_t ta = a.tensor_off[t], tb = a.tensor_off[t + 1];
+        if (tb <= ustart || tb == ta || !a.seg[t].zero) continue;
+        const uint32_t need = keep_of(tb - ta, a.keep_ppm) - a.seg[t].clo;
+        const uint32_t zb = ta >= ustart ? 0u : (ustart - ta) - (raw - a.raw_tbase[t]);
+        if (zb < need) {
+            any = true;
+            if (fill) fill_zeros(a, o, ta > ustart ? ta : ustart, tb < uend ? tb : uend, ta, zb, need, a.out_base[t]);
+        }
+    }
+    return any;
+}
+
+// The zero mode's part of the count pass, after the candidate tiles: the kept
+// counts of its tensors, all its candidates plus the zeros kept before each
+// tensor's end less those kept before its start (per tensor: k), then the
+// kept zeros.  It runs before emit, which sets the residual of sent
+// candidates to +0, since it tells zeros from candidates by the residual.
+// Unit u goes to wave u mod W, so the units at the start of a segment, which
+// hold its kept zeros, spread over many waves.
+__device__ __forceinline__ void zero_fill(const CandArgs& a, const EmitArgs& o) {
+    const uint32_t W = gridDim.x * kWavesPerBlock, wid = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int lane = lane_id();
+    for (uint64_t t = (uint64_t)wid * kWave + lane; t < a.T; t += (uint64_t)W * kWave) {
+        const uint32_t s = a.per_tensor ? (uint32_t)t : 0u;
+        if (!a.seg[s].zero) continue;
+        const uint32_t seg_a = a.seg_off[s], seg_b = a.seg_off[s + 1];
+        const uint32_t need = keep_of(seg_b - seg_a, a.keep_ppm) - a.seg[s].clo;
+        const uint32_t raw_seg = a.per_tensor ? a.raw_tbase[t] : 0u;
+        const uint32_t zs = (a.tensor_off[t] - seg_a) - (a.raw_tbase[t] - raw_seg);
+        const uint32_t ze = (a.tensor_off[t + 1] - seg_a) - (a.raw_tbase[t + 1] - raw_seg);
+        o.tensor_counts[t] = (a.raw_tbase[t + 1] - a.raw_tbase[t]) + (ze < need ? ze : need) - (zs < need ? zs : need);
+    }
+    for (uint64_t u0 = wid; u0 < a.num_units; u0 += (uint64_t)W * kWave) {
+        const uint64_t u = u0 + (uint64_t)W * lane;
+        const bool fill = u < a.num_units && zero_unit(a, o, (uint32_t)u, false);
+        uint64_t todo = ballot(fill);
+        while (todo) {
+            const int src = __ffsll((unsigned long long)todo) - 1;
+            todo &= todo - 1;
+            zero_unit(a, o, lane_value((uint32_t)u, src), true);
+        }
+    }
+}
+
+__device__ __forceinline__ void phase_count(const CandArgs& a, const EmitArgs& o) {
     const int w = threadIdx.x >> 6, lane = lane_id();
     const uint32_t ntiles = a.tile_base[a.T];
     uint32_t cached_s = kNoKey, thr = kNoKey, need = 0;
@@ -378,13 +469,20 @@ __device__ __forceinline__ void phase_count(const CandArgs& a) {
         uint32_t key[kRows];
         load_keys(a, v, key);
         if (v.s != cached_s) {
-            // digit 2 in two steps: its coarse bin, then the bin among 32
-            const uint32_t p18 = a.seg[v.s].p18, r2 = a.seg[v.s].r2;
-            uint32_t dc, abc, df, abf;
-            wave_pick<kNB2c>(seg_hist(a, v.s, kHistH2c), r2, dc, abc);
-            wave_pick<kNB2 / kNB2c>(seg_hist(a, v.s, kHistH2) + (dc << kD2cShift), r2 - abc, df, abf);
-            thr = (p18 << kD1Shift) | (dc << kD2cShift) | df;
-            need = r2 - abc - abf;
+            if (a.seg[v.s].zero) {
+                // zero mode: T = key 0; every candidate (nonzero) is above it
+                // and the first k - cnt zeros, none of them a candidate, are kept
+                thr = 0;
+                need = v.k - a.seg[v.s].clo;
+            } else {
+                // digit 2 in two steps: its coarse bin, then the bin among 32
+                const uint32_t p18 = a.seg[v.s].p18, r2 = a.seg[v.s].r2;
+                uint32_t dc, abc, df, abf;
+                wave_pick<kNB2c>(seg_hist(a, v.s, kHistH2c), r2, dc, abc);
+                wave_pick<kNB2 / kNB2c>(seg_hist(a, v.s, kHistH2) + (dc << kD2cShift), r2 - abc, df, abf);
+                thr = (p18 << kD1Shift) | (dc << kD2cShift) | df;
+                need = r2 - abc - abf;
+            }
             cached_s = v.s;
         }
         if (tile == v.first_tile && lane == 0) {
@@ -409,6 +507,7 @@ __device__ __forceinline__ void phase_count(const CandArgs& a) {
             }
         }
     }
+    if (a.flags[1]) zero_fill(a, o);  // some segment takes the zero mode
 }
 
 // This lane's part of the sums of x and y over [lo, hi) (wave_sum gives the
@@ -466,6 +565,9 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
         }
         const uint32_t hi = v.miss ? kNoKey : a.seg[v.s].hi;
         const uint32_t thr = a.seg[v.s].thr, need = a.seg[v.s].need;
+        // zero mode: the zeros kept before a candidate (at most need) shift it
+        const bool zseg = a.seg[v.s].zero != 0;
+        const uint32_t seg_a = a.per_tensor ? a.tensor_off[v.t] : 0u;
         // A pull from the copy reads the copy word of every entry that may be
         // kept, to add the sent value to it; the loads are issued here, early
         // enough to overlap the prefix work.
@@ -501,7 +603,8 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             const bool iseq = valid && !a.sampled && key == thr;
             const uint64_t mg = ballot(isgt), me = ballot(iseq);
             const uint32_t G = bg + lanes_below(mg), E = be + lanes_below(me);
-            const uint64_t pos = ob + G + (E < need ? E : need);
+            const uint32_t zb = ix[r] - seg_a - G;  // zero mode: zeros of the segment before ix
+            const uint64_t pos = ob + G + (zseg ? (zb < need ? zb : need) : (E < need ? E : need));
             // past the capacity (only possible under a sampled threshold) an
             // entry is not sent and keeps acc in the residual
             const bool kept = (isgt || (iseq && E < need)) && pos < o.capacity;
@@ -530,7 +633,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
             bg += popc64(mg);
             be += popc64(me);
         }
-        if (tile == v.tfirst) {
+        if (tile == v.tfirst && !zseg) {  // (zero-mode counts: zero_fill)
             // The first tile of a tensor writes the tensor's kept count: every
             // candidate of the tensor above T, plus as many of its candidates
             // equal to T as the segment still needs at this tile (ties go to
@@ -583,7 +686,7 @@ __global__ __launch_bounds__(kBlock) void k_radix(CandArgs a) {
     phase_radix<L>(a, lds);
 }
 
-__global__ __launch_bounds__(kBlock) void k_count(CandArgs a) { phase_count(a); }
+__global__ __launch_bounds__(kBlock) void k_count(CandArgs a, EmitArgs o) { phase_count(a, o); }
 
 template <bool QUANT>
 __global__ __launch_bounds__(kBlock) void k_emit(CandArgs a, EmitArgs o) {
@@ -602,7 +705,7 @@ hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, u
         hipLaunchKernelGGL(k_radix<1>, gt, b, 0, st, a);
         hipLaunchKernelGGL(k_radix<2>, gt, b, 0, st, a);
     }
-    if (!a.sampled) hipLaunchKernelGGL(k_count, gt, b, 0, st, a);  // under a sampled threshold every candidate is sent
+    if (!a.sampled) hipLaunchKernelGGL(k_count, gt, b, 0, st, a, o);  // under a sampled threshold every candidate is sent
     if (quant) hipLaunchKernelGGL(k_emit<true>, gt, b, 0, st, a, o);
     else hipLaunchKernelGGL(k_emit<false>, gt, b, 0, st, a, o);
     return hipGetLastError();

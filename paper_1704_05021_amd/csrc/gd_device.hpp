@@ -91,7 +91,8 @@ struct SegState {
     uint32_t r2;    // rank among candidates with that prefix
     uint32_t thr;   // the threshold key T (kNoKey when nothing is kept)
     uint32_t need;  // entries with key == T to keep, lowest index first
-    uint32_t pad[6];
+    uint32_t zero;  // 1 when fewer than k keys are nonzero and all of them are candidates: T = 0
+    uint32_t pad[5];
 };
 
 __device__ __forceinline__ uint32_t key_of(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }

@@ -4,7 +4,9 @@
 //              counts.
 //   k_scan_final : one block scans the block totals and derives, per
 //              threshold segment, the candidate total and
-//              whether the bracket missed (fewer than k candidates; under a
+//              whether the bracket missed (fewer than k candidates, unless
+//              the candidates are every nonzero key and nothing was zeroed
+//              early: then the segment takes the zero mode; under a
 //              sampled threshold, where every candidate is sent, the first
 //              output slot instead), and per
 //              tensor the first candidate in dense-pass order, the first
@@ -75,9 +77,12 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(CandArgs a) {
 __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_t nblocks) {
     __shared__ uint32_t lds[kScanThreads / kWave + 1];
     __shared__ uint32_t boff[kMaxScanBlocks];
-    __shared__ uint32_t any_miss;
+    __shared__ uint32_t any_miss, any_zero;
     const int tid = threadIdx.x;
-    if (tid == 0) any_miss = 0;
+    if (tid == 0) {
+        any_miss = 0;
+        any_zero = 0;
+    }
     uint32_t carry = 0, necarry = 0;
     for (uint32_t b0 = 0; b0 < nblocks; b0 += kScanThreads) {
         const uint32_t b = b0 + tid;
@@ -109,10 +114,18 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
         const uint32_t n = a.seg_off[s + 1] - a.seg_off[s];
         const uint32_t k = keep_of(n, a.keep_ppm);
         const uint32_t cnt = a.per_tensor ? a.raw_tbase[s + 1] - a.raw_tbase[s] : grand;
-        const uint32_t miss = (!a.sampled && k > 0 && cnt < k) ? 1u : 0u;
+        const uint32_t short_of_k = (!a.sampled && k > 0 && cnt < k) ? 1u : 0u;
+        // Fewer than k nonzero keys, every one of them a candidate (lo = 1)
+        // and none zeroed early (hi: no key): the threshold is key 0, and the
+        // segment keeps every candidate plus its first k - cnt zeros by index
+        // (the zero mode), so it needs no fallback.
+        const uint32_t zero = (short_of_k && a.zfill && a.seg[s].lo == 1u && a.seg[s].hi == kNoKey) ? 1u : 0u;
+        const uint32_t miss = short_of_k && !zero;
         a.seg[s].clo = cnt;
         a.seg[s].miss = miss;
+        a.seg[s].zero = zero;
         if (miss) atomicOr(&any_miss, 1u);
+        if (zero) atomicOr(&any_zero, 1u);
     }
     __threadfence_block();
     __syncthreads();
@@ -157,6 +170,7 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
         a.ten_cbase[a.T] = ccarry;
         a.tile_base[a.T] = tcarry;
         a.flags[0] = any_miss;
+        a.flags[1] = any_zero;
     }
 }
 

@@ -315,7 +315,7 @@ class Compressor:
         if st != 0:
             raise GDError(st, "gd_debug_force_bracket")
 
-    SEG_FIELDS = ("lo", "hi", "clo", "miss", "d0", "r1", "p18", "r2", "thr", "need")
+    SEG_FIELDS = ("lo", "hi", "clo", "miss", "d0", "r1", "p18", "r2", "thr", "need", "zero")
 
     def debug_state(self):
         """(per-segment state of the last call as a list of dicts, decomposition info dict)."""
@@ -326,7 +326,7 @@ class Compressor:
         st = _lib().gd_debug_state(self._h, words.ctypes.data, self.T, info.ctypes.data)
         if st != 0:
             raise GDError(st, "gd_debug_state")
-        segs = [dict(zip(self.SEG_FIELDS, (int(x) for x in row[:10]))) for row in words]
+        segs = [dict(zip(self.SEG_FIELDS, (int(x) for x in row[:len(self.SEG_FIELDS)]))) for row in words]
         keys = ("unit_len", "units", "tile", "max_tiles")
         return segs, dict(zip(keys, (int(x) for x in info)))
 
