@@ -230,7 +230,9 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
                 a.cand_idx[pl] = ix[r];
                 a.cand_val[pl] = vb[r];
             }
-            lds_hist_add16_wave(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active && !a.sampled);
+            // a missed tensor's rows can be all one key (zeros): one add per row there
+            if (v.miss) lds_hist_add16_wave(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active);
+            else lds_hist_add16(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active && !a.sampled);
         }
         if (lane == 0) wseg[w] = v.s;
         if (!a.sampled) block_flush<kNB0>(a, lh, wseg, kHistH0);  // a sampled threshold needs no histogram
@@ -325,24 +327,30 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
             uint32_t key[kRows];
             load_keys(a, v, key);
             if (v.s != cached_s) {
-                if (a.seg[v.s].zero) {
-                    prefix = kNoKey;  // the zero mode knows its threshold: no key matches, nothing counted
-                } else {
-                    uint32_t p0, r0, d, ab;
-                    read_level<L>(a.seg[v.s], v.k, p0, r0);
-                    wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
-                    prefix = (p0 << Lv::kPrevBits) | d;
-                    rank = r0 - ab;
-                }
+                // (the zero flag is loaded beside the rest, not branched on
+                // first: a dependent load would cost a round trip per segment)
+                const uint32_t zero = a.seg[v.s].zero;
+                uint32_t p0, r0, d, ab;
+                read_level<L>(a.seg[v.s], v.k, p0, r0);
+                wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
+                // the zero mode knows its threshold: no key matches, nothing counted
+                prefix = zero ? kNoKey : (p0 << Lv::kPrevBits) | d;
+                rank = r0 - ab;
                 cached_s = v.s;
             }
             if (tile == v.first_tile && lane == 0 && prefix != kNoKey) write_level<L>(a.seg[v.s], prefix, rank);
             if (kBlockHist) {
+                if (v.miss) {  // a missed tensor's rows can be all one key (zeros): one add per row
 #pragma unroll
-                for (int r = 0; r < kRows; ++r) {
-                    const bool active = (uint32_t)(r * kWave + lane) < v.p1 - v.p0;
-                    lds_hist_add16_wave(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
-                                   active && (key[r] >> Lv::kPrefixShift) == prefix);
+                    for (int r = 0; r < kRows; ++r)
+                        lds_hist_add16_wave(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
+                                            (uint32_t)(r * kWave + lane) < v.p1 - v.p0 &&
+                                                (key[r] >> Lv::kPrefixShift) == prefix);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < kRows; ++r)
+                        lds_hist_add16(hw, (key[r] >> Lv::kDigitShift) & (Lv::kNB - 1),
+                                       (uint32_t)(r * kWave + lane) < v.p1 - v.p0 && (key[r] >> Lv::kPrefixShift) == prefix);
                 }
                 if (lane == 0) wseg[w] = v.s;
             } else {
@@ -469,20 +477,16 @@ __device__ __forceinline__ void phase_count(const CandArgs& a, const EmitArgs& o
         uint32_t key[kRows];
         load_keys(a, v, key);
         if (v.s != cached_s) {
-            if (a.seg[v.s].zero) {
-                // zero mode: T = key 0; every candidate (nonzero) is above it
-                // and the first k - cnt zeros, none of them a candidate, are kept
-                thr = 0;
-                need = v.k - a.seg[v.s].clo;
-            } else {
-                // digit 2 in two steps: its coarse bin, then the bin among 32
-                const uint32_t p18 = a.seg[v.s].p18, r2 = a.seg[v.s].r2;
-                uint32_t dc, abc, df, abf;
-                wave_pick<kNB2c>(seg_hist(a, v.s, kHistH2c), r2, dc, abc);
-                wave_pick<kNB2 / kNB2c>(seg_hist(a, v.s, kHistH2) + (dc << kD2cShift), r2 - abc, df, abf);
-                thr = (p18 << kD1Shift) | (dc << kD2cShift) | df;
-                need = r2 - abc - abf;
-            }
+            // digit 2 in two steps: its coarse bin, then the bin among 32
+            const uint32_t zero = a.seg[v.s].zero, clo = a.seg[v.s].clo;
+            const uint32_t p18 = a.seg[v.s].p18, r2 = a.seg[v.s].r2;
+            uint32_t dc, abc, df, abf;
+            wave_pick<kNB2c>(seg_hist(a, v.s, kHistH2c), r2, dc, abc);
+            wave_pick<kNB2 / kNB2c>(seg_hist(a, v.s, kHistH2) + (dc << kD2cShift), r2 - abc, df, abf);
+            // zero mode: T = key 0; every candidate (nonzero) is above it and
+            // the first k - cnt zeros, none of them a candidate, are kept
+            thr = zero ? 0u : (p18 << kD1Shift) | (dc << kD2cShift) | df;
+            need = zero ? v.k - clo : r2 - abc - abf;
             cached_s = v.s;
         }
         if (tile == v.first_tile && lane == 0) {
