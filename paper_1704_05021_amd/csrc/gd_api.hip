@@ -165,7 +165,7 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     ca.tile_q = ctx->scr.tile_q;
     ca.out_base = ctx->scr.out_base;
     ca.sampled = sampled ? 1u : 0u;
-    ca.zfill = (!sampled && quant == GD_QUANT_NONE && residual != nullptr) ? 1u : 0u;
+    ca.zfill = (!sampled && quant != GD_QUANT_COLUMN_MEAN && residual != nullptr) ? 1u : 0u;
     if (!residual) {  // a pull from the last pulled copy (base)
         ca.pull_p = grad;
         ca.pull_copy = const_cast<float*>(base);
@@ -189,6 +189,7 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
         qa.means = out->means;
         qa.tensor_counts = out->tensor_counts;
         qa.tile_base = ctx->scr.tile_base;
+        qa.ten_cbase = ctx->scr.ten_cbase;
         qa.tile_q = ctx->scr.tile_q;
         qa.qbase = ctx->scr.qbase;
         qa.T = ctx->T;

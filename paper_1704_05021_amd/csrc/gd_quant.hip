@@ -24,6 +24,12 @@ namespace gd {
 constexpr uint32_t kColSlice = 4096;  // sent entries per column-sum block
 constexpr int kColLds = 2048;         // most columns a block sums in LDS (48 KB)
 
+// Zeros tensor u keeps in the zero mode (every candidate kept, plus zeros):
+// its kept count less its candidates; 0 outside the zero mode.
+__device__ __forceinline__ uint32_t zeros_kept(const QuantArgs& q, uint32_t u) {
+    return q.seg[q.per_tensor ? u : 0u].zero ? q.tensor_counts[u] - (q.ten_cbase[u + 1] - q.ten_cbase[u]) : 0u;
+}
+
 // Centres per tensor (every kind but the column mean) and the first output
 // slot of each tensor.  One wave per tensor.
 __global__ __launch_bounds__(kBlock) void k_means(QuantArgs q) {
@@ -53,7 +59,7 @@ __global__ __launch_bounds__(kBlock) void k_means(QuantArgs q) {
             }
             key = wave_min(key);
         } else if (keep_of(q.seg_off[s + 1] - q.seg_off[s], q.keep_ppm) > 0) {
-            key = q.seg[s].thr;
+            key = q.seg[s].zero ? 0u : q.seg[s].thr;  // zero mode: T = 0 (the count pass may see no tile)
         }
         if (key != kNoKey) {
             pos = __uint_as_float(key);
@@ -73,6 +79,15 @@ __global__ __launch_bounds__(kBlock) void k_means(QuantArgs q) {
         sn = wave_sum(sn);
         np = wave_sum(np);
         nn = wave_sum(nn);
+        // zero mode: the kept zeros are in no tile's sums; each counts as a
+        // positive value (not below zero) and adds nothing to sp
+        uint32_t zk = 0;
+        if (global) {
+            for (uint32_t u = lane; u < q.T; u += kWave) zk += zeros_kept(q, u);
+        } else if (lane == 0) {
+            zk = zeros_kept(q, t);
+        }
+        np += (double)wave_sum(zk);
         pos = np > 0.0 ? (float)(sp / np) : 0.0f;
         neg = nn > 0.0 ? (float)(sn / nn) : 0.0f;
     }

@@ -2,9 +2,9 @@
 
 Such a segment keeps every nonzero entry and then its lowest-index zeros
 (Algorithm 1, Section 4: the k largest |acc|, ties to the lower index; here
-the threshold is 0).  Unquantised calls with a residual take the zero mode
-(no fallback to every element); quantised ones and pulls from the copy take
-the fallback.  Results must match the oracle bit for bit: indices, values
+the threshold is 0).  Calls with a residual take the zero mode (no fallback
+to every element), except under column centres; those and pulls from the
+copy take the fallback.  Results must match the oracle bit for bit: indices, values
 (-0 kept as -0), residuals (+0 where sent) and per-tensor counts.
 """
 import numpy as np
@@ -84,11 +84,27 @@ def test_zero_mode_over_steps():
     assert modes[0] == [1, 0, 1, 0, 1]
 
 
-@pytest.mark.parametrize("quant", [gd.GD_QUANT_SIGN_MEAN, gd.GD_QUANT_GLOBAL_MEAN])
-def test_short_of_nonzeros_quantised_takes_the_fallback(quant):
+@pytest.mark.parametrize("per_tensor", [True, False], ids=["per_tensor", "global"])
+@pytest.mark.parametrize("quant", [gd.GD_QUANT_SIGN_MEAN, gd.GD_QUANT_THRESHOLD, gd.GD_QUANT_GLOBAL_MEAN],
+                         ids=["sign_mean", "threshold", "global_mean"])
+def test_zero_mode_quantised(quant, per_tensor):
+    # kept zeros are positive values (not below zero): they count in the
+    # positive centre's average, and under threshold centres T = 0
     g, r = _sparse_inputs(24)
     comp = gd.Compressor(OFF)
-    check_case(g, r, OFF, 0.99, False, quant, comp=comp, what=f"short of nonzeros, quant={quant}")
+    check_case(g, r, OFF, 0.99, per_tensor, quant, comp=comp,
+               what=f"zero mode, quant={quant}, per_tensor={per_tensor}")
+    segs = _segments(comp, per_tensor)
+    assert segs[0]["zero"] == 1 and not any(s["miss"] for s in segs)
+
+
+def test_short_of_nonzeros_column_centres_take_the_fallback():
+    g, r = _sparse_inputs(26)
+    cols = [1, 1, 1, 4, 1]  # one column per tensor; the 100-element tensor as 25 x 4
+    comp = gd.Compressor(OFF)
+    comp.set_columns(cols)
+    check_case(g, r, OFF, 0.99, False, gd.GD_QUANT_COLUMN_MEAN, comp=comp, columns=cols,
+               what="short of nonzeros, column centres")
     seg = _segments(comp, False)[0]
     assert seg["zero"] == 0 and seg["miss"] == 1
 
