@@ -387,22 +387,25 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
 // Zero mode, elements [xs, xe) of one segment (segment start seg_a, zb of its
 // zeros before xs, output slots from ob): the zeros whose rank among the
 // segment's zeros is below need are kept.  Every element before such a zero
-// is kept too, so it goes to slot ob + (e - seg_a); its residual becomes +0.
-// The residual holds acc here (nothing was zeroed early).  Whole wave.
+// is kept too, so it goes to slot ob + (e - seg_a); its residual becomes +0,
+// or for a pull from the copy the copy takes the sent value.  acc is the
+// residual here (nothing was zeroed early), or p - copy.  Whole wave.
 __device__ __forceinline__ void fill_zeros(const CandArgs& a, const EmitArgs& o, uint32_t xs, uint32_t xe,
                                            uint32_t seg_a, uint32_t zb, uint32_t need, uint64_t ob) {
     for (uint32_t d0 = 0; d0 < xe - xs && zb < need; d0 += kWave) {
         const uint32_t d = d0 + lane_id();
         const bool valid = d < xe - xs;
         const uint32_t e = xs + (valid ? d : 0u);
-        const float x = a.res[e];
+        const float c = a.res ? 0.0f : a.pull_copy[e];
+        const float x = a.res ? a.res[e] : a.pull_p[e] - c;
         const bool z = valid && (__float_as_uint(x) & 0x7FFFFFFFu) == 0u;
         const uint64_t m = ballot(z);
         if (z && zb + lanes_below(m) < need) {
             const uint64_t pos = ob + (e - seg_a);
             o.idx[pos] = e;
             o.val[pos] = x;  // +0 or -0, as acc is
-            a.res[e] = 0.0f;
+            if (a.res) a.res[e] = 0.0f;
+            else a.pull_copy[e] = c + x;  // as the client adds what it receives (-0 + +0 is +0)
         }
         zb += popc64(m);
     }

@@ -116,10 +116,12 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
         const uint32_t cnt = a.per_tensor ? a.raw_tbase[s + 1] - a.raw_tbase[s] : grand;
         const uint32_t short_of_k = (!a.sampled && k > 0 && cnt < k) ? 1u : 0u;
         // Fewer than k nonzero keys, every one of them a candidate (lo = 1)
-        // and none zeroed early (hi: no key): the threshold is key 0, and the
-        // segment keeps every candidate plus its first k - cnt zeros by index
-        // (the zero mode), so it needs no fallback.
-        const uint32_t zero = (short_of_k && a.zfill && a.seg[s].lo == 1u && a.seg[s].hi == kNoKey) ? 1u : 0u;
+        // and none zeroed early (hi: no key, or a pull from the copy, whose
+        // dense pass writes nothing): the threshold is key 0, and the segment
+        // keeps every candidate plus its first k - cnt zeros by index (the
+        // zero mode), so it needs no fallback.
+        const uint32_t zero =
+            (short_of_k && a.zfill && a.seg[s].lo == 1u && (a.seg[s].hi == kNoKey || a.res == nullptr)) ? 1u : 0u;
         const uint32_t miss = short_of_k && !zero;
         a.seg[s].clo = cnt;
         a.seg[s].miss = miss;

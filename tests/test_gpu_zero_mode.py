@@ -2,9 +2,8 @@
 
 Such a segment keeps every nonzero entry and then its lowest-index zeros
 (Algorithm 1, Section 4: the k largest |acc|, ties to the lower index; here
-the threshold is 0).  Calls with a residual take the zero mode (no fallback
-to every element), except under column centres; those and pulls from the
-copy take the fallback.  Results must match the oracle bit for bit: indices, values
+the threshold is 0).  Such segments take the zero mode (no fallback to every
+element), except under column centres, which take the fallback.  Results must match the oracle bit for bit: indices, values
 (-0 kept as -0), residuals (+0 where sent) and per-tensor counts.
 """
 import numpy as np
@@ -109,22 +108,28 @@ def test_short_of_nonzeros_column_centres_take_the_fallback():
     assert seg["zero"] == 0 and seg["miss"] == 1
 
 
-def test_short_of_nonzeros_pull_from_copy():
-    # no residual to hold acc: the fallback, with the copy taking the sent values
+@pytest.mark.parametrize("per_tensor", [True, False], ids=["per_tensor", "global"])
+def test_zero_mode_pull_from_copy(per_tensor):
+    # no residual: acc = p - copy, and a kept zero updates the copy to
+    # copy + acc, which turns a -0 copy under a +0 difference into +0
     g, _ = _sparse_inputs(25)
+    rng = np.random.default_rng(27)
     copy = np.zeros_like(g)
+    copy[rng.random(g.size) < 0.3] = np.float32(-0.0)
+    same = rng.random(g.size) < 0.1
+    copy[same] = g[same]  # p - copy = +0 there
     comp = gd.Compressor(OFF)
     p_t = torch.from_numpy(g).to(comp.device)
     c_t = torch.from_numpy(copy).to(comp.device)
-    out = comp.compress_pull(p_t, c_t, 0.99, per_tensor=True)
+    out = comp.compress_pull(p_t, c_t, 0.99, per_tensor=per_tensor)
     torch.cuda.synchronize()
-    o, o_copy = oracle.compress_pull(g, copy, OFF, 0.99, per_tensor=True)
+    o, o_copy = oracle.compress_pull(g, copy, OFF, 0.99, per_tensor=per_tensor)
     k = out.k
     assert np.array_equal(out.idx[:k].cpu().numpy().view(np.uint32), o.idx)
     assert np.array_equal(out.val[:k].cpu().numpy().view(np.uint32), o.val.view(np.uint32))
     assert np.array_equal(c_t.cpu().numpy().view(np.uint32), o_copy.view(np.uint32))
     assert np.array_equal(out.tensor_counts[:comp.T].cpu().numpy().view(np.uint32), o.tensor_counts)
-    assert _segments(comp, True)[0]["zero"] == 0
+    assert _segments(comp, per_tensor)[0]["zero"] == 1
 
 
 @pytest.mark.parametrize("per_tensor", [True, False], ids=["per_tensor", "global"])
