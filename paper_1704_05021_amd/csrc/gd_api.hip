@@ -165,7 +165,7 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     ca.tile_q = ctx->scr.tile_q;
     ca.out_base = ctx->scr.out_base;
     ca.sampled = sampled ? 1u : 0u;
-    ca.zfill = (!sampled && quant != GD_QUANT_COLUMN_MEAN) ? 1u : 0u;
+    ca.zfill = sampled ? 0u : 1u;
     if (!residual) {  // a pull from the last pulled copy (base)
         ca.pull_p = grad;
         ca.pull_copy = const_cast<float*>(base);

@@ -114,7 +114,7 @@ struct CandArgs {
     uint64_t* out_base;   // [S] first output slot of each segment (the sampled mode writes it here)
     uint32_t* flags;      // [0]: some segment missed its bracket; [1]: some segment takes the zero mode
     uint32_t sampled;     // sampled threshold: every candidate is kept, no bracket can miss
-    uint32_t zfill;       // 1: a segment short of nonzero keys may take the zero mode (not under column centres)
+    uint32_t zfill;       // 1: a segment short of nonzero keys may take the zero mode (any exact threshold)
     const float* pull_p;  // pull from the last pulled copy (res is then null): the parameters
     float* pull_copy;     //   and the copy, which takes the sent values
 };

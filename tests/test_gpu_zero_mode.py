@@ -2,8 +2,8 @@
 
 Such a segment keeps every nonzero entry and then its lowest-index zeros
 (Algorithm 1, Section 4: the k largest |acc|, ties to the lower index; here
-the threshold is 0).  Such segments take the zero mode (no fallback to every
-element), except under column centres, which take the fallback.  Results must match the oracle bit for bit: indices, values
+the threshold is 0).  Under an exact threshold such segments take the zero
+mode (no fallback to every element), with or without 1-bit forms.  Results must match the oracle bit for bit: indices, values
 (-0 kept as -0), residuals (+0 where sent) and per-tensor counts.
 """
 import numpy as np
@@ -97,15 +97,17 @@ def test_zero_mode_quantised(quant, per_tensor):
     assert segs[0]["zero"] == 1 and not any(s["miss"] for s in segs)
 
 
-def test_short_of_nonzeros_column_centres_take_the_fallback():
+@pytest.mark.parametrize("per_tensor", [True, False], ids=["per_tensor", "global"])
+def test_zero_mode_column_centres(per_tensor):
+    # the column sums are taken over the sent list, kept zeros included
     g, r = _sparse_inputs(26)
-    cols = [1, 1, 1, 4, 1]  # one column per tensor; the 100-element tensor as 25 x 4
+    cols = [13, 1, 3, 4, 1]  # 300001 = 23077 x 13, 399999 = 133333 x 3, 100 = 25 x 4
     comp = gd.Compressor(OFF)
     comp.set_columns(cols)
-    check_case(g, r, OFF, 0.99, False, gd.GD_QUANT_COLUMN_MEAN, comp=comp, columns=cols,
-               what="short of nonzeros, column centres")
-    seg = _segments(comp, False)[0]
-    assert seg["zero"] == 0 and seg["miss"] == 1
+    check_case(g, r, OFF, 0.99, per_tensor, gd.GD_QUANT_COLUMN_MEAN, comp=comp, columns=cols,
+               what=f"zero mode, column centres, per_tensor={per_tensor}")
+    seg = _segments(comp, per_tensor)[0]
+    assert seg["zero"] == 1 and seg["miss"] == 0
 
 
 @pytest.mark.parametrize("per_tensor", [True, False], ids=["per_tensor", "global"])
