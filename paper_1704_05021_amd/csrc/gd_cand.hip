@@ -255,12 +255,12 @@ template <int L>
 struct Level;
 template <>
 struct Level<1> {
-    static constexpr int kPrevNB = kNB0, kPrevHist = kHistH0, kNB = kNB1, kHist = kHistH1;
+    static constexpr int kPrevNB = kNB0, kPrevHist = kHistH0, kPrevCopies = 1, kNB = kNB1, kHist = kHistH1;
     static constexpr int kPrefixShift = kD0Shift, kDigitShift = kD1Shift, kPrevBits = 0;
 };
 template <>
 struct Level<2> {
-    static constexpr int kPrevNB = kNB1, kPrevHist = kHistH1, kNB = kNB2, kHist = kHistH2;
+    static constexpr int kPrevNB = kNB1, kPrevHist = kHistH1, kPrevCopies = kH1Copies, kNB = kNB2, kHist = kHistH2;
     static constexpr int kPrefixShift = kD1Shift, kDigitShift = 0, kPrevBits = kD0Shift - kD1Shift;
 };
 
@@ -332,7 +332,7 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
                 const uint32_t zero = a.seg[v.s].zero;
                 uint32_t p0, r0, d, ab;
                 read_level<L>(a.seg[v.s], v.k, p0, r0);
-                wave_pick<Lv::kPrevNB>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
+                wave_pick<Lv::kPrevNB, Lv::kPrevCopies>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
                 // the zero mode knows its threshold: no key matches, nothing counted
                 prefix = zero ? kNoKey : (p0 << Lv::kPrevBits) | d;
                 rank = r0 - ab;
@@ -379,7 +379,7 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
         } else if (kBlockHist && lane == 0) {
             wseg[w] = kNoKey;
         }
-        if (kBlockHist) block_flush<Lv::kNB>(a, lh, wseg, Lv::kHist);
+        if (kBlockHist) block_flush<Lv::kNB>(a, lh, wseg, Lv::kHist + (int)(blockIdx.x % kH1Copies) * Lv::kNB);
     }
     if (!kBlockHist) run_flush(a, run_s, run_d, run_c);
 }

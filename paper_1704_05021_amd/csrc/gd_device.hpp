@@ -29,8 +29,12 @@ constexpr int kNB2 = 8192;                 // key bits 12..0
 // Histogram words per threshold segment: one histogram per digit, and digit
 // 2 also in 256 coarse bins of 32 (its top 8 bits) for a two-step pick.
 constexpr int kNB2c = 256, kD2cShift = 5;
-constexpr int kHistH0 = 0, kHistH1 = kNB0, kHistH2 = kNB0 + kNB1, kHistH2c = kNB0 + kNB1 + kNB2;
-constexpr int kHistWords = kNB0 + kNB1 + kNB2 + kNB2c;
+// Digit 1 is counted into kH1Copies copies of its histogram, picked by block
+// number, so that the many blocks of one large segment spread their adds
+// over several addresses per bin; the pick of digit 1 sums the copies.
+constexpr int kH1Copies = 8;
+constexpr int kHistH0 = 0, kHistH1 = kNB0, kHistH2 = kNB0 + kH1Copies * kNB1, kHistH2c = kHistH2 + kNB2;
+constexpr int kHistWords = kNB0 + kH1Copies * kNB1 + kNB2 + kNB2c;
 
 // Sampling: units of 16 consecutive elements (one 64-byte line per array),
 // at most kMaxUnits units per segment.  A sample key is the top 16 bits of
@@ -163,7 +167,7 @@ __device__ __forceinline__ double wave_sum(double v) {
 // holding the r-th largest element (r >= 1) and the number of elements in
 // higher digits.  Returns false when the histogram holds fewer than r
 // elements.  Called by a whole wave; hist may be global or LDS memory.
-template <int NB>
+template <int NB, int C = 1>
 __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uint32_t& above) {
     constexpr int B = NB >= kWave ? NB / kWave : 1;
     const int lane = lane_id();
@@ -172,7 +176,11 @@ __device__ bool wave_pick(const uint32_t* hist, uint32_t r, uint32_t& digit, uin
     uint32_t sum = 0;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-        c[i] = top - 1 - i >= 0 ? hist[top - 1 - i] : 0u;
+        uint32_t x = 0;
+        if (top - 1 - i >= 0)
+#pragma unroll
+            for (int j = 0; j < C; ++j) x += hist[j * NB + top - 1 - i];  // C copies, NB words apart
+        c[i] = x;
         sum += c[i];
     }
     const uint32_t incl = wave_incl_scan(sum);
