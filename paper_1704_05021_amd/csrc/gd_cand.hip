@@ -139,12 +139,14 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
     uint32_t* wseg = lh + kWavesPerBlock * (kNB0 / 2 + kWin + 1 + kWin + kTile);
     for (int i = lane; i < kNB0 / 2; i += kWave) hw[i] = 0;
     wave_lds_sync();
+    // this block's copy of the digit-0 histogram (global threshold only)
+    const int h0_at = kHistH0 + (a.per_tensor ? 0 : (int)(blockIdx.x % kH0Copies) * kNB0);
     const uint32_t ntiles = a.tile_base[a.T];
     for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += gridDim.x * kWavesPerBlock) {
         const uint32_t tile = t0 + w;
         if (tile >= ntiles) {
             if (lane == 0) wseg[w] = kNoKey;
-            if (!a.sampled) block_flush<kNB0>(a, lh, wseg, kHistH0);  // block-uniform
+            if (!a.sampled) block_flush<kNB0>(a, lh, wseg, h0_at);  // block-uniform
             continue;
         }
         TileView v;
@@ -235,7 +237,7 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
             else lds_hist_add16(hw, (vb[r] & 0x7FFFFFFFu) >> kD0Shift, active && !a.sampled);
         }
         if (lane == 0) wseg[w] = v.s;
-        if (!a.sampled) block_flush<kNB0>(a, lh, wseg, kHistH0);  // a sampled threshold needs no histogram
+        if (!a.sampled) block_flush<kNB0>(a, lh, wseg, h0_at);  // a sampled threshold needs no histogram
     }
 }
 
@@ -332,7 +334,10 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
                 const uint32_t zero = a.seg[v.s].zero;
                 uint32_t p0, r0, d, ab;
                 read_level<L>(a.seg[v.s], v.k, p0, r0);
-                wave_pick<Lv::kPrevNB, Lv::kPrevCopies>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
+                if (L == 1 && !a.per_tensor)
+                    wave_pick<Lv::kPrevNB, kH0Copies>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
+                else
+                    wave_pick<Lv::kPrevNB, Lv::kPrevCopies>(seg_hist(a, v.s, Lv::kPrevHist), r0, d, ab);
                 // the zero mode knows its threshold: no key matches, nothing counted
                 prefix = zero ? kNoKey : (p0 << Lv::kPrevBits) | d;
                 rank = r0 - ab;
