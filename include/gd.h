@@ -78,7 +78,7 @@ typedef struct gd_ctx gd_ctx;
  *     the sequence non-decreasing (empty tensors are allowed) and
  *     N = tensor_offsets[T] at most 2^32 - 2 (indices are sent as uint32).
  *   Allocates all device scratch on the current HIP device (about 16 bytes
- *   per element plus about 128 KB per tensor for the per-tensor histograms);
+ *   per element plus about 135 KB per tensor for the per-tensor histograms);
  *   gd_compress never allocates.  Any number of tensors is accepted.
  *   Returns GD_ERR_LAYOUT for a bad layout, GD_ERR_OOM when allocation fails.
  */

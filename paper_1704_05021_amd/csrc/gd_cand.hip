@@ -299,10 +299,15 @@ constexpr int radix_lds() {
 // wave keeps a run: the first bin it meets and how many of its candidates
 // fell in it, added once when the wave moves to another segment or ends.
 // Candidates in other bins are added one by one.
+// This block's copy of the coarse digit-2 bins (global threshold only).
+__device__ __forceinline__ int h2c_copy(const CandArgs& a) {
+    return a.per_tensor ? 0 : (int)(blockIdx.x % kH2cCopies) * kNB2c;
+}
+
 __device__ __forceinline__ void run_flush(const CandArgs& a, uint32_t s, uint32_t d, uint32_t c) {
     if (c != 0 && lane_id() == 0) {
         atomicAdd(seg_hist(a, s, kHistH2) + d, c);
-        atomicAdd(seg_hist(a, s, kHistH2c) + (d >> kD2cShift), c);
+        atomicAdd(seg_hist(a, s, kHistH2c) + h2c_copy(a) + (d >> kD2cShift), c);
     }
 }
 
@@ -365,7 +370,7 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
                     run_c = 0;
                 }
                 uint32_t* hf = seg_hist(a, v.s, kHistH2);
-                uint32_t* hc = seg_hist(a, v.s, kHistH2c);
+                uint32_t* hc = seg_hist(a, v.s, kHistH2c) + h2c_copy(a);
 #pragma unroll
                 for (int r = 0; r < kRows; ++r) {
                     const bool in = (uint32_t)(r * kWave + lane) < v.p1 - v.p0 && (key[r] >> Lv::kPrefixShift) == prefix;
@@ -489,7 +494,8 @@ __device__ __forceinline__ void phase_count(const CandArgs& a, const EmitArgs& o
             const uint32_t zero = a.seg[v.s].zero, clo = a.seg[v.s].clo;
             const uint32_t p18 = a.seg[v.s].p18, r2 = a.seg[v.s].r2;
             uint32_t dc, abc, df, abf;
-            wave_pick<kNB2c>(seg_hist(a, v.s, kHistH2c), r2, dc, abc);
+            if (a.per_tensor) wave_pick<kNB2c>(seg_hist(a, v.s, kHistH2c), r2, dc, abc);
+            else wave_pick<kNB2c, kH2cCopies>(seg_hist(a, v.s, kHistH2c), r2, dc, abc);
             wave_pick<kNB2 / kNB2c>(seg_hist(a, v.s, kHistH2) + (dc << kD2cShift), r2 - abc, df, abf);
             // zero mode: T = key 0; every candidate (nonzero) is above it and
             // the first k - cnt zeros, none of them a candidate, are kept

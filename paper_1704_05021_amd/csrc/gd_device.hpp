@@ -32,12 +32,14 @@ constexpr int kNB2c = 256, kD2cShift = 5;
 // Digit 1 is counted into kH1Copies copies of its histogram, picked by block
 // number, so that the many blocks of one large segment spread their adds
 // over several addresses per bin; the pick of digit 1 sums the copies.
-// Digit 0 likewise under a global threshold, whose one segment takes every
-// block's flush (per tensor, summing the copies costs more than it saves).
+// Digit 0 and the coarse bins of digit 2 likewise under a global threshold,
+// whose one segment takes every block's adds (per tensor, summing the copies
+// costs more than it saves).
 constexpr int kH1Copies = 8;
 constexpr int kH0Copies = 4;
+constexpr int kH2cCopies = 8;
 constexpr int kHistH0 = 0, kHistH1 = kH0Copies * kNB0, kHistH2 = kHistH1 + kH1Copies * kNB1, kHistH2c = kHistH2 + kNB2;
-constexpr int kHistWords = kH0Copies * kNB0 + kH1Copies * kNB1 + kNB2 + kNB2c;
+constexpr int kHistWords = kH0Copies * kNB0 + kH1Copies * kNB1 + kNB2 + kH2cCopies * kNB2c;
 
 // Sampling: units of 16 consecutive elements (one 64-byte line per array),
 // at most kMaxUnits units per segment.  A sample key is the top 16 bits of
