@@ -40,6 +40,12 @@
 // each wave counts into its own LDS histogram and the block adds the four
 // to the segment histogram once per round (waves of one segment merged), so
 // the global atomics on the few hot bins are a quarter of one per tile.
+// Those adds still meet on one address per bin from every block of a large
+// segment, so some histograms have copies, picked by block number, that the
+// next pick sums: digit 1 always, digit 0 and digit 2's coarse bins under a
+// global threshold (one segment, every block).  A segment of more than
+// kBigSegTiles tiles also keeps group sums of its tile counts, for emit's
+// prefixes.
 
 #include "gd_kernels.h"
 
