@@ -145,3 +145,21 @@ def test_zero_mode_full_size_sparse_step(per_tensor):
     # per tensor the three embeddings are short of nonzeros; globally the
     # dense tensors supply more than k nonzeros
     assert [s["zero"] for s in segs[:4]] == ([1, 1, 1, 0] if per_tensor else [0])
+
+
+@pytest.mark.parametrize("quant", [False, gd.GD_QUANT_SIGN_MEAN], ids=["plain", "sign_mean"])
+@pytest.mark.parametrize("per_tensor", [True, False], ids=["per_tensor", "global"])
+def test_zero_mode_all_zero(per_tensor, quant):
+    # tensors with no nonzero entry at all: no candidates and no tiles, so
+    # their kept zeros and counts come from the fill alone
+    off = [0, 100_000, 100_000, 100_003, 400_000]
+    rng = np.random.default_rng(28)
+    g = np.where(rng.random(off[-1]) < 0.5, np.float32(-0.0), np.float32(0.0)).astype(np.float32)
+    comp = gd.Compressor(off)
+    check_case(g, np.zeros_like(g), off, 0.99, per_tensor, quant, comp=comp,
+               what=f"all zero, per_tensor={per_tensor}, quant={quant}")
+    segs = _segments(comp, per_tensor)
+    if per_tensor:
+        assert [s["zero"] for s in segs] == [1, 0, 0, 1]  # the 3-element tensor keeps nothing
+    else:
+        assert segs[0]["zero"] == 1
