@@ -8,15 +8,28 @@ embeddings with Zipf-sparse rows plus GRU-shaped dense tensors), per-tensor
 threshold, 99% drop.  Ten seeded gradient steps are staged in HBM before
 timing; timed steps cycle through them with the residual carried.
 
+Timing protocol: after the warm-up calls, each of the K timed calls is
+preceded by a read-modify-write of a 1 GiB scrub buffer (four times the
+256 MB Infinity Cache), so that no input is served from the cache, and is
+bracketed by HIP events on the stream it runs on.  ``ms_per_step`` is the
+median of those cold calls (p10 and p90 beside it); K more calls without the
+scrub are reported as ``warm`` for information.
+
 Prints one JSON line.  ``value`` is gradient elements compressed per second
-(whole job, inputs resident in HBM).  ``roofline`` reports the dense pass
-(the kernel that streams grad and residual) against the 8 TB/s HBM peak under
-the 12-bytes-per-element model; ``cpu_baseline`` times the CPU oracle on a
-bounded sample of the same workload.
+(whole job, inputs resident in HBM), from the cold median.  ``roofline``
+reports the dense pass (the kernel that streams grad and residual) against
+the 8 TB/s HBM peak under the 12-bytes-per-element model; ``cpu_baseline``
+times the CPU oracle on a bounded sample of the same workload.  On the
+NMT-shaped per-tensor workload the same staged gradients are also run with a
+global threshold and per-tensor sign-mean 1-bit centres (Section 5.4), and
+that row is reported under ``nmt_85k_global_signmean``.
 """
 import argparse
 import json
 import os
+import platform
+import statistics
+import subprocess
 import sys
 import time
 
@@ -26,6 +39,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 METRIC = "G grad-elements/s compressed at 99% drop; % of HBM peak (1 GPU)"
 SAMPLED_CAPACITY_PCT = 4  # output room of the sampled mode, in percent of the elements
+SCRUB_BYTES = 1 << 30  # read and written before every cold call: four times the 256 MB Infinity Cache
 QUANT_KINDS = {"none": 0, "sign_mean": 1, "threshold": 2, "global_mean": 3, "column_mean": 4}
 
 
@@ -48,6 +62,9 @@ def parse():
                     help="sample size per million entries for --selection sampled (1000 = 0.1%%)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=12.0,
                     help="rough bound on oracle CPU time for the cpu_baseline leg (0 disables it)")
+    ap.add_argument("--with-global-signmean", type=int, default=1,
+                    help="on nmt_85k_per_tensor, also time the global threshold with sign-mean centres on the "
+                         "same gradients (1, the default) or not (0)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB five times (the known-size "
                          "kernel that scales the HBM byte counters), then exit")
@@ -90,7 +107,93 @@ def cpu_baseline(w, grads_host, budget_s, sample_ppm=0, quant=0):
         "kind": "oracle",
         "sample": f"{done} consecutive steps of {w.name} from zero residual, cycling its {len(grads_host)} "
                   f"staged gradients ({elapsed:.1f} s of single-threaded oracle time)",
+        **host_info(),
     }, first
+
+
+def host_info():
+    """The host the oracle ran on: logical CPUs, those this process may use, and the CPU model."""
+    model = None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.lower().startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except (OSError, subprocess.SubprocessError):
+        pass
+    if model is None:
+        try:
+            with open("/proc/cpuinfo") as fh:
+                for line in fh:
+                    if line.lower().startswith("model name"):
+                        model = line.split(":", 1)[1].strip()
+                        break
+        except OSError:
+            model = platform.processor() or None
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = None
+    return {"host_cpus": os.cpu_count(), "host_cpus_usable": usable, "cpu_model": model}
+
+
+def make_scrub(torch):
+    """A callable that reads and writes SCRUB_BYTES of device memory on the current stream."""
+    buf = torch.zeros(SCRUB_BYTES // 4, dtype=torch.float32, device="cuda")
+
+    def scrub():
+        buf.add_(1.0)
+
+    return scrub
+
+
+def time_calls(torch, step, first, count, scrub=None):
+    """Per-call times (ms) of step(first) .. step(first + count - 1), each bracketed by HIP events on
+    the current stream (the stream the calls are enqueued on); with ``scrub``, it runs before each
+    call, outside the events."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(count)]
+    for i in range(count):
+        if scrub is not None:
+            scrub()
+        ev[i][0].record()
+        step(first + i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def pct(xs, q):
+    """q-th percentile (0..100) of xs by linear interpolation."""
+    ys = sorted(xs)
+    if len(ys) == 1:
+        return ys[0]
+    x = (len(ys) - 1) * q / 100.0
+    i = int(x)
+    j = min(i + 1, len(ys) - 1)
+    return ys[i] + (ys[j] - ys[i]) * (x - i)
+
+
+def spread(ms):
+    return {"ms_median": round(statistics.median(ms), 4), "ms_p10": round(pct(ms, 10), 4),
+            "ms_p90": round(pct(ms, 90), 4)}
+
+
+def quant_residuals_ok(np, idx, val, sign_bits, means, residual, offsets, quant, columns=None):
+    """Each kept entry's residual is one binary32 subtraction, acc - centre: bit-equal to it, taken
+    with this call's own centre of the entry's group (tensor, or column) and sign."""
+    off = np.asarray(offsets, np.int64)
+    i = idx.astype(np.int64)
+    t = np.searchsorted(off, i, side="right") - 1
+    if quant == 4:
+        cols = np.asarray(columns, np.int64)
+        grp = np.concatenate([[0], np.cumsum(cols)])[t] + (i - off[t]) % cols[t]
+    else:
+        grp = t
+    j = np.arange(idx.size, dtype=np.int64)
+    bit = (sign_bits[j >> 5].astype(np.int64) >> (j & 31)) & 1
+    want = val.astype(np.float32) - means.astype(np.float32)[2 * grp + bit]
+    return bool(np.array_equal(residual[idx].view(np.uint32), want.view(np.uint32)))
 
 
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_dense_nmt_85k_per_tensor_traffic.md")
@@ -190,16 +293,30 @@ def main_shard(args, torch, np, gd, wl):
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    scrub = make_scrub(torch)
     comp.profile_enable(DENSE_TIMING_EVERY)
     torch.cuda.synchronize()
+    # cold calls, with the apply's share timed by an event between its two parts
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i)
+        scrub()
+        ev[i][0].record()
+        gd.apply_sparse(p, idx, val, lr=1.0)
+        ev[i][1].record()
+        if use_copy:
+            comp.compress_pull(p, p_last, drop, per_tensor=False, out=out)
+        else:
+            comp.compress(p, pull_res, drop, per_tensor=False, base=p_last, out=out)
+        ev[i][2].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    cold = [a.elapsed_time(c) for a, _, c in ev]
+    cold_apply = [a.elapsed_time(b) for a, b, _ in ev]
     dense_ms, dense_n = comp.profile_read()
     comp.profile_enable(0)
-    sec = (t1 - t0) / args.steps
+    warm = time_calls(torch, step, args.warmup + args.steps, args.steps)
+    sec = statistics.median(cold) / 1e3
     dense_avg_s = dense_ms / 1e3 / max(dense_n, 1)
     dense_bytes = 8 if use_copy else 16  # params and copy read; or params, base and residual read, residual written
     achieved = dense_bytes * N / dense_avg_s / 1e9
@@ -218,6 +335,15 @@ def main_shard(args, torch, np, gd, wl):
         "dtype": "f32",
         "data": "synthetic",
         "hbm_model_frac": round(model_bytes / sec / 1e9 / HBM_PEAK_GBPS, 4),
+        "timing": {
+            "cold": spread(cold),
+            "warm": spread(warm),
+            "apply_cold": spread(cold_apply),
+            "per_call": "HIP events around each step (apply, then the pull) on its stream; cold calls follow "
+                        f"a read-modify-write of a {SCRUB_BYTES >> 20} MiB scrub buffer; ms_per_step is the "
+                        "cold median",
+            "timed_region_s": round(t1 - t0, 4),
+        },
         "config": {
             "workload": "shard_apply_pull",
             "elements": N,
@@ -258,11 +384,64 @@ def main_shard(args, torch, np, gd, wl):
             "value": N / el / 1e9, "unit": "G grad-elements/s", "cores": 1, "kind": "oracle",
             "sample": f"one step (apply of {len(sh.idx)} pushes, then the pull delta) of the 37M shard "
                       f"({el:.1f} s of single-threaded oracle time)",
+            **host_info(),
         }
         line["parity_step0"] = bool(np.array_equal(p1.view(np.uint32), first_p.view(np.uint32)) and
                                     np.array_equal(o.idx, first_idx) and
                                     np.array_equal(want_state.view(np.uint32), first_res.view(np.uint32)))
     print(json.dumps(line), flush=True)
+
+
+def oracle_quant_step_ok(np, o, idx, val, res, sign_bits, means, offsets, quant, columns=None):
+    """One quantised call against the oracle's: sent indices and values and sign bits bit-exact, centres
+    within 1e-6 relative (fp64 sums in another order), dropped residuals bit-exact, and every kept
+    residual bit-equal to fl32(acc - its own centre) with the GPU's centres."""
+    kept = np.zeros(res.size, bool)
+    kept[o.idx] = True
+    m_o = o.means.astype(np.float64)
+    return bool(np.array_equal(o.idx, idx) and np.array_equal(o.val.view(np.uint32), val.view(np.uint32)) and
+                np.array_equal(o.sign_bits, sign_bits) and
+                np.all(np.abs(means.astype(np.float64) - m_o) <= 1e-6 * np.abs(m_o)) and
+                np.array_equal(o.residual[~kept].view(np.uint32), res[~kept].view(np.uint32)) and
+                quant_residuals_ok(np, idx, val, sign_bits, means, res, offsets, quant, columns))
+
+
+def bench_global_signmean(args, torch, np, gd, wl, comp, grads, scrub):
+    """The global threshold with per-tensor sign-mean centres (Section 5.4) on the same staged NMT-shaped
+    gradients and the same context: its own carried residual, the same cold/warm protocol."""
+    N = comp.N
+    drop = 0.99
+    residual = torch.zeros(N, dtype=torch.float32, device="cuda")
+    k = comp.keep_total(drop, False)
+    out = comp.alloc_out(drop, False, 1)
+
+    def step(i):
+        comp.compress(grads[i % len(grads)], residual, drop, per_tensor=False, quant=1, out=out)
+
+    step(0)
+    torch.cuda.synchronize()
+    rec = {"idx": out.idx[:k].cpu().numpy().view(np.uint32).copy(), "val": out.val[:k].cpu().numpy().copy(),
+           "res": residual.cpu().numpy().copy(),
+           "bits": out.sign_bits[:(k + 31) // 32].cpu().numpy().view(np.uint32).copy(),
+           "means": out.means[:2 * comp.T].cpu().numpy().copy()}
+    residual.zero_()
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    cold = time_calls(torch, step, args.warmup, args.steps, scrub)
+    warm = time_calls(torch, step, args.warmup + args.steps, args.steps)
+    sec = statistics.median(cold) / 1e3
+    rec["line"] = {
+        "value": round(N / sec / 1e9, 3),
+        "unit": "G grad-elements/s",
+        "ms_per_step": round(sec * 1e3, 4),
+        "hbm_model_frac": round((12 * N + 8 * k) / sec / 1e9 / HBM_PEAK_GBPS, 4),
+        "timing": {"cold": spread(cold), "warm": spread(warm)},
+        "config": {"workload": "nmt_85k_global_signmean", "elements": N, "kept_per_step": k,
+                   "threshold": "global", "quant": "sign_mean", "drop": drop,
+                   "byte_model": "12 B/element + 8 B/kept element"},
+    }
+    return rec
 
 
 def main():
@@ -325,23 +504,26 @@ def main():
     torch.cuda.synchronize()
     k0 = kept_now()
     first_idx = out.idx[:k0].cpu().numpy().view(np.uint32).copy()
+    first_val = out.val[:k0].cpu().numpy().copy()
     first_res = residual.cpu().numpy().copy()
+    first_bits = out.sign_bits[:(k0 + 31) // 32].cpu().numpy().view(np.uint32).copy() if quant else None
+    first_means = out.means[:comp.quant_centres(quant)].cpu().numpy().copy() if quant else None
     residual.zero_()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    scrub = make_scrub(torch)
     comp.profile_enable(DENSE_TIMING_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(args.warmup + i)
-    torch.cuda.synchronize()
+    cold = time_calls(torch, step, args.warmup, args.steps, scrub)
     t1 = time.perf_counter()
     dense_ms, dense_n = comp.profile_read()
     comp.profile_enable(0)
+    warm = time_calls(torch, step, args.warmup + args.steps, args.steps)
 
-    sec = (t1 - t0) / args.steps
+    sec = statistics.median(cold) / 1e3
     value = N / sec / 1e9
     k = kept_now()  # the sampled mode's count varies: the last timed step's
     model_bytes = 12 * N + 8 * k
@@ -361,6 +543,13 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "hbm_model_frac": round(model_bytes / sec / 1e9 / HBM_PEAK_GBPS, 4),
+        "timing": {
+            "cold": spread(cold),
+            "warm": spread(warm),
+            "per_call": "HIP events around each call on its stream; cold calls follow a read-modify-write "
+                        f"of a {SCRUB_BYTES >> 20} MiB scrub buffer; ms_per_step is the cold median",
+            "timed_region_s": round(t1 - t0, 4),
+        },
         "config": {
             "workload": w.name,
             "elements": N,
@@ -387,15 +576,27 @@ def main():
             "dense_timed_every": DENSE_TIMING_EVERY,
         },
     }
+    extra = None
+    if w.name == "nmt_85k_per_tensor" and not sampled and args.quant == "workload" and args.with_global_signmean:
+        extra = bench_global_signmean(args, torch, np, gd, wl, comp, grads, scrub)
+        line["nmt_85k_global_signmean"] = extra["line"]
     if args.cpu_baseline_seconds > 0:
         cb, first = cpu_baseline(w, grads_host, args.cpu_baseline_seconds, args.sample_ppm if sampled else 0, quant)
         line["cpu_baseline"] = cb
-        if quant in (0, 2):  # no float reduction: bit-exact
+        if quant in (0,):  # no float reduction: bit-exact everywhere
             res_ok = np.array_equal(first.residual.view(np.uint32), first_res.view(np.uint32))
-        else:  # centres are fp64 sums in another order: within 1e-6 of the largest centre
-            scale = float(np.max(np.abs(first.means))) if first.means is not None and first.means.size else 0.0
-            res_ok = bool(np.all(np.abs(first.residual.astype(np.float64) - first_res) <= 1e-6 * scale))
+        else:
+            res_ok = oracle_quant_step_ok(np, first, first_idx, first_val, first_res, first_bits, first_means,
+                                          off, quant, w.layout.columns)
         line["parity_step0"] = bool(np.array_equal(first.idx, first_idx) and res_ok)
+        if extra is not None:
+            import oracle
+
+            o = oracle.compress(grads_host[0], np.zeros(N, np.float32), off, w.drop, per_tensor=False, quant=1)
+            line["nmt_85k_global_signmean"]["parity_step0"] = bool(
+                np.array_equal(o.idx, extra["idx"]) and
+                oracle_quant_step_ok(np, o, extra["idx"], extra["val"], extra["res"], extra["bits"],
+                                     extra["means"], off, 1))
     print(json.dumps(line), flush=True)
 
 

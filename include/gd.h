@@ -72,7 +72,10 @@ typedef enum {
 typedef struct gd_ctx gd_ctx;
 
 /*
- * gd_create - describe a gradient made of T tensors laid end to end.
+ * gd_create - describe a gradient made of T tensors laid end to end
+ * (Section 4, last paragraph: the threshold is chosen either over all
+ * parameters or separately for each parameter matrix, so the compressor must
+ * know where each matrix starts; Algorithm 1 then runs over this layout).
  *   tensor_offsets (host, T+1 entries): tensor t occupies flat indices
  *     [tensor_offsets[t], tensor_offsets[t+1]); tensor_offsets[0] must be 0,
  *     the sequence non-decreasing (empty tensors are allowed) and
@@ -84,18 +87,25 @@ typedef struct gd_ctx gd_ctx;
  */
 gd_status gd_create(gd_ctx** out, const uint64_t* tensor_offsets, uint32_t num_tensors);
 
-/* Frees the scratch.  The caller must make sure no enqueued call still uses it. */
+/* Infrastructure, no passage of the paper: frees the scratch gd_create
+ * allocated.  The caller must make sure no enqueued call still uses it.  NULL
+ * is accepted and ignored. */
 void gd_destroy(gd_ctx* ctx);
 
 /*
- * Number of entries kept out of n at drop ratio R (Algorithm 1: "R% of |grad|
- * is smaller").  R is taken in parts per million: keep_ppm = round((1-R)*1e6)
+ * Number of entries kept out of n at drop ratio R (Algorithm 1, threshold
+ * selection: the threshold is placed so that the fraction R of |acc| lies
+ * below it).  R is taken in parts per million: keep_ppm = round((1-R)*1e6)
  * and k = floor(n * keep_ppm / 1e6).  Returns 0 for R outside [0,1].
  */
 uint64_t gd_keep_count(uint64_t n, double drop_ratio);
 
-/* Total kept entries of one gd_compress call: k(N) for GD_GLOBAL, the sum of
- * k(n_t) over tensors for GD_PER_TENSOR.  This is the exact output size. */
+/* Total kept entries of one gd_compress call (Algorithm 1 applied once over
+ * all parameters, or once per parameter matrix as Section 4's last paragraph
+ * allows): k(N) for GD_GLOBAL, the sum of k(n_t) over tensors for
+ * GD_PER_TENSOR.  This is the exact output size, known on the host before
+ * anything is enqueued.  Returns 0 for a NULL ctx or R outside [0,1]; any
+ * mode other than GD_GLOBAL is taken as GD_PER_TENSOR. */
 uint64_t gd_keep_total(const gd_ctx* ctx, double drop_ratio, gd_threshold mode);
 
 /* Output buffers of gd_compress (all device pointers, caller-owned). */
@@ -217,7 +227,11 @@ gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base,
  *   For every index i that appears in any push: s = sum of the pushed values
  *   at i, added in push order starting from +0.0; params[i] -= lr * s.
  *   num_pushes may be 0 (nothing happens); at most 64 pushes per call.
- *   The result is deterministic.
+ *   The result is deterministic when the precondition above holds.  It is not
+ *   checked on the device (that would need a host synchronisation): an index
+ *   repeated inside one push is applied by two threads that race, and an
+ *   unsorted push can have entries skipped.  The Python binding checks it on
+ *   request (apply_sparse(..., validate=True)).
  */
 gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const uint32_t* const* idx,
                           const float* const* val, const uint64_t* nnz, float lr, void* stream);
@@ -242,7 +256,8 @@ gd_status gd_apply_quantised(gd_ctx* ctx, float* params, uint32_t num_pushes, co
                              const uint32_t* const* sign_bits, const float* const* means, const uint64_t* nnz,
                              gd_quant quant, float lr, void* stream);
 
-/* Static description of a status code. */
+/* Infrastructure, no passage of the paper: a static, NUL-terminated
+ * description of a status code ("unknown status" for other values). */
 const char* gd_status_string(gd_status status);
 
 /*

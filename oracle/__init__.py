@@ -28,11 +28,12 @@ CXXFLAGS = ["-O2", "-std=c++17", "-ffp-contract=off", "-fno-fast-math", "-fPIC",
 _lib_cache = {}
 
 
-def build(out: Optional[str] = None, defines: Sequence[str] = ()) -> str:
-    """Compile the oracle with g++ into ``out`` (default: next to the source)."""
+def build(out: Optional[str] = None, defines: Sequence[str] = (), extra_flags: Sequence[str] = ()) -> str:
+    """Compile the oracle with g++ into ``out`` (default: next to the source);
+    ``extra_flags`` are added to the g++ line (e.g. sanitizers, for a test build)."""
     out = out or _LIB
     tmp = out + f".tmp{os.getpid()}"
-    cmd = ["g++", *CXXFLAGS, *[f"-D{d}" for d in defines], _SRC, "-o", tmp]
+    cmd = ["g++", *CXXFLAGS, *extra_flags, *[f"-D{d}" for d in defines], _SRC, "-o", tmp]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
     return out
@@ -74,6 +75,11 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib = _declare(ctypes.CDLL(path))
     _lib_cache[path] = lib
     return lib
+
+
+def declare(lib: ctypes.CDLL) -> ctypes.CDLL:
+    """Set the argument and result types of an oracle library loaded elsewhere."""
+    return _declare(lib)
 
 
 def build_variant(defines: Sequence[str]) -> ctypes.CDLL:

@@ -33,6 +33,20 @@ struct DeviceGuard {
 
 uint64_t keep_ppm_of(double drop_ratio) { return (uint64_t)std::llround((1.0 - drop_ratio) * 1e6); }
 
+// The integer a C caller passed for an enum parameter.  A C caller may pass
+// any int; in C++ reading an enum object that holds a value outside the
+// enumeration is undefined, so the bytes are copied out instead and checked
+// as an int.
+template <typename E>
+int enum_int(const E* e) {
+    static_assert(sizeof(E) == sizeof(int), "C enums are int-sized");
+    int v;
+    std::memcpy(&v, e, sizeof v);
+    return v;
+}
+bool valid_mode(int m) { return m == GD_GLOBAL || m == GD_PER_TENSOR; }
+bool valid_quant(int q) { return q >= GD_QUANT_NONE && q <= GD_QUANT_COLUMN_MEAN; }
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // Units of 16 elements sampled for a segment [a, b) and the number of sample keys stored.
@@ -216,8 +230,8 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
 
 extern "C" {
 
-const char* gd_status_string(gd_status s) {
-    switch (s) {
+const char* gd_status_string(gd_status status) {
+    switch (enum_int(&status)) {
         case GD_OK: return "ok";
         case GD_ERR_ARG: return "invalid argument";
         case GD_ERR_LAYOUT: return "invalid tensor layout";
@@ -236,7 +250,7 @@ uint64_t gd_keep_count(uint64_t n, double drop_ratio) {
 
 uint64_t gd_keep_total(const gd_ctx* ctx, double drop_ratio, gd_threshold mode) {
     if (!ctx) return 0;
-    if (mode == GD_GLOBAL) return gd_keep_count(ctx->N, drop_ratio);
+    if (enum_int(&mode) == GD_GLOBAL) return gd_keep_count(ctx->N, drop_ratio);
     uint64_t k = 0;
     for (uint32_t t = 0; t < ctx->T; ++t) k += gd_keep_count(ctx->offsets[t + 1] - ctx->offsets[t], drop_ratio);
     return k;
@@ -351,8 +365,7 @@ void gd_destroy(gd_ctx* ctx) {
 gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* residual, double drop_ratio,
                       gd_threshold mode, gd_quant quant, const gd_sparse* out, void* stream) {
     if (!ctx || !out || (ctx->N > 0 && (!grad || !residual))) return GD_ERR_ARG;  // an empty layout needs no data
-    if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
-    if (quant < GD_QUANT_NONE || quant > GD_QUANT_COLUMN_MEAN) return GD_ERR_ARG;
+    if (!valid_mode(enum_int(&mode)) || !valid_quant(enum_int(&quant))) return GD_ERR_ARG;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
     if (!out->idx || !out->val || !out->tensor_counts) return GD_ERR_ARG;
     if (quant != GD_QUANT_NONE && (!out->sign_bits || !out->means)) return GD_ERR_ARG;
@@ -392,7 +405,7 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
 gd_status gd_compress_pull(gd_ctx* ctx, const float* params, float* copy, double drop_ratio, gd_threshold mode,
                            const gd_sparse* out, void* stream) {
     if (!ctx || !out || (ctx->N > 0 && (!params || !copy))) return GD_ERR_ARG;  // an empty layout needs no data
-    if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
+    if (!valid_mode(enum_int(&mode))) return GD_ERR_ARG;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
     if (!out->idx || !out->val || !out->tensor_counts) return GD_ERR_ARG;
     if (!aligned16(params) || !aligned16(copy)) return GD_ERR_ALIGN;
@@ -441,16 +454,16 @@ gd_status gd_set_columns(gd_ctx* ctx, const uint32_t* columns) {
 }
 
 uint64_t gd_quant_centres(const gd_ctx* ctx, gd_quant quant) {
-    if (!ctx || quant == GD_QUANT_NONE) return 0;
-    return quant == GD_QUANT_COLUMN_MEAN ? 2 * (uint64_t)ctx->cols.groups : 2 * (uint64_t)ctx->T;
+    const int q = enum_int(&quant);
+    if (!ctx || q == GD_QUANT_NONE || !valid_quant(q)) return 0;
+    return q == GD_QUANT_COLUMN_MEAN ? 2 * (uint64_t)ctx->cols.groups : 2 * (uint64_t)ctx->T;
 }
 
 gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base, float* residual,
                               double drop_ratio, gd_threshold mode, uint32_t sample_ppm, uint64_t seed,
                               gd_quant quant, const gd_sparse* out, void* stream) {
     if (!ctx || !out || (ctx->N > 0 && (!grad || !residual))) return GD_ERR_ARG;  // an empty layout needs no data
-    if (mode != GD_GLOBAL && mode != GD_PER_TENSOR) return GD_ERR_ARG;
-    if (quant < GD_QUANT_NONE || quant > GD_QUANT_COLUMN_MEAN) return GD_ERR_ARG;
+    if (!valid_mode(enum_int(&mode)) || !valid_quant(enum_int(&quant))) return GD_ERR_ARG;
     if (quant != GD_QUANT_NONE && (!out->means || (out->capacity && !out->sign_bits))) return GD_ERR_ARG;
     if (!(drop_ratio >= 0.0 && drop_ratio <= 1.0)) return GD_ERR_ARG;
     if (sample_ppm == 0 || sample_ppm > 1000000u) return GD_ERR_ARG;
@@ -521,7 +534,7 @@ gd_status gd_apply_quantised(gd_ctx* ctx, float* params, uint32_t num_pushes, co
                              const uint32_t* const* sign_bits, const float* const* means, const uint64_t* nnz,
                              gd_quant quant, float lr, void* stream) {
     if (!ctx || num_pushes > gd::kMaxPushes) return GD_ERR_ARG;
-    if (quant < GD_QUANT_SIGN_MEAN || quant > GD_QUANT_COLUMN_MEAN) return GD_ERR_ARG;
+    if (!valid_quant(enum_int(&quant)) || enum_int(&quant) == GD_QUANT_NONE) return GD_ERR_ARG;
     if (num_pushes == 0 || ctx->N == 0) return GD_OK;
     if (!params || !idx || !sign_bits || !means || !nnz) return GD_ERR_ARG;
     gd::ApplyArgs a{};

@@ -267,7 +267,10 @@ __device__ uint32_t block_excl_scan(uint32_t v, uint32_t* lds, uint32_t* total) 
     return incl - v + carry;
 }
 
-// Stateless 32-bit mixer (a fixed integer hash) for sample positions.
+// Stateless 32-bit mixer for the bracket sample's positions: the published
+// "lowbias32" integer hash (xor-shift / multiply rounds with the shifts and
+// multipliers found by C. Wellons' hash-prospector search, 2018).  Any good
+// mixer would do; the positions only have to spread over each stratum.
 __device__ __forceinline__ uint32_t mix32(uint32_t x) {
     x ^= x >> 16;
     x *= 0x7feb352dU;

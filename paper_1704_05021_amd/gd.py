@@ -244,8 +244,11 @@ class Compressor:
         return out
 
     def apply_quantised(self, params: torch.Tensor, idx, sign_bits, means, quant: int, lr: float = 1.0,
-                        stream: Optional[torch.cuda.Stream] = None) -> None:
-        """gd_apply_quantised: decode quantised pushes of this layout and apply them to params."""
+                        stream: Optional[torch.cuda.Stream] = None, validate: bool = False) -> None:
+        """gd_apply_quantised: decode quantised pushes of this layout and apply them to params.
+
+        validate: as for ``apply_sparse``, check first that each push's indices are strictly ascending.
+        """
         _check_f32(params, "params", self.N)
         C = len(idx)
         if not (len(sign_bits) == len(means) == C):
@@ -256,6 +259,8 @@ class Compressor:
             if not (a.is_cuda and b.is_cuda and m.is_cuda and a.is_contiguous() and b.is_contiguous()
                     and m.is_contiguous()):
                 raise TypeError("push tensors must be contiguous GPU tensors")
+        if validate:
+            _check_pushes_ascending(idx)
         arr = lambda xs: (ctypes.c_void_p * max(C, 1))(*[x.data_ptr() for x in xs])
         ip, bp, mp = arr(idx), arr(sign_bits), arr(means)
         nz = (ctypes.c_uint64 * max(C, 1))(*[a.numel() for a in idx])
@@ -346,9 +351,25 @@ class Compressor:
         return ms.value, n.value
 
 
+def _check_pushes_ascending(idx: List[torch.Tensor]) -> None:
+    """Raises GDError(GD_ERR_ARG) unless every push's indices (uint32 bits in
+    int32 storage) are strictly ascending: the precondition gd_apply_sparse
+    relies on and does not check.  Synchronises with the device."""
+    for c, a in enumerate(idx):
+        if a.numel() > 1:
+            u = a.to(torch.int64) & 0xFFFFFFFF
+            if not bool(torch.all(u[1:] > u[:-1])):
+                raise GDError(1, f"apply: push {c} is not strictly ascending")
+
+
 def apply_sparse(params: torch.Tensor, idx: List[torch.Tensor], val: List[torch.Tensor], lr: float = 1.0,
-                 stream: Optional[torch.cuda.Stream] = None) -> None:
-    """gd_apply_sparse: params[i] -= lr * (sum of pushed values at i, in push order)."""
+                 stream: Optional[torch.cuda.Stream] = None, validate: bool = False) -> None:
+    """gd_apply_sparse: params[i] -= lr * (sum of pushed values at i, in push order).
+
+    validate: first check that each push's indices are strictly ascending
+    (unique and sorted), which the library assumes and does not check, and
+    raise GDError(GD_ERR_ARG) otherwise.  This synchronises with the device.
+    """
     if params.dtype != torch.float32 or not params.is_cuda or not params.is_contiguous():
         raise TypeError("params must be a contiguous float32 tensor on the GPU")
     C = len(idx)
@@ -359,6 +380,8 @@ def apply_sparse(params: torch.Tensor, idx: List[torch.Tensor], val: List[torch.
             raise TypeError("each push is an int32 (uint32 bits) index tensor and a float32 value tensor")
         if not (a.is_cuda and b.is_cuda and a.is_contiguous() and b.is_contiguous()):
             raise TypeError("push tensors must be contiguous GPU tensors")
+    if validate:
+        _check_pushes_ascending(idx)
     ip = (ctypes.c_void_p * max(C, 1))(*[a.data_ptr() for a in idx])
     vp = (ctypes.c_void_p * max(C, 1))(*[b.data_ptr() for b in val])
     nz = (ctypes.c_uint64 * max(C, 1))(*[a.numel() for a in idx])

@@ -17,6 +17,7 @@ from paper_1704_05021_amd import gd
 # Tolerance for results whose float reductions may be reordered on the GPU
 # (quantisation centres summed in fp64 in a different order).
 REL_TOL = 1e-6
+QUANT_COLUMN_MEAN = 4
 
 
 def bits(a: np.ndarray) -> np.ndarray:
@@ -60,9 +61,35 @@ def oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base=None,
     return Result(o.idx, o.val, o.residual, o.tensor_counts, o.sign_bits, o.means)
 
 
-def assert_parity(g: Result, o: Result, quant: bool, what: str = "") -> None:
+def centre_slots(idx: np.ndarray, bits_words: np.ndarray, offsets: Sequence[int], quant: int,
+                 columns: Optional[Sequence[int]] = None) -> np.ndarray:
+    """Position in the centre array of the centre each kept entry is sent as:
+    2 * group + sign bit, where the group is the entry's tensor, or under
+    column-wise centres its column (tensor t's columns follow those of the
+    tensors before it)."""
+    off = np.asarray(offsets, np.int64)
+    i = idx.astype(np.int64)
+    t = np.searchsorted(off, i, side="right") - 1  # last tensor starting at or before i (skips empty ones)
+    if int(quant) == QUANT_COLUMN_MEAN:
+        cols = np.asarray(columns if columns is not None else np.ones(off.size - 1), np.int64)
+        colbase = np.concatenate([[0], np.cumsum(cols)])
+        grp = colbase[t] + (i - off[t]) % cols[t]
+    else:
+        grp = t
+    j = np.arange(idx.size, dtype=np.int64)
+    bit = (bits_words[j >> 5].astype(np.int64) >> (j & 31)) & 1
+    return 2 * grp + bit
+
+
+def assert_parity(g: Result, o: Result, quant, what: str = "", offsets: Optional[Sequence[int]] = None,
+                  columns: Optional[Sequence[int]] = None) -> None:
     """Bit-exact on indices, values, counts, sign bits and unquantised residuals;
-    quantisation centres and the residuals built from them within REL_TOL."""
+    quantisation centres within REL_TOL of the oracle's.  A quantised kept
+    entry's residual is one binary32 subtraction, acc - centre: it must equal
+    that subtraction bit for bit, taken with the GPU's own centre of the
+    entry's group and sign (so each entry is judged against its own centre).
+    ``offsets`` (and ``columns`` for the column-wise centres) are required
+    for quantised results."""
     assert g.idx.shape == o.idx.shape, f"{what}: kept {g.idx.size} vs oracle {o.idx.size}"
     if not np.array_equal(g.idx, o.idx):
         bad = np.nonzero(g.idx != o.idx)[0]
@@ -82,9 +109,14 @@ def assert_parity(g: Result, o: Result, quant: bool, what: str = "") -> None:
     kept = np.zeros(o.residual.size, bool)
     kept[o.idx] = True
     assert np.array_equal(bits(g.residual[~kept]), bits(o.residual[~kept])), f"{what}: dropped residuals differ"
-    scale = np.max(np.abs(m_o)) if m_o.size else 0.0
-    diff = np.abs(g.residual[kept].astype(np.float64) - o.residual[kept].astype(np.float64))
-    assert np.all(diff <= REL_TOL * scale), f"{what}: quantised residuals differ by {diff.max()}"
+    assert offsets is not None, "quantised parity needs the layout's offsets"
+    slot = centre_slots(g.idx, g.sign_bits, offsets, int(quant), columns)
+    want = np.ascontiguousarray(g.val, np.float32) - g.means.astype(np.float32)[slot]  # one binary32 rounding
+    got = g.residual[g.idx]
+    if not np.array_equal(bits(got), bits(want)):
+        bad = np.nonzero(bits(got) != bits(want))[0]
+        raise AssertionError(f"{what}: {bad.size} quantised residuals are not fl32(acc - own centre), first at "
+                             f"index {g.idx[bad[0]]}: gpu {got[bad[0]]!r}, want {want[bad[0]]!r}")
     if np.array_equal(bits(g.means), bits(o.means)):
         assert np.array_equal(bits(g.residual), bits(o.residual)), f"{what}: equal centres but residuals differ"
 
@@ -104,5 +136,5 @@ def check_case(grad, residual, offsets: Sequence[int], drop: float, per_tensor: 
     finally:
         comp.debug_force_bracket(0)
     o = oracle_compress(grad, residual, offsets, drop, per_tensor, quant, base, columns)
-    assert_parity(g, o, quant, what)
+    assert_parity(g, o, quant, what, offsets=offsets, columns=columns)
     return o

@@ -72,3 +72,19 @@ def test_product_path_does_not_import_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text and "oracle.cpp" not in text, f
                 assert "gdo_" not in text, f
+
+
+def test_create_refuses_layouts_past_uint32_indices(gd):
+    """Indices are sent as uint32 and 2^32 - 1 is reserved, so gd_create takes N <= 2^32 - 2 and returns
+    GD_ERR_LAYOUT for N = 2^32 - 1 and above, before touching any device (checked without a GPU)."""
+    import ctypes
+
+    lib = gd.load()
+    h = ctypes.c_void_p()
+    for n in (2 ** 32 - 1, 2 ** 32, 2 ** 40):
+        offs = (ctypes.c_uint64 * 3)(0, 5, n)
+        assert lib.gd_create(ctypes.byref(h), offs, 2) == 2, n
+        assert h.value is None
+    for bad in ((3, 10), (0, 10, 5)):
+        offs = (ctypes.c_uint64 * len(bad))(*bad)
+        assert lib.gd_create(ctypes.byref(h), offs, len(bad) - 1) == 2, bad

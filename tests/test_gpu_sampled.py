@@ -58,7 +58,7 @@ def check(grad, residual, offsets, drop, per, ppm, seed, base=None, capacity=Non
             comp.set_columns(columns)
     g = gpu_sampled(comp, grad, residual, drop, per, ppm, seed, base, capacity, quant)
     o = oracle_sampled(grad, residual, offsets, drop, per, ppm, seed, base, capacity, quant, columns)
-    assert_parity(g, o, quant, what)
+    assert_parity(g, o, quant, what, offsets=offsets, columns=columns)
     return o
 
 
