@@ -9,9 +9,9 @@ threshold, 99% drop.  Ten seeded gradient steps are staged in HBM before
 timing; timed steps cycle through them with the residual carried.
 
 Timing protocol: after the warm-up calls, each of the K timed calls is
-preceded by a read-modify-write of a 1 GiB scrub buffer (four times the
-256 MB Infinity Cache), so that no input is served from the cache, and is
-bracketed by HIP events on the stream it runs on.  ``ms_per_step`` is the
+preceded by a read of a 1 GiB scrub buffer (four times the 256 MB Infinity
+Cache), so that no input is served from the cache, and is bracketed by HIP
+events on the stream it runs on.  ``ms_per_step`` is the
 median of those cold calls (p10 and p90 beside it); K more calls without the
 scrub are reported as ``warm`` for information.
 
@@ -62,6 +62,8 @@ def parse():
                     help="sample size per million entries for --selection sampled (1000 = 0.1%%)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=12.0,
                     help="rough bound on oracle CPU time for the cpu_baseline leg (0 disables it)")
+    ap.add_argument("--scrub", choices=("read", "rw"), default="read",
+                    help="what runs before each cold call: a 1 GiB read (default) or read-modify-write")
     ap.add_argument("--with-global-signmean", type=int, default=1,
                     help="on nmt_85k_per_tensor, also time the global threshold with sign-mean centres on the "
                          "same gradients (1, the default) or not (0)")
@@ -138,14 +140,21 @@ def host_info():
     return {"host_cpus": os.cpu_count(), "host_cpus_usable": usable, "cpu_model": model}
 
 
-def make_scrub(torch):
-    """A callable that reads and writes SCRUB_BYTES of device memory on the current stream."""
-    buf = torch.zeros(SCRUB_BYTES // 4, dtype=torch.float32, device="cuda")
+def make_scrub(torch, kind="read"):
+    """A callable that streams SCRUB_BYTES of device memory through the caches on the current stream:
+    a read (a sum into one float; the default) evicts the inputs and leaves only clean lines behind, a
+    read-modify-write (``rw``) also leaves the caches full of dirty lines that get written back while
+    the next call runs."""
+    buf = torch.ones(SCRUB_BYTES // 4, dtype=torch.float32, device="cuda")
+    acc = torch.zeros((), dtype=torch.float32, device="cuda")
 
-    def scrub():
+    def scrub_read():
+        torch.sum(buf, dim=0, out=acc)
+
+    def scrub_rw():
         buf.add_(1.0)
 
-    return scrub
+    return scrub_rw if kind == "rw" else scrub_read
 
 
 def time_calls(torch, step, first, count, scrub=None):
@@ -293,7 +302,7 @@ def main_shard(args, torch, np, gd, wl):
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    scrub = make_scrub(torch)
+    scrub = make_scrub(torch, args.scrub)
     comp.profile_enable(DENSE_TIMING_EVERY)
     torch.cuda.synchronize()
     # cold calls, with the apply's share timed by an event between its two parts
@@ -340,8 +349,8 @@ def main_shard(args, torch, np, gd, wl):
             "warm": spread(warm),
             "apply_cold": spread(cold_apply),
             "per_call": "HIP events around each step (apply, then the pull) on its stream; cold calls follow "
-                        f"a read-modify-write of a {SCRUB_BYTES >> 20} MiB scrub buffer; ms_per_step is the "
-                        "cold median",
+                        f"a {'read' if args.scrub == 'read' else 'read-modify-write'} of a {SCRUB_BYTES >> 20} "
+                        "MiB scrub buffer; ms_per_step is the cold median",
             "timed_region_s": round(t1 - t0, 4),
         },
         "config": {
@@ -513,7 +522,7 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    scrub = make_scrub(torch)
+    scrub = make_scrub(torch, args.scrub)
     comp.profile_enable(DENSE_TIMING_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -546,8 +555,9 @@ def main():
         "timing": {
             "cold": spread(cold),
             "warm": spread(warm),
-            "per_call": "HIP events around each call on its stream; cold calls follow a read-modify-write "
-                        f"of a {SCRUB_BYTES >> 20} MiB scrub buffer; ms_per_step is the cold median",
+            "per_call": "HIP events around each call on its stream; cold calls follow a "
+                        f"{'read' if args.scrub == 'read' else 'read-modify-write'} of a {SCRUB_BYTES >> 20} MiB "
+                        "scrub buffer; ms_per_step is the cold median",
             "timed_region_s": round(t1 - t0, 4),
         },
         "config": {
