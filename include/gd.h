@@ -256,6 +256,31 @@ gd_status gd_apply_quantised(gd_ctx* ctx, float* params, uint32_t num_pushes, co
                              const uint32_t* const* sign_bits, const float* const* means, const uint64_t* nnz,
                              gd_quant quant, float lr, void* stream);
 
+/*
+ * gd_compress_static - gd_compress for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  It takes the layout per call instead of a gd_ctx and
+ * allocates nothing (no device or host allocation, no memset); its kernels
+ * use a fixed 48 MiB scratch array compiled into the library, one copy per
+ * GPU, held from the first call on that GPU until the process ends.
+ *   tensor_offsets (host, num_tensors + 1 entries): as gd_create, with at
+ *     most 64 tensors and N = tensor_offsets[num_tensors] <= 2,097,152
+ *     elements; larger layouts return GD_ERR_LAYOUT (use gd_create).
+ *   grad, base, residual, drop_ratio, mode, out, stream: as gd_compress, and
+ *     the results are those of gd_compress on a context of the same layout.
+ *   quant: GD_QUANT_NONE, GD_QUANT_SIGN_MEAN, GD_QUANT_THRESHOLD or
+ *     GD_QUANT_GLOBAL_MEAN; GD_QUANT_COLUMN_MEAN needs a column view
+ *     (gd_set_columns) and is GD_ERR_ARG here.
+ *   Every call on one GPU shares that GPU's array, and a call starts by
+ *   rewriting the parts it uses: calls on one stream are ordered and safe,
+ *   but calls that overlap in time on one GPU (other streams, other threads)
+ *   race and give wrong results.  The first call on each GPU looks up that
+ *   GPU's copy of the array (GD_ERR_HIP if that fails).
+ */
+gd_status gd_compress_static(const uint64_t* tensor_offsets, uint32_t num_tensors, const float* grad,
+                             const float* base, float* residual, double drop_ratio, gd_threshold mode,
+                             gd_quant quant, const gd_sparse* out, void* stream);
+
 /* Infrastructure, no passage of the paper: a static, NUL-terminated
  * description of a status code ("unknown status" for other values). */
 const char* gd_status_string(gd_status status);

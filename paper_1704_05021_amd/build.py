@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libgd.so")
-SOURCES = ["gd_select.hip", "gd_sampled.hip", "gd_dense.hip", "gd_layout.hip", "gd_cand.hip", "gd_quant.hip", "gd_apply.hip", "gd_api.hip"]
+SOURCES = ["gd_select.hip", "gd_sampled.hip", "gd_dense.hip", "gd_layout.hip", "gd_cand.hip", "gd_quant.hip", "gd_apply.hip", "gd_api.hip", "gd_static.hip"]
 HEADERS = ["gd_device.hpp", "gd_kernels.h", "gd_internal.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

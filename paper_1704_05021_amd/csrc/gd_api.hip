@@ -228,6 +228,33 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
 
 }  // namespace
 
+namespace gd {
+
+gd_status compress_exact(gd_ctx* ctx, const float* grad, const float* base, float* residual, double drop_ratio,
+                         bool per, gd_quant quant, uint64_t k_total, const gd_sparse* out, hipStream_t st) {
+    const uint32_t ppm = (uint32_t)keep_ppm_of(drop_ratio);
+    SampleArgs sa{};
+    sa.grad = grad;
+    sa.base = base;
+    sa.res = residual;
+    sa.seg_off = per ? ctx->tab.tensor_off : ctx->tab.global_off;
+    sa.skey_base = per ? ctx->tab.skey_base_tensor : ctx->tab.skey_base_global;
+    sa.S = per ? ctx->T : 1u;
+    sa.T = ctx->T;
+    sa.keep_ppm = ppm;
+    sa.debug_bracket = ctx->debug_bracket;
+    sa.skeys = ctx->scr.skeys;
+    sa.seg = ctx->scr.seg;
+    sa.hist = ctx->scr.hist;
+    sa.shist = ctx->scr.shist;
+    sa.out_base = ctx->scr.out_base;
+    sa.tensor_counts = out->tensor_counts;
+    if (launch_sample(sa, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
+    return run_after_bracket(ctx, grad, base, residual, per, ppm, false, quant, k_total, out, st);
+}
+
+}  // namespace gd
+
 extern "C" {
 
 const char* gd_status_string(gd_status status) {
@@ -375,31 +402,8 @@ gd_status gd_compress(gd_ctx* ctx, const float* grad, const float* base, float* 
 
     DeviceGuard guard(ctx->device);
     if (!guard.ok) return GD_ERR_HIP;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    const bool per = mode == GD_PER_TENSOR;
-    const uint32_t ppm = (uint32_t)keep_ppm_of(drop_ratio);
-    const uint32_t S = per ? ctx->T : 1u;
-    const uint32_t* seg_off = per ? ctx->tab.tensor_off : ctx->tab.global_off;
-
-    gd::SampleArgs sa{};
-    sa.grad = grad;
-    sa.base = base;
-    sa.res = residual;
-    sa.seg_off = seg_off;
-    sa.skey_base = per ? ctx->tab.skey_base_tensor : ctx->tab.skey_base_global;
-    sa.S = S;
-    sa.T = ctx->T;
-    sa.keep_ppm = ppm;
-    sa.debug_bracket = ctx->debug_bracket;
-    sa.skeys = ctx->scr.skeys;
-    sa.seg = ctx->scr.seg;
-    sa.hist = ctx->scr.hist;
-    sa.shist = ctx->scr.shist;
-    sa.out_base = ctx->scr.out_base;
-    sa.tensor_counts = out->tensor_counts;
-    if (gd::launch_sample(sa, base != nullptr, st) != hipSuccess) return GD_ERR_HIP;
-
-    return run_after_bracket(ctx, grad, base, residual, per, ppm, false, quant, k_total, out, st);
+    return gd::compress_exact(ctx, grad, base, residual, drop_ratio, mode == GD_PER_TENSOR, quant, k_total, out,
+                              static_cast<hipStream_t>(stream));
 }
 
 gd_status gd_compress_pull(gd_ctx* ctx, const float* params, float* copy, double drop_ratio, gd_threshold mode,

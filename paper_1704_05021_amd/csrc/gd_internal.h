@@ -6,6 +6,7 @@
 
 #include <vector>
 
+#include "gd.h"
 #include "gd_device.hpp"
 
 namespace gd {
@@ -65,6 +66,18 @@ struct ColumnTables {
     uint32_t* ccnt = nullptr;     // [2 * groups] positive and negative counts
     uint32_t groups = 0;
 };
+
+}  // namespace gd
+
+struct gd_ctx;
+
+namespace gd {
+
+// The launch sequence of one exact-threshold compression (sample, bracket,
+// dense pass, candidate passes, quantisation) on the tables and scratch ctx
+// points to, after the caller's argument checks; k_total is the output size.
+gd_status compress_exact(gd_ctx* ctx, const float* grad, const float* base, float* residual, double drop_ratio,
+                         bool per, gd_quant quant, uint64_t k_total, const gd_sparse* out, hipStream_t st);
 
 }  // namespace gd
 

@@ -46,6 +46,7 @@ EXPORTS = [
     "gd_profile_read",
     "gd_debug_force_bracket",
     "gd_debug_state",
+    "gd_compress_static",
 ]
 
 
@@ -110,6 +111,8 @@ def _lib() -> ctypes.CDLL:
     lib.gd_debug_force_bracket.restype = i32
     lib.gd_debug_state.argtypes = [vp, vp, u32, vp]
     lib.gd_debug_state.restype = i32
+    lib.gd_compress_static.argtypes = [vp, u32, vp, vp, vp, dbl, i32, i32, ctypes.POINTER(_Sparse), vp]
+    lib.gd_compress_static.restype = i32
     _LIB = lib
     return lib
 
@@ -390,3 +393,36 @@ def apply_sparse(params: torch.Tensor, idx: List[torch.Tensor], val: List[torch.
                                 _stream_handle(stream))
     if st != 0:
         raise GDError(st, "gd_apply_sparse")
+
+
+STATIC_MAX_ELEMENTS = 1 << 21
+STATIC_MAX_TENSORS = 64
+
+
+def compress_static(offsets: Sequence[int], grad: torch.Tensor, residual: torch.Tensor, out: SparseOut,
+                    drop_ratio: float = 0.99, per_tensor: bool = False, quant=False,
+                    base: Optional[torch.Tensor] = None, stream: Optional[torch.cuda.Stream] = None) -> SparseOut:
+    """gd_compress_static: gd_compress without a context and without any allocation, for layouts of at
+    most STATIC_MAX_TENSORS tensors and STATIC_MAX_ELEMENTS elements.  ``out`` must be preallocated (for
+    example by ``Compressor.alloc_out`` of the same layout); its ``k`` is set to the kept count."""
+    n = int(offsets[-1])
+    _check_f32(grad, "grad", n)
+    _check_f32(residual, "residual", n)
+    if base is not None:
+        _check_f32(base, "base", n)
+    off = (ctypes.c_uint64 * len(offsets))(*[int(o) for o in offsets])
+    sp = _Sparse(out.idx.data_ptr(), out.val.data_ptr(),
+                 out.sign_bits.data_ptr() if (quant and out.sign_bits is not None) else None,
+                 out.means.data_ptr() if (quant and out.means is not None) else None,
+                 out.tensor_counts.data_ptr(), out.idx.numel())
+    st = _lib().gd_compress_static(off, len(offsets) - 1, grad.data_ptr(),
+                                   None if base is None else base.data_ptr(), residual.data_ptr(),
+                                   float(drop_ratio), GD_PER_TENSOR if per_tensor else GD_GLOBAL, int(quant),
+                                   ctypes.byref(sp), _stream_handle(stream))
+    if st != 0:
+        raise GDError(st, "gd_compress_static")
+    if per_tensor:
+        out.k = sum(keep_count(int(offsets[t + 1]) - int(offsets[t]), drop_ratio) for t in range(len(offsets) - 1))
+    else:
+        out.k = keep_count(n, drop_ratio)
+    return out

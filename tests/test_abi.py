@@ -88,3 +88,17 @@ def test_create_refuses_layouts_past_uint32_indices(gd):
     for bad in ((3, 10), (0, 10, 5)):
         offs = (ctypes.c_uint64 * len(bad))(*bad)
         assert lib.gd_create(ctypes.byref(h), offs, len(bad) - 1) == 2, bad
+
+
+def test_static_entry_point_source_allocates_nothing():
+    """gd_compress_static's file names no allocating or memset call, and host code reaches the scratch array
+    only through the address hipGetSymbolAddress gives for the device."""
+    src = open(os.path.join(ROOT, "paper_1704_05021_amd", "csrc", "gd_static.hip")).read()
+    code = re.sub(r"//[^\n]*", "", src)
+    for banned in ("hipMalloc", "hipFree", "hipMemset", "hipHostMalloc", "malloc(", " new ", "std::vector",
+                   "torch"):
+        assert banned not in code, banned
+    assert "static __device__ __align__(256)" in code
+    assert code.count("HIP_SYMBOL(scratch)") == 1 and "hipGetSymbolAddress" in code
+    # the array's name appears only in its definition and in the symbol lookup
+    assert len(re.findall(r"\bscratch\b(?!_)", code)) == 2
