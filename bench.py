@@ -172,6 +172,23 @@ def time_calls(torch, step, first, count, scrub=None):
     return [a.elapsed_time(b) for a, b in ev]
 
 
+def written_elements(torch, step, first, count, residual):
+    """Elements per call in the 16-byte vectors of the residual that a call changes (the dense pass stores
+    only those), averaged over ``count`` calls after the timed ones."""
+    n = residual.numel()
+    n4 = n - n % 4
+    total = 0
+    for i in range(count):
+        before = residual.clone()
+        step(first + i)
+        torch.cuda.synchronize()
+        a, b = before.view(torch.int32), residual.view(torch.int32)
+        total += 4 * int((a[:n4].view(-1, 4) != b[:n4].view(-1, 4)).any(dim=1).sum())
+        total += int((a[n4:] != b[n4:]).sum())
+        del before
+    return total / count
+
+
 def pct(xs, q):
     """q-th percentile (0..100) of xs by linear interpolation."""
     ys = sorted(xs)
@@ -327,9 +344,12 @@ def main_shard(args, torch, np, gd, wl):
     warm = time_calls(torch, step, args.warmup + args.steps, args.steps)
     sec = statistics.median(cold) / 1e3
     dense_avg_s = dense_ms / 1e3 / max(dense_n, 1)
-    dense_bytes = 8 if use_copy else 16  # params and copy read; or params, base and residual read, residual written
-    achieved = dense_bytes * N / dense_avg_s / 1e9
-    model_bytes = 16 * entries + dense_bytes * N + 8 * k
+    # params and copy read; or params, base and residual read and the changed residual vectors written
+    written = 0 if use_copy else written_elements(torch, step, args.warmup + 2 * args.steps, 4, pull_res)
+    per_elem = 8 if use_copy else 16
+    dense_alg = (8 * N) if use_copy else (12 * N + 4 * written)
+    achieved = dense_alg / dense_avg_s / 1e9
+    model_bytes = 16 * entries + per_elem * N + 8 * k
     line = {
         "metric": METRIC,
         "value": round(N / sec / 1e9, 3),
@@ -362,7 +382,7 @@ def main_shard(args, torch, np, gd, wl):
             "threshold": "global",
             "drop": drop,
             "pull": "from the last pulled copy" if use_copy else "delta with a carried residual",
-            "byte_model": f"16 B/push entry + {dense_bytes} B/element + 8 B/kept element",
+            "byte_model": f"16 B/push entry + {per_elem} B/element + 8 B/kept element",
         },
         "roofline": {
             "kernel": "k_dense<2>" if use_copy else "k_dense<1>",
@@ -372,6 +392,10 @@ def main_shard(args, torch, np, gd, wl):
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": None,
+            "algorithmic_bytes": round(dense_alg),
+            "bytes_rule": "8 B/element read (params, copy)" if use_copy else
+                          "12 B/element read (params, base, residual) + 4 B/element of the 16-byte residual "
+                          "vectors the call changes",
             "dense_us": round(dense_avg_s * 1e6, 2),
             "dense_launches": dense_n,
             "dense_timed_every": DENSE_TIMING_EVERY,
@@ -531,13 +555,15 @@ def main():
     dense_ms, dense_n = comp.profile_read()
     comp.profile_enable(0)
     warm = time_calls(torch, step, args.warmup + args.steps, args.steps)
+    written = written_elements(torch, step, args.warmup + 2 * args.steps, len(grads), residual)
 
     sec = statistics.median(cold) / 1e3
     value = N / sec / 1e9
     k = kept_now()  # the sampled mode's count varies: the last timed step's
     model_bytes = 12 * N + 8 * k
     dense_avg_s = dense_ms / 1e3 / max(dense_n, 1)
-    achieved = 12 * N / dense_avg_s / 1e9
+    dense_bytes = 8 * N + 4 * written  # grad and residual read, the changed residual vectors written
+    achieved = dense_bytes / dense_avg_s / 1e9
     line = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -581,6 +607,10 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": None if sampled else measured_traffic(w.name),
+            "algorithmic_bytes": round(dense_bytes),
+            "bytes_rule": "8 B/element read (grad, residual) + 4 B/element of the 16-byte residual vectors "
+                          "the call changes",
+            "written_fraction": round(written / N, 4),
             "dense_us": round(dense_avg_s * 1e6, 2),
             "dense_launches": dense_n,
             "dense_timed_every": DENSE_TIMING_EVERY,

@@ -4,7 +4,9 @@
 // (together with the later passes) keep the largest |acc|, leaving the rest
 // as the new residual.  This kernel is the only one that streams the whole
 // gradient: per element it reads grad (and, for a pull, the last pulled
-// copy) and the residual, writes the residual back, and appends the few
+// copy) and the residual, writes the residual back where it changes (a
+// 16-byte vector whose four values keep their bits is not stored: a zero
+// gradient leaves acc equal to the residual), and appends the few
 // elements whose key reaches the sampled bracket (key >= lo) to per-unit
 // slots in ascending index order.  Elements with key >= hi are almost
 // surely kept, so their residual is written as +0 now; the emit pass fixes
@@ -117,12 +119,20 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
         ov[q] = (valid && key >= hi[q]) ? 0.0f : acc[q];
     }
     if (!NORES) {
+        // Only what changes is written back.  Where the gradient is zero (the
+        // rows of an embedding that no word of the batch touched) acc equals
+        // the residual bit for bit and nothing is stored: such rows cost
+        // their 8 bytes of reads, not 12.  The test is on bit patterns, so
+        // -0 and +0 count as different.
         if (whole) {
-            __builtin_nontemporal_store(ov, reinterpret_cast<f4*>(a.res) + (e0 >> 2));
+            bool same = true;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) same = same && __float_as_uint(ov[q]) == __float_as_uint(r[q]);
+            if (!same) __builtin_nontemporal_store(ov, reinterpret_cast<f4*>(a.res) + (e0 >> 2));
         } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                if (e0 + q < uend) a.res[e0 + q] = ov[q];
+                if (e0 + q < uend && __float_as_uint(ov[q]) != __float_as_uint(r[q])) a.res[e0 + q] = ov[q];
         }
     }
     // ordered compaction over the unit: waves in order, lanes in order, then
