@@ -182,13 +182,12 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
 // in one load.  Words: tensor | miss << 31, the non-empty unit ne holding
 // the tile's first candidate, its compact candidates [p0, p1), the
 // segment's first tile, the segment's k, and the tensor's tiles [first, end).
+// t0, t1: the tensor's tiles; c0, c1: its compact candidates; miss: whether
+// its segment missed; k: the segment's keep count.
 __device__ __forceinline__ void mark_tiles(const CandArgs& a, uint32_t t, uint32_t base, uint32_t p, uint32_t q,
-                                           uint32_t ne) {
-    const uint32_t t0 = a.tile_base[t], t1 = a.tile_base[t + 1];
-    const uint32_t s = a.per_tensor ? t : 0u;
-    const uint32_t miss = a.seg[s].miss != 0 ? 0x80000000u : 0u;
-    const uint32_t k = keep_of(a.seg_off[s + 1] - a.seg_off[s], a.keep_ppm);
-    const uint32_t c0 = a.ten_cbase[t], c1 = a.ten_cbase[t + 1];
+                                           uint32_t ne, uint32_t t0, uint32_t t1, uint32_t c0, uint32_t c1,
+                                           bool missed, uint32_t k) {
+    const uint32_t miss = missed ? 0x80000000u : 0u;
     // (64-bit positions: a tile start past 2^32 must end the loop, not wrap)
     for (uint32_t j = p > base ? (p - base + kTile - 1) / kTile : 0u; (uint64_t)base + (uint64_t)j * kTile < q; ++j) {
         const uint32_t p0 = c0 + j * kTile, p1 = p0 + kTile < c1 ? p0 + kTile : c1;
@@ -198,36 +197,40 @@ __device__ __forceinline__ void mark_tiles(const CandArgs& a, uint32_t t, uint32
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
-    const uint32_t u = blockIdx.x * kBlock + threadIdx.x;
-    const bool have = u < a.num_units;
-    uint32_t raw = 0, cnt = 0, info = 0;
+// The per-unit part of the layout: the unit's offsets, its place in the list
+// of non-empty units, the tiles starting in it, and for missed segments the
+// residual restored.  TAB gives the per-tensor and per-segment tables: global
+// memory written by k_scan_final, or the block's own copy in LDS.
+template <typename TAB>
+__device__ __forceinline__ void layout_unit(const CandArgs& a, const TAB& tab, uint32_t u, bool have, uint32_t raw,
+                                            uint32_t cnt, uint32_t ne) {
     bool restore = false;
     if (have) {
-        raw = a.loc[u] + a.boff[u / kScanUnits];
-        cnt = a.cnt[u];
-        const uint32_t ne = a.neloc[u] + a.beoff[u / kScanUnits];
         if (cnt) {
             a.ne_unit[ne] = u;
             a.ne_off[ne] = raw;
         }
-        info = a.unit_info[u];
+        const uint32_t info = a.unit_info[u];
         const uint32_t ustart = u * kUnitLen, uend = a.N - ustart > kUnitLen ? ustart + kUnitLen : a.N;
         // every tensor overlapping the unit (one, unless it holds a boundary)
         for (uint32_t t = info & 0x7FFFFFFFu; t < a.T && a.tensor_off[t] < uend; ++t) {
             const uint32_t ta = a.tensor_off[t], tb = a.tensor_off[t + 1];
             if (tb <= ustart || tb == ta) continue;
             const uint32_t s = a.per_tensor ? t : 0u;
-            if (a.seg[s].miss) {
+            const bool missed = tab.miss(s);
+            const uint32_t k = keep_of(a.seg_off[s + 1] - a.seg_off[s], a.keep_ppm);
+            const uint32_t t0 = tab.tile_base(t), t1 = tab.tile_base(t + 1);
+            const uint32_t c0 = tab.ten_cbase(t), c1 = tab.ten_cbase(t + 1);
+            if (missed) {
                 // direct tiles start at element offsets ta + j * kTile
                 const uint32_t lo_e = ta > ustart ? ta : ustart, hi_e = tb < uend ? tb : uend;
-                mark_tiles(a, t, ta, lo_e, hi_e, ne);
+                mark_tiles(a, t, ta, lo_e, hi_e, ne, t0, t1, c0, c1, true, k);
                 // nothing to restore after a pull from the copy, or where no key reached hi
                 restore = restore || (cnt > 0 && a.res != nullptr && a.seg[s].hi != kNoKey);
             } else {
-                const uint32_t rb = a.raw_tbase[t], re = a.raw_tbase[t + 1];
+                const uint32_t rb = tab.raw_tbase(t), re = tab.raw_tbase(t + 1);
                 const uint32_t p = raw > rb ? raw : rb, q = raw + cnt < re ? raw + cnt : re;
-                if (p < q) mark_tiles(a, t, rb, p, q, ne);
+                if (p < q) mark_tiles(a, t, rb, p, q, ne, t0, t1, c0, c1, false, k);
             }
         }
     }
@@ -250,9 +253,174 @@ __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
                 }
                 s = lo;
             }
-            if (a.seg[s].miss && (e.y & 0x7FFFFFFFu) >= a.seg[s].hi) a.res[e.x] = __uint_as_float(e.y);
+            if (tab.miss(s) && (e.y & 0x7FFFFFFFu) >= a.seg[s].hi) a.res[e.x] = __uint_as_float(e.y);
         }
     }
+}
+
+// Tables as k_scan_final wrote them.
+struct GlobalTables {
+    const CandArgs& a;
+    __device__ bool miss(uint32_t s) const { return a.seg[s].miss != 0; }
+    __device__ uint32_t tile_base(uint32_t t) const { return a.tile_base[t]; }
+    __device__ uint32_t ten_cbase(uint32_t t) const { return a.ten_cbase[t]; }
+    __device__ uint32_t raw_tbase(uint32_t t) const { return a.raw_tbase[t]; }
+};
+
+__global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
+    const uint32_t u = blockIdx.x * kBlock + threadIdx.x;
+    const bool have = u < a.num_units;
+    uint32_t raw = 0, cnt = 0, ne = 0;
+    if (have) {
+        raw = a.loc[u] + a.boff[u / kScanUnits];
+        cnt = a.cnt[u];
+        ne = a.neloc[u] + a.beoff[u / kScanUnits];
+    }
+    layout_unit(a, GlobalTables{a}, u, have, raw, cnt, ne);
+}
+
+// k_scan_final and k_layout in one kernel, for layouts of at most
+// kFusedMaxT tensors and kFusedMaxG scan blocks.  Every block derives the
+// block offsets, the per-tensor and per-segment tables from the scan blocks'
+// totals (a few hundred words, read from the cache) into its LDS, and uses
+// its own copy; block 0 also stores them for the passes that follow.  This
+// costs each block a short prologue and saves a kernel boundary.
+constexpr uint32_t kFusedMaxT = 256;
+constexpr uint32_t kFusedMaxG = 1024;
+
+struct LdsTables {
+    const uint32_t* rtb;  // [T + 1]
+    const uint32_t* tcb;  // [T + 1]
+    const uint32_t* ttb;  // [T + 1]
+    const uint32_t* smiss;  // [S]
+    __device__ bool miss(uint32_t s) const { return smiss[s] != 0; }
+    __device__ uint32_t tile_base(uint32_t t) const { return ttb[t]; }
+    __device__ uint32_t ten_cbase(uint32_t t) const { return tcb[t]; }
+    __device__ uint32_t raw_tbase(uint32_t t) const { return rtb[t]; }
+};
+
+__global__ __launch_bounds__(kBlock) void k_layout_fused(CandArgs a, uint32_t nblocks) {
+    __shared__ uint32_t lds[kBlock / kWave + 1];
+    __shared__ uint32_t goff[kFusedMaxG], geoff[kFusedMaxG];
+    __shared__ uint32_t rtb[kFusedMaxT + 1], tcb[kFusedMaxT + 1], ttb[kFusedMaxT + 1], smiss[kFusedMaxT];
+    __shared__ uint32_t any_miss, any_zero;
+    const int tid = threadIdx.x;
+    const bool lead = blockIdx.x == 0;  // stores the tables for the later passes
+    if (tid == 0) {
+        any_miss = 0;
+        any_zero = 0;
+    }
+    // 1. offsets of the scan blocks
+    uint32_t carry = 0, necarry = 0;
+    for (uint32_t b0 = 0; b0 < nblocks; b0 += kBlock) {
+        const uint32_t b = b0 + tid;
+        const uint32_t t = b < nblocks ? a.btot[b] : 0u;
+        const uint32_t te = b < nblocks ? a.betot[b] : 0u;
+        uint32_t tot, netot;
+        const uint32_t e = block_excl_scan<kBlock>(t, lds, &tot);
+        const uint32_t ne = block_excl_scan<kBlock>(te, lds, &netot);
+        if (b < nblocks) {
+            goff[b] = carry + e;
+            geoff[b] = necarry + ne;
+            if (lead) a.boff[b] = carry + e;
+        }
+        carry += tot;
+        necarry += netot;
+    }
+    const uint32_t grand = carry;
+    __syncthreads();
+    // 2. first candidate of each tensor in dense-pass order
+    for (uint32_t t = tid; t <= a.T; t += kBlock) {
+        const uint32_t x = a.tensor_off[t];
+        uint32_t r = grand;
+        if (x < a.N) {
+            const uint32_t u = x / kUnitLen;
+            r = a.loc[u] + goff[u / kScanUnits] + ((x % kUnitLen) ? a.split[t] : 0u);
+        }
+        rtb[t] = r;
+        if (lead) a.raw_tbase[t] = r;
+    }
+    __syncthreads();
+    // 3. per segment: candidates, bracket miss, zero mode (as k_scan_final)
+    const uint32_t S = a.per_tensor ? a.T : 1u;
+    for (uint32_t s = tid; s < S; s += kBlock) {
+        const uint32_t n = a.seg_off[s + 1] - a.seg_off[s];
+        const uint32_t k = keep_of(n, a.keep_ppm);
+        const uint32_t cnt = a.per_tensor ? rtb[s + 1] - rtb[s] : grand;
+        const uint32_t short_of_k = (!a.sampled && k > 0 && cnt < k) ? 1u : 0u;
+        const uint32_t zero =
+            (short_of_k && a.zfill && a.seg[s].lo == 1u && (a.seg[s].hi == kNoKey || a.res == nullptr)) ? 1u : 0u;
+        const uint32_t miss = short_of_k && !zero;
+        smiss[s] = miss;
+        if (lead) {
+            a.seg[s].clo = cnt;
+            a.seg[s].miss = miss;
+            a.seg[s].zero = zero;
+        }
+        if (miss) atomicOr(&any_miss, 1u);
+        if (zero) atomicOr(&any_zero, 1u);
+    }
+    __syncthreads();
+    // 4. per tensor: first compact candidate and first tile
+    {
+        const uint32_t t = tid;  // T <= kFusedMaxT <= kBlock: one round
+        uint32_t cc = 0, tiles = 0;
+        if (t < a.T) {
+            const uint32_t s = a.per_tensor ? t : 0u;
+            cc = smiss[s] ? a.tensor_off[t + 1] - a.tensor_off[t] : rtb[t + 1] - rtb[t];
+            tiles = (uint32_t)(((uint64_t)cc + kTile - 1) / kTile);
+        }
+        uint32_t ctot, ttot;
+        const uint32_t ce = block_excl_scan<kBlock>(cc, lds, &ctot);
+        const uint32_t te = block_excl_scan<kBlock>(tiles, lds, &ttot);
+        if (t < a.T) {
+            tcb[t] = ce;
+            ttb[t] = te;
+        }
+        if (t == 0) {
+            tcb[a.T] = ctot;
+            ttb[a.T] = ttot;
+        }
+        if (lead) {
+            if (t < a.T) {
+                a.ten_cbase[t] = ce;
+                a.tile_base[t] = te;
+            }
+            for (uint32_t i = tid; i < ttot / kGroupTiles + 1; i += kBlock) {
+                a.grp_gt[i] = 0;
+                a.grp_eq[i] = 0;
+            }
+            if (t == 0) {
+                a.ten_cbase[a.T] = ctot;
+                a.tile_base[a.T] = ttot;
+                a.num_ne[0] = necarry;
+                a.ne_off[necarry] = grand;
+            }
+        }
+    }
+    if (lead && a.sampled) {
+        // every candidate is sent: segment s starts after the candidates of the segments before it
+        const uint32_t s = tid;
+        const uint32_t c = s < S ? (a.per_tensor ? rtb[s + 1] - rtb[s] : grand) : 0u;
+        uint32_t tot;
+        const uint32_t e = block_excl_scan<kBlock>(c, lds, &tot);
+        if (s < S) a.out_base[s] = e;
+    }
+    __syncthreads();
+    if (lead && tid == 0) {
+        a.flags[0] = any_miss;
+        a.flags[1] = any_zero;
+    }
+    // 5. this block's units
+    const uint32_t u = blockIdx.x * kBlock + tid;
+    const bool have = u < a.num_units;
+    uint32_t raw = 0, cnt = 0, ne = 0;
+    if (have) {
+        raw = a.loc[u] + goff[u / kScanUnits];
+        cnt = a.cnt[u];
+        ne = a.neloc[u] + geoff[u / kScanUnits];
+    }
+    layout_unit(a, LdsTables{rtb, tcb, ttb, smiss}, u, have, raw, cnt, ne);
 }
 
 hipError_t launch_layout(const CandArgs& a, hipStream_t st) {
@@ -264,8 +432,12 @@ hipError_t launch_layout(const CandArgs& a, hipStream_t st) {
     }
     const uint32_t sb = (a.num_units + kScanUnits - 1) / kScanUnits;
     hipLaunchKernelGGL(k_scan, dim3(sb), dim3(kScanThreads), 0, st, a);
-    hipLaunchKernelGGL(k_scan_final, dim3(1), dim3(kScanThreads), 0, st, a, sb);
-    hipLaunchKernelGGL(k_layout, dim3((a.num_units + kBlock - 1) / kBlock), dim3(kBlock), 0, st, a);
+    if (a.T <= kFusedMaxT && sb <= kFusedMaxG) {
+        hipLaunchKernelGGL(k_layout_fused, dim3((a.num_units + kBlock - 1) / kBlock), dim3(kBlock), 0, st, a, sb);
+    } else {
+        hipLaunchKernelGGL(k_scan_final, dim3(1), dim3(kScanThreads), 0, st, a, sb);
+        hipLaunchKernelGGL(k_layout, dim3((a.num_units + kBlock - 1) / kBlock), dim3(kBlock), 0, st, a);
+    }
     return hipGetLastError();
 }
 
