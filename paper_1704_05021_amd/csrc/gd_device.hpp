@@ -101,7 +101,9 @@ struct SegState {
     uint32_t thr;   // the threshold key T (kNoKey when nothing is kept)
     uint32_t need;  // entries with key == T to keep, lowest index first
     uint32_t zero;  // 1 when fewer than k keys are nonzero and all of them are candidates: T = 0
-    uint32_t pad[5];
+    uint32_t runs;  // kept between calls: 1 when the last sample's units counted like independent
+                    // draws, so the next call samples one run of 16 neighbours per unit
+    uint32_t pad[4];
 };
 
 __device__ __forceinline__ uint32_t key_of(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }

@@ -46,6 +46,10 @@ __device__ __forceinline__ float acc_of(float g, float b, float r) {
     return g + r;
 }
 
+// Dispersion index (variance over mean of the per-unit counts) below which a
+// segment's sample counts as independent draws.
+constexpr double kRunsMaxDispersion = 1.5;
+
 __device__ __forceinline__ uint32_t key16_of(uint32_t key) {
     const uint32_t k = key >> kK16Shift;
     return k < kNoKey16 ? k : kNoKey16 - 1;  // the top NaN keys share one value
@@ -101,6 +105,10 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
 #pragma unroll
     for (int q = 0; q < kUnit; ++q) k16[q] = kNoKey16;
     const bool nores = a.res == nullptr;  // a pull from the last pulled copy has no residual
+    // The previous call on this segment found its units' counts no more spread
+    // than independent draws: neighbours carry independent information, so one
+    // run of 16 (two lines) serves as well as four spread groups (eight lines).
+    const bool runs = a.seg[s].runs != 0;
     if (j < U) {
         // stratum j: 16-element blocks [lo_j, hi_j) of the segment's aligned grid
         const uint32_t lo_j = (uint32_t)(((uint64_t)j * n16) / U);
@@ -128,6 +136,35 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
 #pragma unroll
                 for (int q = 0; q < kUnit; ++q) {
                     const uint32_t e = s0 + q;
+                    if (e >= seg_a && e < seg_b)
+                        k16[q] = key16_of(key_of(acc_of<BASE>(a.grad[e], BASE ? a.base[e] : 0.0f, nores ? 0.0f : a.res[e])));
+                }
+            }
+        } else if (runs) {
+            // one aligned run of 16 neighbours (one 64-byte line per array) at a
+            // fixed hash position in the stratum
+            const uint32_t h = mix32(j * 0x9E3779B9u ^ (s + 1u) * 0x85EBCA6Bu);
+            const uint32_t r0 = ((seg_a >> 4) + lo_j + h % (hi_j - lo_j)) * kUnit;
+            if (r0 >= seg_a && r0 < seg_b && seg_b - r0 >= (uint32_t)kUnit) {
+                const f4* g4 = reinterpret_cast<const f4*>(a.grad + r0);
+                const f4* r4 = reinterpret_cast<const f4*>(nores ? a.grad + r0 : a.res + r0);
+                const f4* b4 = reinterpret_cast<const f4*>(BASE ? a.base + r0 : a.grad + r0);
+                f4 g[4], r[4], b[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    g[q] = g4[q];
+                    r[q] = nores ? f4{0.f, 0.f, 0.f, 0.f} : r4[q];
+                    b[q] = BASE ? b4[q] : g[q];
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        k16[4 * q + c] = key16_of(key_of(acc_of<BASE>(g[q][c], b[q][c], r[q][c])));
+            } else {
+#pragma unroll
+                for (int q = 0; q < kUnit; ++q) {
+                    const uint32_t e = r0 + q;
                     if (e >= seg_a && e < seg_b)
                         k16[q] = key16_of(key_of(acc_of<BASE>(a.grad[e], BASE ? a.base[e] : 0.0f, nores ? 0.0f : a.res[e])));
                 }
@@ -337,6 +374,10 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
                 const double mean = (double)sums[2] / U;
                 const double var = fmax((double)sums[3] / U - mean * mean, 0.0);
                 const double disp = mean > 0.0 ? var / mean : 1.0;
+                // whether the next call may sample runs of neighbours: the
+                // counts spread no more than independent draws (index about 1),
+                // whichever way this sample was drawn
+                if (tid == 0 && mean > 0.0) a.seg[s].runs = disp < kRunsMaxDispersion ? 1u : 0u;
                 const double sd = sqrt(q * fmax(1.0, disp));
                 const double fl = ceil(q + 5.0 * sd + 4.0);
                 if (fl > (double)mnz) {
