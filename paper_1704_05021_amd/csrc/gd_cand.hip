@@ -127,6 +127,8 @@ __device__ __forceinline__ void block_flush(const CandArgs& a, uint32_t* lh, con
 
 constexpr int kRows = kTile / kWave;  // rows of 64 candidates in a tile
 constexpr uint32_t kWin = kTile;      // non-empty units held in the gather window
+constexpr int kWinRows = (kWin + kWave) / kWave;  // rows of 64 window entries (kWin + 1 of them)
+constexpr int kWinHeadRows = 3;                   // rows loaded first
 
 // A tile of kTile candidates lies in at most kTile consecutive non-empty
 // units, so a window of kTile non-empty units starting at the unit that
@@ -157,10 +159,12 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
         }
         TileView v;
         tile_setup(a, tile, v);
+        // compact position -> source position (element, or dense-pass offset)
+        const uint32_t shift = reinterpret_cast<const uint4*>(a.tile_desc + (size_t)tile * kTileDescWords)[2].x;
         uint32_t ix[kRows], vb[kRows];
         if (v.miss) {
             // every element of the tensor is a candidate; acc is in the residual
-            const uint32_t e_base = a.tensor_off[v.t] - a.ten_cbase[v.t];
+            const uint32_t e_base = shift;
 #pragma unroll
             for (int r = 0; r < kRows; ++r) {
                 const uint32_t pl = v.p0 + r * kWave + lane;
@@ -172,36 +176,52 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
             }
         } else {
             // compact position p <-> dense-pass offset p + shift
-            const uint32_t shift = a.raw_tbase[v.t] - a.ten_cbase[v.t];
             const uint32_t j0 = v.ne0;
             const uint32_t nne = a.num_ne[0];
+            const uint32_t cnt = v.p1 - v.p0, r0 = v.p0 + shift, last = r0 + (cnt - 1);
+            // The window runs from the unit holding the tile's first candidate
+            // to the first unit that starts after its last one, W entries on
+            // (W <= kWin: every unit before it holds a candidate of the tile).
+            // The first kWinHead entries nearly always reach it; the others are
+            // loaded only when they do not.
+            uint32_t W = kWin;
             {
-                constexpr int NW = (kWin + kWave) / kWave;
-                uint32_t xo[NW], xu[NW];
+                auto load_rows = [&](int i0, int i1) {
+                    uint32_t xo[kWinRows], xu[kWinRows];
 #pragma unroll
-                for (int i = 0; i < NW; ++i) {
-                    const uint32_t j = i * kWave + lane;
-                    const bool in = j < kWin && j0 + j < nne;
-                    // unconditional loads at clamped positions (j0 < nne here), so
-                    // that all of them are in flight together
-                    const uint32_t jo = j0 + j <= nne ? j0 + j : nne, ju = in ? j0 + j : j0;
-                    const uint32_t o = a.ne_off[jo], u = a.ne_unit[ju];
-                    xo[i] = (j <= kWin && j0 + j <= nne) ? o : kNoKey;
-                    xu[i] = in ? u : 0u;
-                }
+                    for (int i = 0; i < kWinRows; ++i) {
+                        if (i < i0 || i >= i1) continue;
+                        const uint32_t j = i * kWave + lane;
+                        const bool in = j < kWin && j0 + j < nne;
+                        // unconditional loads at clamped positions (j0 < nne here), so
+                        // that all of them are in flight together
+                        const uint32_t jo = j0 + j <= nne ? j0 + j : nne, ju = in ? j0 + j : j0;
+                        const uint32_t o = a.ne_off[jo], u = a.ne_unit[ju];
+                        xo[i] = (j <= kWin && j0 + j <= nne) ? o : kNoKey;
+                        xu[i] = in ? u : 0u;
+                    }
+                    uint32_t found = kNoKey;
 #pragma unroll
-                for (int i = 0; i < NW; ++i) {
-                    const uint32_t j = i * kWave + lane;
-                    if (j <= kWin) wo[j] = xo[i];
-                    if (j < kWin) wu[j] = xu[i];
-                }
+                    for (int i = 0; i < kWinRows; ++i) {
+                        if (i < i0 || i >= i1) continue;
+                        const uint32_t j = i * kWave + lane;
+                        if (j <= kWin) wo[j] = xo[i];
+                        if (j < kWin) wu[j] = xu[i];
+                        const uint64_t m = ballot(j <= kWin && xo[i] > last);
+                        if (m && found == kNoKey) found = (uint32_t)(i * kWave + __ffsll((unsigned long long)m) - 1);
+                    }
+                    return found;
+                };
+                const uint32_t w0 = load_rows(0, kWinHeadRows);
+                if (w0 != kNoKey) W = w0;
+                else load_rows(kWinHeadRows, kWinRows);
                 wave_lds_sync();
             }
             // merge path: lane L maps the kRows consecutive candidates starting
             // at kRows * L to slot indices (one search, then a forward walk)
-            const uint32_t q0 = kRows * lane, cnt = v.p1 - v.p0, r0 = v.p0 + shift;
+            const uint32_t q0 = kRows * lane;
             if (q0 < cnt) {
-                uint32_t lo = 0, hi = kWin;
+                uint32_t lo = 0, hi = W;  // wo[0] <= every position of the tile < wo[W]
                 const uint32_t rp0 = r0 + q0;
                 while (hi - lo > 1) {
                     const uint32_t mid = (lo + hi) >> 1;

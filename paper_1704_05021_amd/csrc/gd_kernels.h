@@ -67,7 +67,7 @@ struct DenseArgs {
 };
 
 constexpr uint32_t kTile = 1024;        // candidates per tile of the candidate passes
-constexpr uint32_t kTileDescWords = 8;  // words of a tile descriptor (two 16-byte loads)
+constexpr uint32_t kTileDescWords = 12;  // words of a tile descriptor (three 16-byte loads)
 constexpr uint32_t kTileBlocks = 512;   // most blocks a candidate pass launches (4 waves each)
 // A segment of more than kBigSegTiles tiles also keeps per-group sums of its
 // tiles' counts (groups of kGroupTiles consecutive tiles), so that a tile's

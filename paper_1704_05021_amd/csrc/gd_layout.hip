@@ -181,19 +181,25 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_final(CandArgs a, uint32_
 // descriptor, so that the candidate passes find all they need about a tile
 // in one load.  Words: tensor | miss << 31, the non-empty unit ne holding
 // the tile's first candidate, its compact candidates [p0, p1), the
-// segment's first tile, the segment's k, and the tensor's tiles [first, end).
+// segment's first tile, the segment's k, and the tensor's tiles [first, end),
+// then the shift from a compact position to the tile's source position (its
+// dense-pass position, or for a missed tensor its element index).
 // t0, t1: the tensor's tiles; c0, c1: its compact candidates; miss: whether
 // its segment missed; k: the segment's keep count.
 __device__ __forceinline__ void mark_tiles(const CandArgs& a, uint32_t t, uint32_t base, uint32_t p, uint32_t q,
                                            uint32_t ne, uint32_t t0, uint32_t t1, uint32_t c0, uint32_t c1,
                                            bool missed, uint32_t k) {
     const uint32_t miss = missed ? 0x80000000u : 0u;
+    // base is the tensor's first source position: its first element (missed)
+    // or its first candidate in dense-pass order
+    const uint32_t shift = base - c0;
     // (64-bit positions: a tile start past 2^32 must end the loop, not wrap)
     for (uint32_t j = p > base ? (p - base + kTile - 1) / kTile : 0u; (uint64_t)base + (uint64_t)j * kTile < q; ++j) {
         const uint32_t p0 = c0 + j * kTile, p1 = p0 + kTile < c1 ? p0 + kTile : c1;
         uint4* d = reinterpret_cast<uint4*>(a.tile_desc + (size_t)(t0 + j) * kTileDescWords);
         d[0] = make_uint4(t | miss, ne, p0, p1);
         d[1] = make_uint4(a.per_tensor ? t0 : 0u, k, t0, t1);
+        d[2] = make_uint4(shift, 0u, 0u, 0u);
     }
 }
 

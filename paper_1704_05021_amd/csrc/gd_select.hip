@@ -271,6 +271,32 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
     __shared__ uint32_t sums[4];
     uint32_t n16, U;
     sample_units(seg_a, seg_b, n16, U);
+    const bool selecting = k > 0 && k < n;
+    // thread tid holds sample units tid + j * kBracketThreads, 16 keys each;
+    // their loads are issued first, so that they overlap the histogram's
+    uint32_t kw[kBracketUnits][kUnit / 2];
+    {
+        const uint32_t kb = selecting ? a.skey_base[s] : 0u;
+#pragma unroll
+        for (int j = 0; j < kBracketUnits; ++j) {
+            const uint32_t u = tid + j * kBracketThreads;
+            if (selecting && u < U) {
+                const uint4* src = reinterpret_cast<const uint4*>(a.skeys + kb + (size_t)kUnit * u);
+                const uint4 x0 = src[0], x1 = src[1];
+                kw[j][0] = x0.x;
+                kw[j][1] = x0.y;
+                kw[j][2] = x0.z;
+                kw[j][3] = x0.w;
+                kw[j][4] = x1.x;
+                kw[j][5] = x1.y;
+                kw[j][6] = x1.z;
+                kw[j][7] = x1.w;
+            } else {
+#pragma unroll
+                for (int i = 0; i < kUnit / 2; ++i) kw[j][i] = 0xFFFFFFFFu;
+            }
+        }
+    }
     // the sample's digit histogram and counts, cleared for the next call
     {
         uint32_t* sh = a.shist + (size_t)s * kSHistWords;
@@ -286,27 +312,6 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
     } else if (k >= n) {
         lo = hi = 0;
     } else {
-        // thread tid holds sample units tid + j * kBracketThreads, 16 keys each
-        uint32_t kw[kBracketUnits][kUnit / 2];
-#pragma unroll
-        for (int j = 0; j < kBracketUnits; ++j) {
-            const uint32_t u = tid + j * kBracketThreads;
-            if (u < U) {
-                const uint4* src = reinterpret_cast<const uint4*>(a.skeys + a.skey_base[s] + (size_t)kUnit * u);
-                const uint4 x0 = src[0], x1 = src[1];
-                kw[j][0] = x0.x;
-                kw[j][1] = x0.y;
-                kw[j][2] = x0.z;
-                kw[j][3] = x0.w;
-                kw[j][4] = x1.x;
-                kw[j][5] = x1.y;
-                kw[j][6] = x1.z;
-                kw[j][7] = x1.w;
-            } else {
-#pragma unroll
-                for (int i = 0; i < kUnit / 2; ++i) kw[j][i] = 0xFFFFFFFFu;
-            }
-        }
         const uint32_t m = sums[0], mnz = sums[0] - sums[1];
         const bool full = m >= n;  // every element sampled: exact ranks
         const double q = full ? (double)k : (double)k * (double)m / (double)n;
