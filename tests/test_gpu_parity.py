@@ -347,3 +347,23 @@ def test_empty_layout():
     s = comp.compress_sampled(e, e, 0.99, per_tensor=True, capacity=4, quant=gd.GD_QUANT_THRESHOLD)
     torch.cuda.synchronize()
     assert out.tensor_counts[:2].cpu().tolist() == [0, 0] and s.tensor_counts[:2].cpu().tolist() == [0, 0]
+
+
+def test_apply_unaligned_parameters():
+    """A parameter buffer that is not 16-byte aligned (a view one float in) is updated exactly like an
+    aligned one: results equal the oracle's bit for bit.  With validate=True the binding refuses a push
+    whose indices are not ascending."""
+    s = wl.server_shard(n=100_001, clients=3, nnz=4_000, dup_frac=0.1, seed=21)
+    want = oracle.apply_sparse(s.params, s.idx, s.val, 1.0)
+    buf = torch.zeros(s.params.size + 1, device="cuda")
+    buf[1:] = torch.from_numpy(s.params).cuda()
+    p = buf[1:]
+    assert p.data_ptr() % 16 != 0
+    gd.apply_sparse(p, [torch.from_numpy(a.view(np.int32)).cuda() for a in s.idx],
+                    [torch.from_numpy(a).cuda() for a in s.val], 1.0, validate=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(p.cpu().numpy()), bits(want))
+    with pytest.raises(gd.GDError) as e:  # a push out of order is refused when asked to check
+        bad = torch.from_numpy(s.idx[0][::-1].copy().view(np.int32)).cuda()
+        gd.apply_sparse(p, [bad], [torch.from_numpy(s.val[0]).cuda()], 1.0, validate=True)
+    assert e.value.status == 1
