@@ -226,7 +226,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
 // histogram of the low 6 bits among keys with that digit.  Called by the
 // whole block; hB is cleared here.
 __device__ uint32_t pick16(const uint32_t* hA, uint32_t* hB, uint32_t* par, uint32_t r,
-                           const uint32_t (&kw)[kBracketUnits][kUnit / 2]) {
+                           const uint32_t (&kw)[kBracketUnits][kUnit / 2], uint32_t units) {
     const int tid = threadIdx.x;
     if (tid < kSNB1) hB[tid] = 0;
     if (tid < kWave) {
@@ -243,6 +243,7 @@ __device__ uint32_t pick16(const uint32_t* hA, uint32_t* hB, uint32_t* par, uint
     for (int j = 0; j < kBracketUnits; ++j)
 #pragma unroll
         for (int i = 0; i < kUnit; ++i) {
+            if (j * kBracketThreads + (tid & ~(kWave - 1)) >= (int)units) continue;  // no unit in this wave
             const uint32_t key = (kw[j][i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
             lds_hist_add(hB, key & (kSNB1 - 1), key != kNoKey16 && key != 0 && (key >> kS0Shift) == dq);
         }
@@ -337,17 +338,26 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
             for (int i = tid; i < kBracketWin * kSNB1; i += kBracketThreads) hW[i] = 0;
             __syncthreads();
             const uint32_t dq = par[0], rf = par[1], floor16 = dq << kS0Shift;
+            // The window is digits dq - kBracketWin + 1 .. dq, key16 values
+            // [wbase, floor16 + kSNB1), zero keys left out: row r of hW holds
+            // digit dq - kBracketWin + 1 + r.  Each key costs a subtraction and a
+            // compare for the window and for the unit count (kNoKey16, a missing
+            // key, falls outside both).
+            const uint32_t wbase = dq >= (uint32_t)(kBracketWin - 1) ? (dq - (kBracketWin - 1)) << kS0Shift : 0u;
+            const uint32_t wlo = wbase ? wbase : 1u, wspan = floor16 + kSNB1 - wlo;
+            uint32_t* const hwin = hW + (wlo - wbase);
+            const uint32_t cspan = kNoKey16 - floor16;
             uint32_t s1 = 0, s2 = 0;  // this thread's units: sum of counts and of squared counts
 #pragma unroll
             for (int j = 0; j < kBracketUnits; ++j) {
+                if (j * kBracketThreads + (tid & ~(kWave - 1)) >= (int)U) continue;  // no unit in this wave
                 uint32_t c = 0;
 #pragma unroll
                 for (int i = 0; i < kUnit; ++i) {
                     const uint32_t key = (kw[j][i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
-                    const bool valid = key != kNoKey16;
-                    const uint32_t dd = dq - (key >> kS0Shift);  // wraps above dq
-                    lds_hist_add(hW, dd * kSNB1 + (key & (kSNB1 - 1)), valid && key != 0 && dd < (uint32_t)kBracketWin);
-                    c += valid && key >= floor16;
+                    const uint32_t t = key - wlo;
+                    if (t < wspan) atomicAdd(&hwin[t], 1u);
+                    c += key - floor16 < cspan;
                 }
                 s1 += c;
                 s2 += c * c;
@@ -364,7 +374,7 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
             // P: the fine bin of rank rf within digit dq
             if (tid < kWave) {
                 uint32_t f, ab;
-                wave_pick<kSNB1>(hW, rf, f, ab);
+                wave_pick<kSNB1>(hW + (kBracketWin - 1) * kSNB1, rf, f, ab);
                 if (tid == 0) par[2] = floor16 | f;
             }
             __syncthreads();
@@ -395,7 +405,7 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
                         wave_pick<kNB0>(hA, (uint32_t)fl, dl, abl);
                         if (dq - dl < (uint32_t)kBracketWin) {
                             uint32_t f, ab;
-                            wave_pick<kSNB1>(hW + (dq - dl) * kSNB1, (uint32_t)fl - abl, f, ab);
+                            wave_pick<kSNB1>(hW + (kBracketWin - 1 - (dq - dl)) * kSNB1, (uint32_t)fl - abl, f, ab);
                             lo16 = (dl << kS0Shift) | f;
                         }
                         if (tid == 0) par[3] = lo16;
@@ -403,7 +413,7 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
                     __syncthreads();
                     uint32_t lo16 = par[3];
                     __syncthreads();
-                    if (lo16 == kNoKey) lo16 = pick16(hA, hB, par, (uint32_t)fl, kw);
+                    if (lo16 == kNoKey) lo16 = pick16(hA, hB, par, (uint32_t)fl, kw, U);
                     lo = lo16 << kK16Shift;
                     if (lo == 0) lo = 1;
                 }
