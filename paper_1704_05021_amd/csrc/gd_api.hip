@@ -171,6 +171,7 @@ gd_status run_after_bracket(gd_ctx* ctx, const float* grad, const float* base, f
     ca.ten_cbase = ctx->scr.ten_cbase;
     ca.tile_base = ctx->scr.tile_base;
     ca.tile_desc = ctx->scr.tile_desc;
+    ca.max_tiles = ctx->max_tiles;
     ca.flags = ctx->scr.flags;
     ca.tile_gt = ctx->scr.tile_gt;
     ca.tile_eq = ctx->scr.tile_eq;

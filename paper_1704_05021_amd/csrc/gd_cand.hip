@@ -62,9 +62,32 @@ struct TileView {
     bool miss;
 };
 
-__device__ __forceinline__ void tile_setup(const CandArgs& a, uint32_t tile, TileView& v) {
-    const uint4* d = reinterpret_cast<const uint4*>(a.tile_desc + (size_t)tile * kTileDescWords);
-    const uint4 d0 = d[0], d1 = d[1];
+// A tile descriptor as loaded: three 16-byte words.
+struct TileDesc {
+    uint4 d0, d1, d2;
+};
+
+// The descriptor of tile `tile`, or of tile 0 past the buffer.  The buffer
+// holds a descriptor for every tile there can be, so a wave loads its next
+// tile's descriptor before it knows whether that tile exists (the tile count
+// is written by the layout pass): the descriptor then arrives with the
+// count, or during the previous tile's work, instead of one round trip
+// after it.  A descriptor past the count is stale and never used.
+// The loads are relaxed atomics of wave scope (as in load_early), so that the
+// compiler does not sink them past the test of the tile count.
+__device__ __forceinline__ TileDesc load_desc(const CandArgs& a, uint32_t tile) {
+    const uint64_t* d = reinterpret_cast<const uint64_t*>(a.tile_desc + (size_t)(tile < a.max_tiles ? tile : 0u) * kTileDescWords);
+    uint64_t x[6];
+#pragma unroll
+    for (int i = 0; i < 6; ++i) x[i] = __hip_atomic_load(d + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+    auto lo = [](uint64_t v) { return (uint32_t)v; };
+    auto hi = [](uint64_t v) { return (uint32_t)(v >> 32); };
+    return TileDesc{make_uint4(lo(x[0]), hi(x[0]), lo(x[1]), hi(x[1])), make_uint4(lo(x[2]), hi(x[2]), lo(x[3]), hi(x[3])),
+                    make_uint4(lo(x[4]), hi(x[4]), lo(x[5]), hi(x[5]))};
+}
+
+__device__ __forceinline__ void tile_setup(const CandArgs& a, const TileDesc& td, TileView& v) {
+    const uint4 d0 = td.d0, d1 = td.d1;
     v.t = d0.x & 0x7FFFFFFFu;
     v.miss = (d0.x >> 31) != 0;
     v.ne0 = d0.y;
@@ -149,18 +172,24 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
     wave_lds_sync();
     // this block's copy of the digit-0 histogram (global threshold only)
     const int h0_at = kHistH0 + (a.per_tensor ? 0 : (int)(blockIdx.x % kH0Copies) * kNB0);
+    const uint32_t stride = gridDim.x * kWavesPerBlock;
+    TileDesc next = load_desc(a, blockIdx.x * kWavesPerBlock + w);
     const uint32_t ntiles = a.tile_base[a.T];
-    for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += gridDim.x * kWavesPerBlock) {
+    // non-empty units, loaded with the tile count (an atomic load stays here)
+    const uint32_t nne = load_early(a.num_ne);
+    for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += stride) {
         const uint32_t tile = t0 + w;
+        const TileDesc td = next;
+        if (t0 + stride < ntiles) next = load_desc(a, tile + stride);
         if (tile >= ntiles) {
             if (lane == 0) wseg[w] = kNoKey;
             if (!a.sampled) block_flush<kNB0>(a, lh, wseg, h0_at);  // block-uniform
             continue;
         }
         TileView v;
-        tile_setup(a, tile, v);
+        tile_setup(a, td, v);
         // compact position -> source position (element, or dense-pass offset)
-        const uint32_t shift = reinterpret_cast<const uint4*>(a.tile_desc + (size_t)tile * kTileDescWords)[2].x;
+        const uint32_t shift = td.d2.x;
         uint32_t ix[kRows], vb[kRows];
         if (v.miss) {
             // every element of the tensor is a candidate; acc is in the residual
@@ -177,14 +206,22 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
         } else {
             // compact position p <-> dense-pass offset p + shift
             const uint32_t j0 = v.ne0;
-            const uint32_t nne = a.num_ne[0];
             const uint32_t cnt = v.p1 - v.p0, r0 = v.p0 + shift, last = r0 + (cnt - 1);
             // The window runs from the unit holding the tile's first candidate
             // to the first unit that starts after its last one, W entries on
             // (W <= kWin: every unit before it holds a candidate of the tile).
             // The first kWinHead entries nearly always reach it; the others are
-            // loaded only when they do not.
-            uint32_t W = kWin;
+            // loaded only when they do not.  Window unit j >= 1 with j < W
+            // starts inside the tile: it marks its first position in the slot
+            // map (cleared first), which the map's max-scan then extends over
+            // the unit's other positions.
+            const uint32_t q0 = kRows * lane;
+            {
+                uint4* z = reinterpret_cast<uint4*>(sm + q0);
+#pragma unroll
+                for (int i = 0; i < kRows / 4; ++i) z[i] = make_uint4(0u, 0u, 0u, 0u);
+                wave_lds_sync();
+            }
             {
                 auto load_rows = [&](int i0, int i1) {
                     uint32_t xo[kWinRows], xu[kWinRows];
@@ -207,38 +244,42 @@ __device__ __forceinline__ void phase_gather(const CandArgs& a, uint32_t* lds) {
                         const uint32_t j = i * kWave + lane;
                         if (j <= kWin) wo[j] = xo[i];
                         if (j < kWin) wu[j] = xu[i];
+                        if (j >= 1 && xo[i] <= last) sm[xo[i] - r0] = j;  // 1 <= xo - r0 < cnt: see above
                         const uint64_t m = ballot(j <= kWin && xo[i] > last);
                         if (m && found == kNoKey) found = (uint32_t)(i * kWave + __ffsll((unsigned long long)m) - 1);
                     }
                     return found;
                 };
-                const uint32_t w0 = load_rows(0, kWinHeadRows);
-                if (w0 != kNoKey) W = w0;
-                else load_rows(kWinHeadRows, kWinRows);
+                if (load_rows(0, kWinHeadRows) == kNoKey) load_rows(kWinHeadRows, kWinRows);
                 wave_lds_sync();
             }
-            // merge path: lane L maps the kRows consecutive candidates starting
-            // at kRows * L to slot indices (one search, then a forward walk)
-            const uint32_t q0 = kRows * lane;
-            if (q0 < cnt) {
-                uint32_t lo = 0, hi = W;  // wo[0] <= every position of the tile < wo[W]
-                const uint32_t rp0 = r0 + q0;
-                while (hi - lo > 1) {
-                    const uint32_t mid = (lo + hi) >> 1;
-                    if (wo[mid] <= rp0) lo = mid;
-                    else hi = mid;
+            // Lane L maps positions q0 .. q0 + kRows - 1: the window unit of a
+            // position is the last mark at or before it (unit 0 when none), a
+            // running maximum in the lane, then over the lanes below.  The
+            // position's slot is the unit's slot base plus its offset there.
+            {
+                const uint4* hv = reinterpret_cast<const uint4*>(sm + q0);
+                uint32_t m[kRows];
+#pragma unroll
+                for (int i = 0; i < kRows / 4; ++i) {
+                    const uint4 h = hv[i];
+                    m[4 * i + 0] = h.x;
+                    m[4 * i + 1] = h.y;
+                    m[4 * i + 2] = h.z;
+                    m[4 * i + 3] = h.w;
                 }
-                uint32_t j = lo, cur = wo[j], nxt = wo[j + 1], ub = wu[j] * kUnitLen;
-                for (int i = 0; i < kRows && q0 + i < cnt; ++i) {
-                    const uint32_t rp = rp0 + i;
-                    while (rp >= nxt) {
-                        ++j;
-                        cur = nxt;
-                        nxt = wo[j + 1];
-                        ub = wu[j] * kUnitLen;
-                    }
-                    sm[q0 + i] = ub + (rp - cur);
+#pragma unroll
+                for (int i = 1; i < kRows; ++i) m[i] = max(m[i], m[i - 1]);
+                const uint32_t below = lane_below_value(wave_incl_max(m[kRows - 1]));
+                uint32_t o[kRows];
+#pragma unroll
+                for (int i = 0; i < kRows; ++i) {
+                    const uint32_t j = max(m[i], below);
+                    o[i] = wu[j] * kUnitLen + (r0 + q0 + i - wo[j]);
                 }
+                uint4* dv = reinterpret_cast<uint4*>(sm + q0);
+#pragma unroll
+                for (int i = 0; i < kRows / 4; ++i) dv[i] = make_uint4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
             }
             wave_lds_sync();
             // rows: slot loads and stores are coalesced
@@ -349,14 +390,18 @@ __device__ __forceinline__ void phase_radix(const CandArgs& a, uint32_t* lds) {
         for (int i = lane; i < Lv::kNB / 2; i += kWave) hw[i] = 0;
         wave_lds_sync();
     }
+    const uint32_t stride = gridDim.x * kWavesPerBlock;
+    TileDesc next = load_desc(a, blockIdx.x * kWavesPerBlock + w);
     const uint32_t ntiles = a.tile_base[a.T];
     uint32_t cached_s = kNoKey, prefix = 0, rank = 0;
     uint32_t run_s = kNoKey, run_d = 0, run_c = 0;  // digit 2: this wave's run of one bin
-    for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += gridDim.x * kWavesPerBlock) {
+    for (uint32_t t0 = blockIdx.x * kWavesPerBlock; t0 < ntiles; t0 += stride) {
         const uint32_t tile = t0 + w;
+        const TileDesc td = next;
+        if (t0 + stride < ntiles) next = load_desc(a, tile + stride);
         if (tile < ntiles) {
             TileView v;
-            tile_setup(a, tile, v);
+            tile_setup(a, td, v);
             uint32_t key[kRows];
             load_keys(a, v, key);
             if (v.s != cached_s) {
@@ -508,11 +553,15 @@ __device__ __forceinline__ void zero_fill(const CandArgs& a, const EmitArgs& o) 
 
 __device__ __forceinline__ void phase_count(const CandArgs& a, const EmitArgs& o) {
     const int w = threadIdx.x >> 6, lane = lane_id();
+    const uint32_t stride = gridDim.x * kWavesPerBlock;
+    TileDesc next = load_desc(a, blockIdx.x * kWavesPerBlock + w);
     const uint32_t ntiles = a.tile_base[a.T];
     uint32_t cached_s = kNoKey, thr = kNoKey, need = 0;
-    for (uint32_t tile = blockIdx.x * kWavesPerBlock + w; tile < ntiles; tile += gridDim.x * kWavesPerBlock) {
+    for (uint32_t tile = blockIdx.x * kWavesPerBlock + w; tile < ntiles; tile += stride) {
+        const TileDesc td = next;
+        if (tile + stride < ntiles) next = load_desc(a, tile + stride);
         TileView v;
-        tile_setup(a, tile, v);
+        tile_setup(a, td, v);
         uint32_t key[kRows];
         load_keys(a, v, key);
         if (v.s != cached_s) {
@@ -594,10 +643,14 @@ __device__ __forceinline__ void sum_tiles(const CandArgs& a, bool grouped, uint3
 template <bool QUANT>
 __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o) {
     const int w = threadIdx.x >> 6, lane = lane_id();
+    const uint32_t stride = gridDim.x * kWavesPerBlock;
+    TileDesc next = load_desc(a, blockIdx.x * kWavesPerBlock + w);
     const uint32_t ntiles = a.tile_base[a.T];
-    for (uint32_t tile = blockIdx.x * kWavesPerBlock + w; tile < ntiles; tile += gridDim.x * kWavesPerBlock) {
+    for (uint32_t tile = blockIdx.x * kWavesPerBlock + w; tile < ntiles; tile += stride) {
+        const TileDesc td = next;
+        if (tile + stride < ntiles) next = load_desc(a, tile + stride);
         TileView v;
-        tile_setup(a, tile, v);
+        tile_setup(a, td, v);
         uint32_t ix[kRows], vb[kRows];
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
@@ -720,7 +773,7 @@ __device__ __forceinline__ void phase_emit(const CandArgs& a, const EmitArgs& o)
 }
 
 __global__ __launch_bounds__(kBlock) void k_gather(CandArgs a) {
-    __shared__ uint32_t lds[kGatherLds];
+    __shared__ __align__(16) uint32_t lds[kGatherLds];
     phase_gather(a, lds);
 }
 

@@ -16,10 +16,9 @@
 // A unit is the 1024 elements [1024u, 1024u + 1024) of the flat gradient,
 // one block of 256 threads with one 16-byte vector per thread, so every
 // load is aligned and issued before any table lookup.  The streamed arrays
-// are loaded and the residual stored as non-temporal: the residual's load and
-// store both streaming keeps its lines from filling the L2 with dirty data
-// (either alone gains nothing; both take the 137M-element pass from about
-// 288 to 254 us).  The block compacts
+// are loaded as non-temporal, and the residual's changed vectors stored with
+// device scope (see unit_rsrc), so that the residual does not fill the L2
+// with dirty lines while the pass streams.  The block compacts
 // the unit's candidates into slots [1024u, ...) and stores their count.  A unit
 // that holds a tensor boundary also records, for each tensor starting inside
 // it, how many of its candidates precede that start (the candidate layout
@@ -30,6 +29,21 @@
 #include "gd_kernels.h"
 
 namespace gd {
+
+// The residual's stores go out as buffer stores with device scope (SC1) and
+// no other cache bits.  While the pass streams its reads, such stores disturb
+// the read stream less than non-temporal or plain stores: with 8% of the
+// residual's 2000-byte rows rewritten at scattered places, a 137M-element
+// read-and-store stream measured 186 us against 198 (non-temporal) and
+// 192 us (plain); the pass itself 185.5 against 187.4 us at the NMT-shaped
+// layout and 36.5 against 39.0 at the 20M-element MLP.  The resource covers
+// one unit's bytes, so the 32-bit offsets never wrap and a store past the
+// unit would be dropped by the hardware.
+constexpr int kStoreDeviceScope = 16;  // cache-policy operand: SC1
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t unit_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
 
 template <bool BASE>
 __device__ __forceinline__ float acc_of(float g, float b, float r) {
@@ -128,7 +142,11 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
             bool same = true;
 #pragma unroll
             for (int q = 0; q < 4; ++q) same = same && __float_as_uint(ov[q]) == __float_as_uint(r[q]);
-            if (!same) __builtin_nontemporal_store(ov, reinterpret_cast<f4*>(a.res) + (e0 >> 2));
+            if (!same) {
+                typedef unsigned u4 __attribute__((ext_vector_type(4)));
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, ov), unit_rsrc(a.res + ustart, 4 * (uend - ustart)),
+                                                       16u * tid, 0, kStoreDeviceScope);
+            }
         } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q)
@@ -149,6 +167,9 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense(DenseArgs a) {
         total += qc[i];
     }
     if ((m0 | m1 | m2 | m3) != 0) {
+        // plain stores: gather reads the lists next, partly from the cache
+        // (device-scope or non-temporal stores here cost the pass 8 us at the
+        // NMT-shaped layout)
         uint32_t pos = base + lanes_below(m0) + lanes_below(m1) + lanes_below(m2) + lanes_below(m3);
         uint2* out = a.slots + ustart;
 #pragma unroll

@@ -108,6 +108,14 @@ struct SegState {
 
 __device__ __forceinline__ uint32_t key_of(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }
 
+// A load that stays where it is written.  A relaxed atomic of wave scope is a
+// plain load to the hardware, but the compiler neither sinks it past a branch
+// nor drops it, so loads that do not depend on one another can all be put in
+// flight at the start of a kernel instead of one round trip after another.
+__device__ __forceinline__ uint32_t load_early(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
 // Number of set bits of m in lanes below this one.
@@ -162,6 +170,23 @@ __device__ __forceinline__ uint32_t wave_min(uint32_t v) {
     v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)v, 0x142, 0xA, 0xF, false));  // row_bcast:15
     v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(kId, (int)v, 0x143, 0xC, 0xF, false));  // row_bcast:31
     return lane_value(v, kWave - 1);
+}
+
+// Maximum over this lane and the lanes below it (0 for none), by the same
+// DPP steps as wave_incl_scan.  Every lane must be active.
+__device__ __forceinline__ uint32_t wave_incl_max(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false));  // row_shr:1
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false));  // row_shr:2
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false));  // row_shr:4
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false));  // row_shr:8
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false));  // row_bcast:15
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));  // row_bcast:31
+    return v;
+}
+
+// v of the lane below (0 in lane 0): DPP wave_shr:1.  Every lane must be active.
+__device__ __forceinline__ uint32_t lane_below_value(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x138, 0xF, 0xF, false);
 }
 
 __device__ __forceinline__ double wave_sum(double v) {

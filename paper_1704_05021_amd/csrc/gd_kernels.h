@@ -105,7 +105,8 @@ struct CandArgs {
     uint32_t* cand_val;   // [N] their value bits
     uint32_t* ten_cbase;  // [T + 1] first compact candidate of each tensor
     uint32_t* tile_base;  // [T + 1] first tile of each tensor
-    uint32_t* tile_desc;  // [max tiles * kTileDescWords] per tile, written by the layout pass: see TileView
+    uint32_t* tile_desc;  // [max_tiles * kTileDescWords] per tile, written by the layout pass: see TileView
+    uint32_t max_tiles;   // descriptors the buffer holds (every element a candidate)
     uint32_t* tile_gt;    // [max tiles]
     uint32_t* tile_eq;
     uint32_t* grp_gt;     // [max tiles / kGroupTiles + 1] sums of tile_gt per group (segments of many tiles)

@@ -209,14 +209,13 @@ __device__ __forceinline__ void mark_tiles(const CandArgs& a, uint32_t t, uint32
 // memory written by k_scan_final, or the block's own copy in LDS.
 template <typename TAB>
 __device__ __forceinline__ void layout_unit(const CandArgs& a, const TAB& tab, uint32_t u, bool have, uint32_t raw,
-                                            uint32_t cnt, uint32_t ne) {
+                                            uint32_t cnt, uint32_t ne, uint32_t info) {
     bool restore = false;
     if (have) {
         if (cnt) {
             a.ne_unit[ne] = u;
             a.ne_off[ne] = raw;
         }
-        const uint32_t info = a.unit_info[u];
         const uint32_t ustart = u * kUnitLen, uend = a.N - ustart > kUnitLen ? ustart + kUnitLen : a.N;
         // every tensor overlapping the unit (one, unless it holds a boundary)
         for (uint32_t t = info & 0x7FFFFFFFu; t < a.T && a.tensor_off[t] < uend; ++t) {
@@ -276,13 +275,14 @@ struct GlobalTables {
 __global__ __launch_bounds__(kBlock) void k_layout(CandArgs a) {
     const uint32_t u = blockIdx.x * kBlock + threadIdx.x;
     const bool have = u < a.num_units;
-    uint32_t raw = 0, cnt = 0, ne = 0;
+    uint32_t raw = 0, cnt = 0, ne = 0, info = 0;
     if (have) {
         raw = a.loc[u] + a.boff[u / kScanUnits];
         cnt = a.cnt[u];
         ne = a.neloc[u] + a.beoff[u / kScanUnits];
+        info = a.unit_info[u];
     }
-    layout_unit(a, GlobalTables{a}, u, have, raw, cnt, ne);
+    layout_unit(a, GlobalTables{a}, u, have, raw, cnt, ne, info);
 }
 
 // k_scan_final and k_layout in one kernel, for layouts of at most
@@ -312,6 +312,41 @@ __global__ __launch_bounds__(kBlock) void k_layout_fused(CandArgs a, uint32_t nb
     __shared__ uint32_t any_miss, any_zero;
     const int tid = threadIdx.x;
     const bool lead = blockIdx.x == 0;  // stores the tables for the later passes
+    const uint32_t S = a.per_tensor ? a.T : 1u;
+    // 0. Every load that does not depend on the scan, issued first so that
+    // they are in flight together: this thread's unit, the tensor starts (and
+    // behind them the unit counts at those starts), the segment's bracket.
+    const uint32_t u = blockIdx.x * kBlock + tid;
+    const bool have = u < a.num_units;
+    uint32_t uloc = 0, ucnt = 0, uneloc = 0, uinfo = 0;
+    if (have) {
+        uloc = load_early(a.loc + u);
+        ucnt = load_early(a.cnt + u);
+        uneloc = load_early(a.neloc + u);
+        uinfo = load_early(a.unit_info + u);
+    }
+    uint32_t s_n = 0, s_lo = 0, s_hi = 0;
+    if ((uint32_t)tid < S) {
+        s_n = load_early(a.seg_off + tid + 1) - load_early(a.seg_off + tid);
+        s_lo = load_early(&a.seg[tid].lo);
+        s_hi = load_early(&a.seg[tid].hi);
+    }
+    // tensor t = tid + q * kBlock (T <= kFusedMaxT: t <= T needs q <= 1)
+    static_assert(kFusedMaxT <= 2 * kBlock - 1, "two tensor starts per thread");
+    uint32_t tx[2] = {0, 0}, tl[2] = {0, 0}, tsp[2] = {0, 0};
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const uint32_t t = tid + q * kBlock;
+        if (t <= a.T) tx[q] = load_early(a.tensor_off + t);
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const uint32_t t = tid + q * kBlock;
+        if (t <= a.T && tx[q] < a.N) {
+            tl[q] = load_early(a.loc + tx[q] / kUnitLen);
+            if (tx[q] % kUnitLen) tsp[q] = load_early(a.split + t);
+        }
+    }
     if (tid == 0) {
         any_miss = 0;
         any_zero = 0;
@@ -336,26 +371,24 @@ __global__ __launch_bounds__(kBlock) void k_layout_fused(CandArgs a, uint32_t nb
     const uint32_t grand = carry;
     __syncthreads();
     // 2. first candidate of each tensor in dense-pass order
-    for (uint32_t t = tid; t <= a.T; t += kBlock) {
-        const uint32_t x = a.tensor_off[t];
-        uint32_t r = grand;
-        if (x < a.N) {
-            const uint32_t u = x / kUnitLen;
-            r = a.loc[u] + goff[u / kScanUnits] + ((x % kUnitLen) ? a.split[t] : 0u);
-        }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const uint32_t t = tid + q * kBlock;
+        if (t > a.T) continue;
+        const uint32_t x = tx[q];
+        const uint32_t r = x < a.N ? tl[q] + goff[x / kUnitLen / kScanUnits] + tsp[q] : grand;
         rtb[t] = r;
         if (lead) a.raw_tbase[t] = r;
     }
     __syncthreads();
     // 3. per segment: candidates, bracket miss, zero mode (as k_scan_final)
-    const uint32_t S = a.per_tensor ? a.T : 1u;
-    for (uint32_t s = tid; s < S; s += kBlock) {
-        const uint32_t n = a.seg_off[s + 1] - a.seg_off[s];
-        const uint32_t k = keep_of(n, a.keep_ppm);
+    if ((uint32_t)tid < S) {
+        const uint32_t s = tid;
+        const uint32_t k = keep_of(s_n, a.keep_ppm);
         const uint32_t cnt = a.per_tensor ? rtb[s + 1] - rtb[s] : grand;
         const uint32_t short_of_k = (!a.sampled && k > 0 && cnt < k) ? 1u : 0u;
         const uint32_t zero =
-            (short_of_k && a.zfill && a.seg[s].lo == 1u && (a.seg[s].hi == kNoKey || a.res == nullptr)) ? 1u : 0u;
+            (short_of_k && a.zfill && s_lo == 1u && (s_hi == kNoKey || a.res == nullptr)) ? 1u : 0u;
         const uint32_t miss = short_of_k && !zero;
         smiss[s] = miss;
         if (lead) {
@@ -373,7 +406,7 @@ __global__ __launch_bounds__(kBlock) void k_layout_fused(CandArgs a, uint32_t nb
         uint32_t cc = 0, tiles = 0;
         if (t < a.T) {
             const uint32_t s = a.per_tensor ? t : 0u;
-            cc = smiss[s] ? a.tensor_off[t + 1] - a.tensor_off[t] : rtb[t + 1] - rtb[t];
+            cc = smiss[s] ? a.tensor_off[t + 1] - tx[0] : rtb[t + 1] - rtb[t];
             tiles = (uint32_t)(((uint64_t)cc + kTile - 1) / kTile);
         }
         uint32_t ctot, ttot;
@@ -418,15 +451,12 @@ __global__ __launch_bounds__(kBlock) void k_layout_fused(CandArgs a, uint32_t nb
         a.flags[1] = any_zero;
     }
     // 5. this block's units
-    const uint32_t u = blockIdx.x * kBlock + tid;
-    const bool have = u < a.num_units;
-    uint32_t raw = 0, cnt = 0, ne = 0;
+    uint32_t raw = 0, ne = 0;
     if (have) {
-        raw = a.loc[u] + goff[u / kScanUnits];
-        cnt = a.cnt[u];
-        ne = a.neloc[u] + geoff[u / kScanUnits];
+        raw = uloc + goff[u / kScanUnits];
+        ne = uneloc + geoff[u / kScanUnits];
     }
-    layout_unit(a, LdsTables{rtb, tcb, ttb, smiss}, u, have, raw, cnt, ne);
+    layout_unit(a, LdsTables{rtb, tcb, ttb, smiss}, u, have, raw, ucnt, ne, uinfo);
 }
 
 hipError_t launch_layout(const CandArgs& a, hipStream_t st) {

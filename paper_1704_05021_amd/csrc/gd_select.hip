@@ -68,6 +68,11 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
     const uint32_t s = blockIdx.x / kSampleBlocks, bx = blockIdx.x % kSampleBlocks;
     const int tid = threadIdx.x;
     const uint32_t seg_a = a.seg_off[s], seg_b = a.seg_off[s + 1];
+    // The previous call on this segment found its units' counts no more spread
+    // than independent draws: neighbours carry independent information, so one
+    // run of 16 (two lines) serves as well as four spread groups (eight lines).
+    // (Loaded with the segment bounds, not after the clearing below.)
+    const bool runs = load_early(&a.seg[s].runs) != 0;
     __shared__ uint32_t lds[kSampleThreads / kWave + 1];
 
     // Clear this segment's histograms and state for the passes that follow.
@@ -105,10 +110,6 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs a) {
 #pragma unroll
     for (int q = 0; q < kUnit; ++q) k16[q] = kNoKey16;
     const bool nores = a.res == nullptr;  // a pull from the last pulled copy has no residual
-    // The previous call on this segment found its units' counts no more spread
-    // than independent draws: neighbours carry independent information, so one
-    // run of 16 (two lines) serves as well as four spread groups (eight lines).
-    const bool runs = a.seg[s].runs != 0;
     if (j < U) {
         // stratum j: 16-element blocks [lo_j, hi_j) of the segment's aligned grid
         const uint32_t lo_j = (uint32_t)(((uint64_t)j * n16) / U);
@@ -263,6 +264,7 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
     const uint32_t s = blockIdx.x;
     const int tid = threadIdx.x;
     const uint32_t seg_a = a.seg_off[s], seg_b = a.seg_off[s + 1];
+    const uint32_t kb_all = load_early(a.skey_base + s);  // with the bounds, not after them
     const uint32_t n = seg_b - seg_a;
     const uint32_t k = keep_of(n, a.keep_ppm);
     __shared__ uint32_t hA[kNB0];
@@ -277,7 +279,7 @@ __global__ __launch_bounds__(kBracketThreads) void k_bracket(SampleArgs a) {
     // their loads are issued first, so that they overlap the histogram's
     uint32_t kw[kBracketUnits][kUnit / 2];
     {
-        const uint32_t kb = selecting ? a.skey_base[s] : 0u;
+        const uint32_t kb = kb_all;
 #pragma unroll
         for (int j = 0; j < kBracketUnits; ++j) {
             const uint32_t u = tid + j * kBracketThreads;
