@@ -189,10 +189,31 @@ __device__ __forceinline__ uint32_t lane_below_value(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x138, 0xF, 0xF, false);
 }
 
+// v of the DPP source lane, both halves of the double moved with control
+// CTRL in the rows ROW_MASK enables; a lane with no source gets -0.0, the
+// identity of floating-point addition (x + -0.0 is x for every x, zeros too).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double v) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROW_MASK, 0xF, false);
+    const uint32_t hi =
+        (uint32_t)__builtin_amdgcn_update_dpp((int)0x80000000u, (int)(uint32_t)(b >> 32), CTRL, ROW_MASK, 0xF, false);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Sum over the 64 lanes, in every lane: the steps of wave_incl_scan on
+// doubles (a fixed order, so the result is the same on every run), then the
+// last lane's total.  Every lane must be active.
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-    for (int d = kWave / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, kWave);
-    return v;
+    v += dpp_f64<0x111, 0xF>(v);  // row_shr:1
+    v += dpp_f64<0x112, 0xF>(v);  // row_shr:2
+    v += dpp_f64<0x114, 0xF>(v);  // row_shr:4
+    v += dpp_f64<0x118, 0xF>(v);  // row_shr:8
+    v += dpp_f64<0x142, 0xA>(v);  // row_bcast:15, rows 1 and 3
+    v += dpp_f64<0x143, 0xC>(v);  // row_bcast:31, rows 2 and 3
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = lane_value((uint32_t)b, kWave - 1), hi = lane_value((uint32_t)(b >> 32), kWave - 1);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
 // Rank query on a histogram of NB bins (bin = digit value): find the digit
