@@ -40,9 +40,14 @@ namespace gd {
 // one unit's bytes, so the 32-bit offsets never wrap and a store past the
 // unit would be dropped by the hardware.
 constexpr int kStoreDeviceScope = 16;  // cache-policy operand: SC1
+// Fourth word of the resource: data format 32 bits (field value 4 in bits
+// 18..15), the setting for untyped raw buffer access on this architecture.
+constexpr int kRawBufferWord3 = 0x00020000;
 
+// A raw buffer resource over `bytes` bytes from `base` (stride 0: offsets
+// are byte offsets, and the hardware drops accesses at or past `bytes`).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t unit_rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRawBufferWord3);
 }
 
 template <bool BASE>
