@@ -93,6 +93,38 @@ def test_edge_sizes(n):
                        what=f"n={n} drop={drop} debug={debug}")
 
 
+def test_sparse_candidates_wide_windows():
+    """Candidates so sparse that one tile of 1024 spans hundreds of units, up to
+    one candidate per 1024-element unit: gather loads its whole window of
+    non-empty units (past the first 192) and maps every position to the
+    last unit start at or before it."""
+    units = 3000
+    n = 1024 * units
+    rng = np.random.default_rng(11)
+    u = np.arange(units)
+    r = np.zeros(n, np.float32)
+    comp = gd.Compressor([0, n])
+    for noise in (0.0, 1e-6):  # no noise: the spikes are the only nonzero keys, one candidate per unit
+        g = (rng.normal(0, 1, n) * noise).astype(np.float32)
+        g[u * 1024 + (u * 37) % 1024] = (1.0 + u * 1e-4).astype(np.float32)  # one spike per unit
+        for keep in (2900, 1024, 1025, 2048, 4000):
+            drop = 1.0 - keep / n
+            for per in (False, True):
+                check_case(g, r, [0, n], drop, per, False, comp=comp, what=f"spikes noise={noise} keep={keep} per={per}")
+                if noise == 0.0 and keep > units:
+                    # fewer nonzero keys than k: every spike, and nothing else, is a
+                    # candidate (one per unit, so a full tile's window holds 1024
+                    # units), and the zero mode adds the lowest-index zeros
+                    seg = comp.debug_state()[0][0]
+                    assert seg["clo"] == units and seg["miss"] == 0 and seg["zero"] == 1, seg
+    g2 = rng.normal(0, 1, n).astype(np.float32)
+    r2 = (rng.normal(0, 1, n) * (rng.random(n) < 0.3)).astype(np.float32)
+    offsets = [0, n // 3, n]
+    comp2 = gd.Compressor(offsets)
+    for drop, per, quant in ((0.9995, False, False), (0.9995, True, False), (0.999, False, True)):
+        check_case(g2, r2, offsets, drop, per, quant, comp=comp2, what=f"sparse drop={drop} per={per} q={quant}")
+
+
 def test_unaligned_tensor_offsets():
     # tensors whose offsets are not multiples of 4: vectors straddle tensor boundaries
     offsets = [0, 5, 6, 4103, 4103, 9001, 20003, 20010]
