@@ -97,3 +97,28 @@ def test_errors():
     small = comp.alloc_out(0.99, capacity=5)
     with pytest.raises(gd.GDError):
         comp.compress_pull(p, c, 0.99, out=small)
+
+
+def test_random_cases():
+    """Seeded random cases of the pull from the last pulled copy: layouts of 1
+    to 60 tensors, every drop ratio, both scopes, forced bracket modes, and
+    parameters that equal their copy on a random share of entries."""
+    for case in range(40):
+        rng = np.random.default_rng(30_000 + case)
+        T = int(rng.choice([1, 3, 60]))
+        sizes = rng.integers(0, int(rng.choice([300, 30_000, 300_000])), T)
+        offsets = [0] + np.cumsum(sizes).tolist()
+        if offsets[-1] == 0:
+            offsets[-1] = 1
+        N = offsets[-1]
+        copy = rng.normal(0, 0.1, N).astype(np.float32)
+        params = (copy + rng.standard_t(3, N) * 1e-3).astype(np.float32)
+        same = rng.random(N) < rng.random()
+        params[same] = copy[same]
+        drop = float(rng.choice([0.0, 0.5, 0.9, 0.99, 0.999, 1.0]))
+        per = bool(rng.random() < 0.5)
+        debug = int(rng.choice([0, 0, 1, 3, 4]))
+        comp = gd.Compressor(offsets)
+        check_pull(comp, params, copy, offsets, drop, per, debug,
+                   what=f"case {case}: N={N} T={T} drop={drop} per={per} debug={debug}")
+        comp.close()

@@ -264,3 +264,37 @@ def test_quantised_errors():
     out = comp.alloc_out(1.0, capacity=100)  # no sign_bits or means
     with pytest.raises(gd.GDError):
         comp.compress_sampled(g, r, 0.99, quant=gd.GD_QUANT_SIGN_MEAN, out=out, capacity=100)
+
+
+@pytest.mark.parametrize("block", range(2))
+def test_random_cases(block):
+    """Seeded random cases: 1 to 60 tensors, every value family, sample rates
+    from 0.01% to all, short output buffers, pull deltas and 1-bit forms."""
+    for case in range(block * 40, (block + 1) * 40):
+        rng = np.random.default_rng(20_000 + case)
+        T = int(rng.choice([1, 2, 5, 60]))
+        sizes = rng.integers(0, int(rng.choice([200, 20_000, 400_000])), T)
+        offsets = [0] + np.cumsum(sizes).tolist()
+        if offsets[-1] == 0:
+            offsets[-1] = 1
+            sizes[-1] = 1
+        N = offsets[-1]
+        kind = ["gauss", "ties", "heavy"][case % 3]
+        g, r = _values(rng, N, kind), _values(rng, N, "gauss")
+        base = _values(rng, N, "gauss") if rng.random() < 0.2 else None
+        drop = float(rng.choice([0.0, 0.5, 0.9, 0.99, 0.999, 1.0]))
+        per = bool(rng.random() < 0.5)
+        ppm = int(rng.choice([100, 1000, 20_000, 300_000, 1_000_000]))
+        q = int(rng.choice([0, 0, 1, 2, 3, 4]))
+        cols = _divisor_columns(rng, sizes) if q == gd.GD_QUANT_COLUMN_MEAN else None
+        cap = None
+        if rng.random() < 0.25:
+            full = oracle_sampled(g, r, offsets, drop, per, ppm, case, base)
+            cap = int(full.idx.size * rng.uniform(0.0, 0.9))
+        comp = gd.Compressor(offsets)
+        if cols is not None:
+            comp.set_columns(cols)
+        check(g, r, offsets, drop, per, ppm, case, base=base, capacity=cap, comp=comp, quant=q, columns=cols,
+              what=f"case {case}: N={N} T={T} {kind} drop={drop} per={per} ppm={ppm} q={q} cap={cap} "
+                   f"base={base is not None}")
+        comp.close()
