@@ -248,6 +248,22 @@ def test_apply_dense_buckets_and_many_clients():
     _apply_case(100_003, 64, 40, 0.5, seed=12, lr=0.5)
 
 
+def test_apply_random_cases():
+    """Seeded random server applies: shard sizes from a few hundred to millions
+    of parameters (ragged last buckets), 1 to 64 clients, densities from a few
+    entries to most of the shard, shared-index fractions from none to most, and
+    several learning rates."""
+    for case in range(40):
+        rng = np.random.default_rng(40_000 + case)
+        n = int(rng.choice([300, 33_333, 1 << 15, (1 << 15) + 1, 500_000, 3_000_001]))
+        C = int(rng.choice([1, 2, 4, 9, 64]))
+        # every client's fresh indices must fit outside the earlier clients' union
+        nnz = max(1, min(int(n * float(rng.choice([0.0005, 0.01, 0.1, 0.6]))), n // (2 * C)))
+        dup = float(rng.choice([0.0, 0.05, 0.5, 0.95]))
+        lr = float(rng.choice([1.0, 0.5, 1e-3]))
+        _apply_case(n, C, nnz, dup, seed=50_000 + case, lr=lr)
+
+
 def test_apply_skips_out_of_range_and_empty_pushes():
     rng = np.random.default_rng(13)
     n = 40_000
