@@ -230,7 +230,8 @@ gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base,
  *   The result is deterministic when the precondition above holds.  It is not
  *   checked on the device (that would need a host synchronisation): an index
  *   repeated inside one push is applied by two threads that race, and an
- *   unsorted push can have entries skipped.  The Python binding checks it on
+ *   unsorted push can have entries skipped; no memory outside params[0, n)
+ *   is written either way.  The Python binding checks the precondition on
  *   request (apply_sparse(..., validate=True)).
  */
 gd_status gd_apply_sparse(float* params, uint64_t n, uint32_t num_pushes, const uint32_t* const* idx,

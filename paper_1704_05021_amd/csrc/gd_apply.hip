@@ -77,7 +77,7 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
     __shared__ uint32_t sidx[kApplyLds];
     __shared__ float sval[kApplyLds];
     __shared__ uint32_t seen[2][kBucketWords];  // [0]: index pushed at least once, [1]: more than once
-    const int tid = threadIdx.x, w = tid >> 6, lane = lane_id();
+    const int tid = threadIdx.x, w = (int)wave_index(), lane = lane_id();
     const uint32_t b = blockIdx.x;
     const uint32_t i_lo = b << kApplyBucketShift;
     const uint64_t i_hi64 = ((uint64_t)b + 1) << kApplyBucketShift;
@@ -112,10 +112,11 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
             const uint32_t r0 = rng[c][0], cnt = rng[c][1] - r0, o = base[c];
             for (uint32_t q = tid; q < cnt; q += kBlock) {
                 const uint32_t ii = a.idx[c][r0 + q];
-                sidx[o + q] = ii;
-                sval[o + q] = push_val(a, c, r0 + q, ii);
                 const uint32_t off = ii - i_lo, bit = 1u << (off & 31);
-                if (atomicOr(&seen[0][off >> 5], bit) & bit) atomicOr(&seen[1][off >> 5], bit);
+                // an index outside the bucket (a list out of order) is skipped
+                sidx[o + q] = off < i_hi - i_lo ? ii : kNoKey;
+                sval[o + q] = push_val(a, c, r0 + q, ii);
+                if (off < i_hi - i_lo && (atomicOr(&seen[0][off >> 5], bit) & bit)) atomicOr(&seen[1][off >> 5], bit);
             }
         }
         __syncthreads();
@@ -136,7 +137,7 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
             pv[t] = false;
             pi[t] = i_lo;  // a valid parameter index for the unconditional load below
             pstep[t] = 0.0f;
-            if (e < total) {
+            if (e < total && sidx[e] != kNoKey) {
                 uint32_t c = 0;
                 while (base[c + 1] <= e) ++c;  // client of staged entry e
                 const uint32_t i = sidx[e];
@@ -170,6 +171,7 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
         while (base[c + 1] <= e) ++c;  // client of staged entry e
         const uint32_t q = e - base[c];
         const uint32_t i = staged ? sidx[e] : a.idx[c][rng[c][0] + q];
+        if (i - i_lo >= i_hi - i_lo) continue;  // outside the bucket: a list out of order
         bool owner = true;
         for (uint32_t cc = 0; cc < c && owner; ++cc) {
             const uint32_t hit = staged ? find_u32(sidx, base[cc], base[cc + 1], i)

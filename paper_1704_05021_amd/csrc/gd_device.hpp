@@ -118,6 +118,11 @@ __device__ __forceinline__ uint32_t load_early(const uint32_t* p) {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
+// This wave's index in its block, in a scalar register: the compiler then
+// knows it is the same in every lane, so values indexed by it (kernel
+// arguments, table entries) are read with scalar loads.
+__device__ __forceinline__ uint32_t wave_index() { return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave); }
+
 // Number of set bits of m in lanes below this one.
 __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
