@@ -11,8 +11,7 @@
 // few hundred thousand entries, instead of a binary search's twenty), stages
 // those entries in LDS, marking the indices pushed more than once, and then
 // gives every index to the lowest client holding it, which sums all clients'
-// values for it in client order and writes p once.  Each parameter is loaded
-// as soon as its index arrives, before the marking and settling.  The parameter writes of a block stay inside its bucket.
+// values for it in client order and writes p once.  The parameter writes of a block stay inside its bucket.
 // Quantised pushes (indices, sign bits, centre pairs; Section 5.4) are decoded
 // entry by entry where their values are read.
 
@@ -78,7 +77,6 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
     __shared__ uint32_t sidx[kApplyLds];
     __shared__ float sval[kApplyLds];
     __shared__ uint32_t seen[2][kBucketWords];  // [0]: index pushed at least once, [1]: more than once
-    __shared__ const uint32_t* lidx[kMaxPushes];  // the clients' index lists, for lookups by a lane's client
     const int tid = threadIdx.x, w = (int)wave_index(), lane = lane_id();
     const uint32_t b = blockIdx.x;
     const uint32_t i_lo = b << kApplyBucketShift;
@@ -91,7 +89,6 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
     for (uint32_t c = w; c < a.C; c += kWavesPerBlock) {
         const uint32_t pos = half_lower_bound(a.idx[c], 0, a.nnz[c], half ? i_hi : i_lo, g, mask);
         if (g == 0) rng[c][half] = pos;
-        if (lane == 0) lidx[c] = a.idx[c];
     }
     __syncthreads();
     if (tid == 0) {
@@ -107,56 +104,42 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
     if (total == 0) return;
     const bool staged = total <= (uint32_t)kApplyLds;
     // 2. stage the bucket's entries (index, value) of every client, and mark
-    //    the indices pushed more than once.  Thread tid stages entries
-    //    tid + t * kBlock, the ones it settles in step 3, and loads their
-    //    parameters right after their indices, so that those loads are in
-    //    flight while the entries are marked and settled.
-    constexpr int kPer = kApplyLds / kBlock;
-    float pold[kPer];
-    uint32_t ec[kPer];  // client of each of this thread's entries
+    //    the indices pushed more than once
     if (staged) {
         for (uint32_t q = tid; q < 2u * kBucketWords; q += kBlock) (&seen[0][0])[q] = 0;
-        uint32_t ei[kPer];
-#pragma unroll
-        for (int t = 0; t < kPer; ++t) {
-            const uint32_t e = tid + t * kBlock;
-            uint32_t c = 0;
-            if (e < total)
-                while (base[c + 1] <= e) ++c;
-            ec[t] = c;
-            ei[t] = e < total ? lidx[c][rng[c][0] + (e - base[c])] : kNoKey;
-        }
-        float ev[kPer];
-#pragma unroll
-        for (int t = 0; t < kPer; ++t) {
-            const uint32_t e = tid + t * kBlock;
-            const bool in = e < total && ei[t] - i_lo < i_hi - i_lo;  // outside the bucket: a list out of order
-            pold[t] = a.p[in ? ei[t] : i_lo];
-            ev[t] = e < total ? push_val(a, ec[t], rng[ec[t]][0] + (e - base[ec[t]]), ei[t]) : 0.0f;
-            if (!in) ei[t] = kNoKey;
-        }
-        __syncthreads();  // the bitmaps cleared
-#pragma unroll
-        for (int t = 0; t < kPer; ++t) {
-            const uint32_t e = tid + t * kBlock;
-            if (e < total) {
-                sidx[e] = ei[t];
-                sval[e] = ev[t];
-                const uint32_t off = ei[t] - i_lo, bit = 1u << (off & 31);
-                if (ei[t] != kNoKey && (atomicOr(&seen[0][off >> 5], bit) & bit)) atomicOr(&seen[1][off >> 5], bit);
+        __syncthreads();
+        for (uint32_t c = 0; c < a.C; ++c) {
+            const uint32_t r0 = rng[c][0], cnt = rng[c][1] - r0, o = base[c];
+            for (uint32_t q = tid; q < cnt; q += kBlock) {
+                const uint32_t ii = a.idx[c][r0 + q];
+                const uint32_t off = ii - i_lo, bit = 1u << (off & 31);
+                // an index outside the bucket (a list out of order) is skipped
+                sidx[o + q] = off < i_hi - i_lo ? ii : kNoKey;
+                sval[o + q] = push_val(a, c, r0 + q, ii);
+                if (off < i_hi - i_lo && (atomicOr(&seen[0][off >> 5], bit) & bit)) atomicOr(&seen[1][off >> 5], bit);
             }
         }
         __syncthreads();
     }
     // 3. each entry: skip it if a lower client holds the same index, else sum
     //    every client's value for it in client order and update p once (an
-    //    index pushed once needs no search).
+    //    index pushed once needs no search).  When staged, a thread settles all
+    //    its entries first and then reads all its parameters at once, so their
+    //    latencies overlap instead of adding up.
     if (staged) {
+        constexpr int kPer = kApplyLds / kBlock;
+        uint32_t pi[kPer];
+        float pstep[kPer];
+        bool pv[kPer];
 #pragma unroll
         for (int t = 0; t < kPer; ++t) {
             const uint32_t e = tid + t * kBlock;
+            pv[t] = false;
+            pi[t] = i_lo;  // a valid parameter index for the unconditional load below
+            pstep[t] = 0.0f;
             if (e < total && sidx[e] != kNoKey) {
-                const uint32_t c = ec[t];
+                uint32_t c = 0;
+                while (base[c + 1] <= e) ++c;  // client of staged entry e
                 const uint32_t i = sidx[e];
                 const uint32_t off = i - i_lo;
                 const bool once = (seen[1][off >> 5] & (1u << (off & 31))) == 0;
@@ -169,11 +152,18 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
                         const uint32_t hit = find_u32(sidx, base[cc], base[cc + 1], i);
                         if (hit != base[cc + 1]) sum = sum + sval[hit];
                     }
-                    const float step = a.lr * sum;
-                    a.p[i] = pold[t] - step;
+                    pv[t] = true;
+                    pi[t] = i;
+                    pstep[t] = a.lr * sum;
                 }
             }
         }
+        float pold[kPer];
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) pold[t] = a.p[pi[t]];
+#pragma unroll
+        for (int t = 0; t < kPer; ++t)
+            if (pv[t]) a.p[pi[t]] = pold[t] - pstep[t];
         return;
     }
     for (uint32_t e = tid; e < total; e += kBlock) {
