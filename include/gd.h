@@ -227,6 +227,13 @@ gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base,
  *   For every index i that appears in any push: s = sum of the pushed values
  *   at i, added in push order starting from +0.0; params[i] -= lr * s.
  *   num_pushes may be 0 (nothing happens); at most 64 pushes per call.
+ *   Pushes dense enough that most of the shard's 128-byte lines hold an
+ *   update are applied by reading the shard in order; that form first writes
+ *   a table of num_pushes * (ceil(n / 16384) + 1) uint32 (36 KB for four
+ *   pushes to a 37M shard), allocated in stream order from a memory pool the
+ *   library keeps per device (the pool keeps what it has reserved, so
+ *   repeated calls do not go to the driver).  If that allocation fails the
+ *   pushes are applied in the other form; the results are the same.
  *   The result is deterministic when the precondition above holds.  It is not
  *   checked on the device (that would need a host synchronisation): an index
  *   repeated inside one push is applied by two threads that race, and an
@@ -314,6 +321,19 @@ gd_status gd_profile_read(gd_ctx* ctx, double* dense_ms, uint64_t* dense_launche
  * part of their residual.  GD_ERR_ARG for other modes.
  */
 gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode);
+
+/*
+ * Test hook: the form of later gd_apply_sparse and gd_apply_quantised calls
+ * in this process, so that tests can run both forms at any density.  The
+ * results do not change; only the work done does.  form 0: chosen per call
+ * (streaming, which reads the whole shard in order, when params is 16-byte
+ * aligned, the pushes hold between one entry per 64 parameters and 768 per
+ * 16,384, and there are at most 8 of them; else scattered, which reads only
+ * the pushed parameters); 1: scattered; 2: streaming wherever params is
+ * 16-byte aligned.  A process-wide setting: it applies to every device and thread.
+ * GD_ERR_ARG for other forms.
+ */
+gd_status gd_debug_apply_form(int form);
 
 /*
  * Test hook: waits for the device, then copies the per-segment state of the

@@ -568,6 +568,12 @@ gd_status gd_apply_quantised(gd_ctx* ctx, float* params, uint32_t num_pushes, co
     return GD_OK;
 }
 
+gd_status gd_debug_apply_form(int form) {
+    if (form < 0 || form > 2) return GD_ERR_ARG;
+    gd::set_apply_form(form);
+    return GD_OK;
+}
+
 gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode) {
     if (!ctx || mode < 0 || mode > 4) return GD_ERR_ARG;
     ctx->debug_bracket = (uint32_t)mode;

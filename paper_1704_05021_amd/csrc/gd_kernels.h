@@ -179,6 +179,10 @@ struct ApplyArgs {
     uint32_t T;
     const uint32_t* columns;     // [T]
     const uint32_t* colbase;     // [T + 1]
+    // streaming form: first position in each client's list of every chunk
+    // boundary (row c at tab + c * tstride)
+    const uint32_t* tab;
+    uint32_t tstride;
 };
 
 hipError_t launch_sample(const SampleArgs& a, bool has_base, hipStream_t st);
@@ -189,5 +193,7 @@ hipError_t launch_dense(const DenseArgs& a, bool has_base, hipStream_t st, hipEv
 hipError_t launch_candidates(const CandArgs& a, const EmitArgs& o, bool quant, uint32_t max_tiles, hipStream_t st);
 hipError_t launch_quant(const QuantArgs& q, hipStream_t st);
 hipError_t launch_apply(const ApplyArgs& a, uint32_t max_nnz, hipStream_t st);
+// Form of later applies: 0 chosen per call, 1 scattered, 2 streaming wherever the parameters are 16-byte aligned.
+void set_apply_form(int form);
 
 }  // namespace gd

@@ -45,6 +45,7 @@ EXPORTS = [
     "gd_profile_enable",
     "gd_profile_read",
     "gd_debug_force_bracket",
+    "gd_debug_apply_form",
     "gd_debug_state",
     "gd_compress_static",
 ]
@@ -109,6 +110,8 @@ def _lib() -> ctypes.CDLL:
     lib.gd_profile_read.restype = i32
     lib.gd_debug_force_bracket.argtypes = [vp, i32]
     lib.gd_debug_force_bracket.restype = i32
+    lib.gd_debug_apply_form.argtypes = [i32]
+    lib.gd_debug_apply_form.restype = i32
     lib.gd_debug_state.argtypes = [vp, vp, u32, vp]
     lib.gd_debug_state.restype = i32
     lib.gd_compress_static.argtypes = [vp, u32, vp, vp, vp, dbl, i32, i32, ctypes.POINTER(_Sparse), vp]
@@ -393,6 +396,14 @@ def apply_sparse(params: torch.Tensor, idx: List[torch.Tensor], val: List[torch.
                                 _stream_handle(stream))
     if st != 0:
         raise GDError(st, "gd_apply_sparse")
+
+
+def debug_apply_form(form: int) -> None:
+    """gd_debug_apply_form: the form of later applies in this process (0 chosen per call, 1 scattered,
+    2 streaming wherever the parameters are 16-byte aligned).  A test hook; results do not change."""
+    st = _lib().gd_debug_apply_form(int(form))
+    if st != 0:
+        raise GDError(st, "gd_debug_apply_form")
 
 
 STATIC_MAX_ELEMENTS = 1 << 21

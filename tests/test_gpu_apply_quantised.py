@@ -54,7 +54,7 @@ def run_case(offsets, grads, quant, lr, columns=None, per_flags=None, what=""):
 
 
 @pytest.mark.parametrize("quant", [1, 2, 3, 4])
-def test_small_nmt_layout(quant):
+def test_small_nmt_layout(quant, apply_form):
     w = wl.workload("nmt_small_per_tensor")
     offsets = w.layout.offsets.astype(np.int64).tolist()
     grads = [w.grad(s) for s in range(3)]
@@ -62,7 +62,7 @@ def test_small_nmt_layout(quant):
 
 
 @pytest.mark.parametrize("quant", [1, 4])
-def test_random_layout_many_pushes(quant):
+def test_random_layout_many_pushes(quant, apply_form):
     rng = np.random.default_rng(40 + quant)
     sizes = [7000, 1, 0, 33_000, 640]
     offsets = [0] + np.cumsum(sizes).tolist()
@@ -71,7 +71,7 @@ def test_random_layout_many_pushes(quant):
     run_case(offsets, grads, quant, 0.5, columns=columns if quant == 4 else None, what=f"quant={quant}")
 
 
-def test_full_nmt_layout_sign_mean():
+def test_full_nmt_layout_sign_mean(apply_form):
     """Two pushes of the full NMT-shaped layout (1.37M entries each) under a global threshold."""
     w = wl.workload("nmt_85k_global_signmean")
     offsets = w.layout.offsets.astype(np.int64).tolist()

@@ -237,18 +237,18 @@ def _apply_case(n, C, nnz, dup, seed, lr=1.0):
 
 
 @pytest.mark.parametrize("C,dup,lr", [(1, 0.0, 1.0), (2, 0.05, 1.0), (4, 0.05, 1.0), (4, 0.5, 0.25), (7, 0.3, 1.0)])
-def test_apply_small(C, dup, lr):
+def test_apply_small(C, dup, lr, apply_form):
     _apply_case(60_000, C, 1500, dup, seed=C, lr=lr)
 
 
-def test_apply_dense_buckets_and_many_clients():
+def test_apply_dense_buckets_and_many_clients(apply_form):
     # buckets too full for the staged (LDS) path: about 28,000 entries per bucket
     _apply_case(70_000, 4, 15_000, 0.3, seed=11)
     # the most clients one call takes, heavy sharing, a ragged last bucket
     _apply_case(100_003, 64, 40, 0.5, seed=12, lr=0.5)
 
 
-def test_apply_random_cases():
+def test_apply_random_cases(apply_form):
     """Seeded random server applies: shard sizes from a few hundred to millions
     of parameters (ragged last buckets), 1 to 64 clients, densities from a few
     entries to most of the shard, shared-index fractions from none to most, and
@@ -264,7 +264,7 @@ def test_apply_random_cases():
         _apply_case(n, C, nnz, dup, seed=50_000 + case, lr=lr)
 
 
-def test_apply_skips_out_of_range_and_empty_pushes():
+def test_apply_skips_out_of_range_and_empty_pushes(apply_form):
     rng = np.random.default_rng(13)
     n = 40_000
     p0 = rng.normal(0, 0.1, n).astype(np.float32)
@@ -284,7 +284,7 @@ def test_apply_skips_out_of_range_and_empty_pushes():
     assert np.array_equal(bits(p.cpu().numpy()), bits(want))
 
 
-def test_apply_and_pull_full_shard():
+def test_apply_and_pull_full_shard(apply_form):
     cfg = wl.SHARD_FULL
     s, p1 = _apply_case(cfg["n"], cfg["clients"], cfg["nnz"], cfg["dup_frac"], cfg["seed"])
     comp = gd.Compressor([0, cfg["n"]])
@@ -397,7 +397,7 @@ def test_empty_layout():
     assert out.tensor_counts[:2].cpu().tolist() == [0, 0] and s.tensor_counts[:2].cpu().tolist() == [0, 0]
 
 
-def test_apply_unaligned_parameters():
+def test_apply_unaligned_parameters(apply_form):
     """A parameter buffer that is not 16-byte aligned (a view one float in) is updated exactly like an
     aligned one: results equal the oracle's bit for bit.  With validate=True the binding refuses a push
     whose indices are not ascending."""
