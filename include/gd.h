@@ -229,11 +229,14 @@ gd_status gd_compress_sampled(gd_ctx* ctx, const float* grad, const float* base,
  *   num_pushes may be 0 (nothing happens); at most 64 pushes per call.
  *   Pushes dense enough that most of the shard's 128-byte lines hold an
  *   update are applied by reading the shard in order; that form first writes
- *   a table of num_pushes * (ceil(n / 16384) + 1) uint32 (36 KB for four
- *   pushes to a 37M shard), allocated in stream order from a memory pool the
- *   library keeps per device (the pool keeps what it has reserved, so
- *   repeated calls do not go to the driver).  If that allocation fails the
- *   pushes are applied in the other form; the results are the same.
+ *   a table of num_pushes * (ceil(n / 4096) + 1) uint32 (145 KB for four
+ *   pushes to a 37M shard).  The library keeps one such table per device and
+ *   stream (per host thread for the per-thread default stream) and reuses it
+ *   on later calls on that stream; it is allocated with hipMalloc on the
+ *   first call that needs it (or a larger one) and kept until the process
+ *   ends, so make the first call on a stream outside graph capture.  If that
+ *   allocation fails the pushes are applied in the other form; the results
+ *   are the same.
  *   The result is deterministic when the precondition above holds.  It is not
  *   checked on the device (that would need a host synchronisation): an index
  *   repeated inside one push is applied by two threads that race, and an

@@ -23,7 +23,10 @@
 
 #include <algorithm>
 #include <atomic>
+#include <map>
 #include <mutex>
+#include <thread>
+#include <utility>
 
 #include "gd_kernels.h"
 
@@ -211,319 +214,197 @@ __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a) {
 
 // The streaming form, for pushes dense enough that most 128-byte lines of
 // the shard hold an update (the scattered form above then fetches nearly every
-// line anyway, one scattered word at a time).  One block per chunk of
-// kStreamLen consecutive parameters reads the whole chunk in order with
-// 16-byte loads and writes back only the 16-byte vectors an entry touches.
+// line anyway, one scattered word at a time).  One block per tile of
+// kApplyTileLen consecutive parameters reads the tile in order with 16-byte
+// loads, forms the sum of every pushed parameter of the tile in LDS, and
+// writes back only the 16-byte vectors that an entry touches.
 //
-// How fast a chunk streams is set by the bytes a block keeps in flight over
-// its lifetime, so the roles are split between waves.  The loading waves
-// issue the chunk's loads first thing and hold its 64 KB in registers; the
-// list waves read the chunk's range in every client's list from a bounds
-// table (k_apply_bounds, one pass over the lists before this kernel) and
-// stage the chunk's entries in LDS, each wave the clients it handles, marking
-// the parameters pushed at least once and more than once.  The loading waves
-// then copy the vectors that an entry touches (about one in seven at a few
-// percent of indices pushed) into a compact LDS array and leave, so that the
-// per-parameter work is done for the touched vectors only, by the list
-// waves: a parameter pushed once takes p - lr * (0 + value); the sum of one
-// pushed by several clients is formed in client turns between barriers,
-// started from +0 by the first client's entry, and the parameter then takes
-// p - lr * sum.  The list waves store the compact vectors back.  Each
-// parameter is written once, by one thread, with the scattered form's
-// arithmetic, so the two forms agree bit for bit.
-constexpr int kStreamShift = 14;
-constexpr uint32_t kStreamLen = 1u << kStreamShift;                            // parameters per block
-constexpr int kStreamLoadWaves = 4, kStreamListWaves = 4;
-constexpr int kStreamThreads = (kStreamLoadWaves + kStreamListWaves) * kWave;
-constexpr int kStreamLoadThreads = kStreamLoadWaves * kWave;
-constexpr uint32_t kListThreads = kStreamThreads - kStreamLoadThreads;
-constexpr int kStreamLoadShift = 8;                                            // log2 kStreamLoadThreads
-constexpr int kStreamVecs = (int)kStreamLen / 4 / kStreamLoadThreads;         // 16-byte vectors per loading thread
-constexpr int kStreamCap = 1024;                                               // entries of all clients staged per chunk
-constexpr int kStreamWords = (int)kStreamLen / 32;                             // bitmap words per chunk
-constexpr uint16_t kStreamNoOff = 0xFFFFu;                                     // a staged entry outside the chunk
-constexpr int kStreamBatch = 8;                                                // entries per lane loaded at once when staging
-constexpr int kStreamPer = kStreamCap / (int)kListThreads;                     // staged entries per list thread
+// The sums start at +0 and take the clients in turn, between barriers.  No
+// two entries of one client's turn share an index (a push holds an index at
+// most once), so each LDS sum is formed in client order without atomics, as
+// the scattered form forms it, and the parameter then takes p - lr * sum:
+// the two forms agree bit for bit.  The tile's range in every client's list
+// comes from a bounds table (k_apply_bounds, one pass over the lists before
+// this kernel).  Each thread loads kApplyTileEntries entries of the tile at
+// once, for all clients together (entry e of the tile belongs to the last
+// client whose first entry in the tile is at or before e); a tile with more
+// entries takes further rounds.
+//
+// Small tiles with one vector per thread per 256 parameters keep many
+// blocks in flight, which streams faster on this part than fewer blocks
+// holding larger chunks in registers, or persistent blocks that load the
+// next tile while they settle the current one (both measured slower).
+constexpr int kApplyTileShift = 12;
+constexpr uint32_t kApplyTileLen = 1u << kApplyTileShift;                          // parameters per block
+constexpr int kApplyTileThreads = 256;
+constexpr int kApplyTileVecs = (int)kApplyTileLen / 4 / kApplyTileThreads;        // 16-byte vectors per thread
+constexpr int kApplyTileEntries = 2;                                                // entries per thread per round
+constexpr uint32_t kApplyTileRound = (uint32_t)kApplyTileEntries * kApplyTileThreads;
+static_assert(kMaxPushes <= kWave, "one lane per client holds its range");
 
-static_assert(kStreamLoadThreads == 1 << kStreamLoadShift, "loading threads");
-static_assert(kStreamVecs == 16, "a loading thread's parameters are two bitmap words");
-static_assert(kStreamVecs * 4 * kStreamLoadThreads == (int)kStreamLen, "chunk split over the loading threads");
-static_assert(kStreamCap <= 0xFFFF && kStreamLen / 4 <= 0xFFFF, "staged positions and vectors fit 16 bits");
-
-struct StreamLds {
-    uint32_t rng[kMaxPushes][2];       // the chunk's [begin, end) in each client's list
-    uint32_t base[kMaxPushes + 1];     // first staged entry of each client
-    uint32_t total;                    // staged entries of all clients
-    uint32_t ncomp;                    // touched vectors
-    uint32_t seen[3 * kStreamWords];   // pushed at least once, more than once, sum started
-    uint16_t sofs[kStreamCap];         // staged entry's offset in the chunk
-    float sval[kStreamCap];            // staged entry's value (the running sum, in a first entry)
-    uint16_t vecpos[kStreamLen / 4];   // touched vector -> its place in comp
-    uint16_t compvec[kStreamCap];      // place in comp -> vector
-    uint16_t cfirst[4 * kStreamCap];   // per parameter of comp: the entry holding the sum of its clients
-    f4 comp[kStreamCap];               // the touched vectors
-};
-
-// The bitmaps are laid out by loading thread: the 64 parameters thread t
-// holds (vectors t + kStreamLoadThreads r) are words 2t and 2t + 1, with
-// parameter 4v + q at bit 4 (r mod 8) + q of word 2t + r / 8.
-__device__ __forceinline__ uint32_t stream_word(uint32_t off) {
-    const uint32_t v = off >> 2;
-    return 2u * (v & (kStreamLoadThreads - 1)) + (v >> (kStreamLoadShift + 3));
-}
-__device__ __forceinline__ uint32_t stream_bit(uint32_t off) {
-    return 1u << ((((off >> 2) >> kStreamLoadShift) & 7u) * 4u + (off & 3u));
+// push_val for a client index that differs between lanes: the client's sign
+// bits and centres are picked by comparing it with each client in turn.
+__device__ __forceinline__ float push_val_lanes(const ApplyArgs& a, uint32_t c, uint32_t pos, uint32_t i) {
+    const uint32_t* bits = a.bits[0];
+    const float* means = a.means[0];
+    for (uint32_t cc = 1; cc < a.C; ++cc) {
+        if (c == cc) {
+            bits = a.bits[cc];
+            means = a.means[cc];
+        }
+    }
+    uint32_t lo = 0, hi = a.T;  // tensor holding i
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (a.tensor_off[mid] <= i) lo = mid;
+        else hi = mid;
+    }
+    const uint32_t g = a.qkind == kQuantColumnMean ? a.colbase[lo] + (i - a.tensor_off[lo]) % a.columns[lo] : lo;
+    const uint32_t neg = (bits[pos >> 5] >> (pos & 31)) & 1u;
+    return means[2 * g + neg];
 }
 
-// The loading waves' side of a chunk.  Its barriers pair one for one with
-// the list waves' first four in k_apply_stream, and both sides leave at the
-// same points (no entry in the chunk; more entries than LDS holds, which the
-// list waves then apply alone); after the fourth the loading waves are done.
-__device__ __forceinline__ void stream_params(const ApplyArgs& a, StreamLds& L, uint32_t i_lo, uint32_t len,
-                                              bool whole, int tid) {
-    f4 pv[kStreamVecs];
-    // vector v = tid + kStreamLoadThreads r holds parameters i_lo + 4v .. + 3
+// The bounds table of the streaming form: row c holds, for every tile
+// boundary B_b (b * kApplyTileLen for b < tiles, n for b = tiles), the first
+// position in client c's list whose index is at least B_b.  With f(x) the
+// number of boundaries at or below x, entry e starts the boundaries in
+// [f(x_{e-1}), f(x_e)), the list's head [0, f(x_0)) starts at 0 and its tail
+// [f(x_last), tiles] at the list's length: one pass over the entries, no
+// search.  One row of blocks per client (blockIdx.y); the first tiles + 1
+// threads of a row fill the head and tail, the others one entry each.  (A
+// list out of order leaves some boundaries unwritten; readers clamp.)
+__global__ __launch_bounds__(kBlock) void k_apply_bounds(ApplyArgs a, uint32_t tiles) {
+    const uint32_t c = blockIdx.y;
+    const uint32_t m = a.nnz[c];
+    const uint32_t* list = a.idx[c];
+    uint32_t* row = const_cast<uint32_t*>(a.tab) + (size_t)c * a.tstride;
+    const uint64_t item = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+    const auto f = [&](uint32_t x) { return x < a.n ? (x >> kApplyTileShift) + 1u : tiles + 1u; };
+    if (item <= tiles) {
+        const uint32_t b = (uint32_t)item;
+        if (m == 0 || b < f(list[0])) row[b] = 0;
+        else if (b >= f(list[m - 1])) row[b] = m;
+        return;
+    }
+    const uint64_t e = item - tiles;  // 1 .. m - 1
+    if (e >= m) return;
+    const uint32_t hi = f(list[e]);
+    for (uint32_t b = f(list[e - 1]); b < hi; ++b) row[b] = (uint32_t)e;
+}
+
+__global__ __launch_bounds__(kApplyTileThreads) void k_apply_tile(ApplyArgs a) {
+    __shared__ __align__(16) float sum[kApplyTileLen];      // per parameter of the tile
+    __shared__ uint32_t touched[kApplyTileLen / 32];       // pushed at least once
+    const int tid = threadIdx.x, lane = lane_id();
+    const uint32_t b = blockIdx.x, C = a.C;
+    const uint32_t i_lo = b << kApplyTileShift;
+    const bool whole = (uint64_t)i_lo + kApplyTileLen <= a.n;  // the same in every thread
+    const uint32_t len = whole ? kApplyTileLen : a.n - i_lo;
+    // The tile's range in the list of client `lane` (lanes >= C: none), from
+    // the bounds table and clamped to the list, so that any table content
+    // stays inside it.  Every wave reads it, so no barrier is needed for it.
+    uint32_t r0 = 0, r1 = 0, nz = 0;
+    if ((uint32_t)lane < C) {
+        const uint32_t* row = a.tab + (size_t)lane * a.tstride + b;
+        r0 = row[0];
+        r1 = row[1];
+    }
+    // The tile's parameters: vector v = tid + kApplyTileThreads r holds
+    // parameters i_lo + 4v .. 4v + 3 (each row of vectors is one coalesced
+    // 4 KB read).
+    f4 pv[kApplyTileVecs];
     if (whole) {
 #pragma unroll
-        for (int r = 0; r < kStreamVecs; ++r)
-            pv[r] = *reinterpret_cast<const f4*>(a.p + i_lo + 4u * ((uint32_t)tid + (uint32_t)r * kStreamLoadThreads));
+        for (int r = 0; r < kApplyTileVecs; ++r)
+            pv[r] = *reinterpret_cast<const f4*>(a.p + i_lo + 4u * ((uint32_t)tid + (uint32_t)r * kApplyTileThreads));
     } else {
 #pragma unroll
-        for (int r = 0; r < kStreamVecs; ++r) {
-            const uint32_t o = 4u * ((uint32_t)tid + (uint32_t)r * kStreamLoadThreads);
+        for (int r = 0; r < kApplyTileVecs; ++r) {
+            const uint32_t o = 4u * ((uint32_t)tid + (uint32_t)r * kApplyTileThreads);
             pv[r] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int q = 0; q < 4; ++q)
                 if (o + q < len) pv[r][q] = a.p[i_lo + o + q];
         }
     }
-    for (int q = tid; q < 3 * kStreamWords; q += kStreamLoadThreads) L.seen[q] = 0;
-    if (tid == 0) L.ncomp = 0;
-    __syncthreads();  // 1: ranges read, bitmaps cleared
-    __syncthreads();  // 2: staging offsets
-    // (from LDS: a kernel argument read here would be waited for together
-    // with the LDS clearing above, and under a full memory queue it can miss)
-    const uint32_t total = L.total;
-    if (total == 0 || total > (uint32_t)kStreamCap) return;  // nothing here, or the list waves apply it entry by entry
-    __syncthreads();  // 3: entries staged
-    // This thread's touched vectors (a nonzero nibble of its 64 bits) go to
-    // consecutive places of comp, after those of the lanes below and of the
-    // waves that reserved theirs earlier.
-    const uint2 m = *reinterpret_cast<const uint2*>(L.seen + 2 * tid);
-    const auto nonzero_nibbles = [](uint32_t x) {
-        x |= x >> 1;
-        x |= x >> 2;
-        return (uint32_t)__popc(x & 0x11111111u);
-    };
-    const uint32_t cnt = nonzero_nibbles(m.x) + nonzero_nibbles(m.y);
+    for (uint32_t c = 0; c < C; ++c)
+        if ((uint32_t)lane == c) nz = a.nnz[c];
+    r0 = min(r0, nz);
+    r1 = min(r1, nz);
+    const uint32_t cnt = r1 > r0 ? r1 - r0 : 0u;
     const uint32_t incl = wave_incl_scan(cnt);
-    uint32_t wb = 0;
-    if (lane_id() == kWave - 1) wb = atomicAdd(&L.ncomp, incl);
-    uint32_t pos = lane_value(wb, kWave - 1) + incl - cnt;
+    const uint32_t base = incl - cnt;                        // the client's first entry in the tile
+    const uint32_t total = lane_value(incl, kWave - 1);      // the same in every wave
 #pragma unroll
-    for (int r = 0; r < kStreamVecs; ++r) {
-        const uint32_t nib = ((r < 8 ? m.x : m.y) >> ((r & 7) * 4)) & 0xFu;
-        if (nib == 0) continue;
-        const uint32_t v = (uint32_t)tid + (uint32_t)r * kStreamLoadThreads;
-        L.comp[pos] = pv[r];
-        L.vecpos[v] = (uint16_t)pos;
-        L.compvec[pos] = (uint16_t)v;
-        ++pos;
-    }
-    __syncthreads();  // 4: touched vectors in comp
-}
-
-// The bounds table of the streaming form: row c holds, for every chunk
-// boundary B_b (b * kStreamLen for b < chunks, n for b = chunks), the first
-// position in client c's list whose index is at least B_b.  With f(x) the
-// number of boundaries at or below x, entry e starts the boundaries in
-// [f(x_{e-1}), f(x_e)), the list's head [0, f(x_0)) starts at 0 and its tail
-// [f(x_last), chunks] at the list's length: one pass over the entries, no
-// search.  One row of blocks per client (blockIdx.y); the first chunks + 1
-// threads of a row fill the head and tail, the others one entry each.  (A
-// list out of order leaves some boundaries unwritten; readers clamp.)
-__global__ __launch_bounds__(kBlock) void k_apply_bounds(ApplyArgs a, uint32_t chunks) {
-    const uint32_t c = blockIdx.y;
-    const uint32_t m = a.nnz[c];
-    const uint32_t* list = a.idx[c];
-    uint32_t* row = const_cast<uint32_t*>(a.tab) + (size_t)c * a.tstride;
-    const uint64_t item = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    const auto f = [&](uint32_t x) { return x < a.n ? (x >> kStreamShift) + 1u : chunks + 1u; };
-    if (item <= chunks) {
-        const uint32_t b = (uint32_t)item;
-        if (m == 0 || b < f(list[0])) row[b] = 0;
-        else if (b >= f(list[m - 1])) row[b] = m;
-        return;
-    }
-    const uint64_t e = item - chunks;  // 1 .. m - 1
-    if (e >= m) return;
-    const uint32_t hi = f(list[e]);
-    for (uint32_t b = f(list[e - 1]); b < hi; ++b) row[b] = (uint32_t)e;
-}
-
-__global__ __launch_bounds__(kStreamThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_apply_stream(ApplyArgs a) {
-    __shared__ StreamLds L;
-    uint32_t* const more = L.seen + kStreamWords;
-    uint32_t* const started = L.seen + 2 * kStreamWords;
-    const int tid = threadIdx.x, lane = lane_id();
-    const uint32_t w = wave_index();
-    const uint32_t i_lo = blockIdx.x << kStreamShift;
-    const uint64_t e64 = (uint64_t)i_lo + kStreamLen;
-    const bool whole = e64 <= a.n;  // the same in every thread
-    const uint32_t i_hi = whole ? (uint32_t)e64 : a.n;
-    const uint32_t len = i_hi - i_lo;
-    // Waves 0 to 3 handle the lists and the others load the chunk: the first
-    // waves of a block issue first, so the bounds read is not queued behind
-    // the chunk's loads.
-    if (w >= (uint32_t)kStreamListWaves) {
-        stream_params(a, L, i_lo, len, whole, tid - (int)kListThreads);
-        return;
-    }
-    // The list waves.  The chunk's range in every list, from the bounds table
-    // (clamped to the list, so that any table content stays inside it).
-    const uint32_t lw = w, lt = (uint32_t)tid;
-    for (uint32_t c = lw; c < a.C; c += kStreamListWaves) {
-        if (lane < 2) {
-            const uint32_t v = a.tab[(size_t)c * a.tstride + blockIdx.x + (uint32_t)lane];
-            L.rng[c][lane] = v < a.nnz[c] ? v : a.nnz[c];
-        }
-    }
-    __syncthreads();  // 1
-    if (lw == 0) {
-        const uint32_t c = (uint32_t)lane;
-        const uint32_t r0 = c < a.C ? L.rng[c][0] : 0u, r1 = c < a.C ? L.rng[c][1] : 0u;
-        const uint32_t cnt = r1 > r0 ? r1 - r0 : 0u;
-        const uint32_t incl = wave_incl_scan(cnt);
-        if (c < a.C) L.base[c] = incl - cnt;
-        if (c == kWave - 1) L.base[a.C] = L.total = incl;
-    }
-    __syncthreads();  // 2
-    const uint32_t total = L.total;
-    if (total == 0) return;  // no entry in this chunk: nothing to write
-    if (total <= (uint32_t)kStreamCap) {
-        // each list wave stages the clients it handles, a batch of up to
-        // kStreamBatch entries per lane loaded at once
-        for (uint32_t c = lw; c < a.C; c += kStreamListWaves) {
-            const uint32_t r0 = L.rng[c][0], o = L.base[c], cnt = L.base[c + 1] - o;
-            for (uint32_t q0 = 0; q0 < cnt; q0 += kStreamBatch * kWave) {
-                uint32_t ii[kStreamBatch];
-                float vv[kStreamBatch];
+    for (int r = 0; r < kApplyTileVecs; ++r)
+        reinterpret_cast<f4*>(sum)[tid + r * kApplyTileThreads] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    if (tid < (int)(kApplyTileLen / 32)) touched[tid] = 0;
+    if (total == 0) return;  // nothing pushed here (block-uniform): nothing is written
+    for (uint32_t e0 = 0; e0 < total; e0 += kApplyTileRound) {
+        // this thread's entries e = e0 + tid + kApplyTileThreads k: offset in
+        // the tile, client and value, all loaded at once
+        uint32_t off[kApplyTileEntries], cl[kApplyTileEntries];
+        float val[kApplyTileEntries];
 #pragma unroll
-                for (int j = 0; j < kStreamBatch; ++j) {
-                    const uint32_t q = q0 + (uint32_t)lane + (uint32_t)j * kWave;
-                    ii[j] = q < cnt ? a.idx[c][r0 + q] : i_lo;
-                    if (a.qkind == 0) vv[j] = q < cnt ? a.val[c][r0 + q] : 0.0f;
-                }
-#pragma unroll
-                for (int j = 0; j < kStreamBatch; ++j) {
-                    const uint32_t q = q0 + (uint32_t)lane + (uint32_t)j * kWave;
-                    if (q >= cnt) continue;
-                    const uint32_t off = ii[j] - i_lo;
-                    const bool in = off < len;  // an index outside the chunk (a list out of order) is skipped
-                    L.sofs[o + q] = in ? (uint16_t)off : kStreamNoOff;
-                    L.sval[o + q] = a.qkind == 0 ? vv[j] : push_val(a, c, r0 + q, ii[j]);
-                    if (in) {
-                        const uint32_t wd = stream_word(off), bit = stream_bit(off);
-                        if (atomicOr(&L.seen[wd], bit) & bit) atomicOr(&more[wd], bit);
-                    }
+        for (int k = 0; k < kApplyTileEntries; ++k) {
+            const uint32_t e = e0 + (uint32_t)tid + (uint32_t)k * kApplyTileThreads;
+            uint32_t c = 0, first = 0, at = lane_value(r0, 0);
+            const uint32_t* ip = a.idx[0];
+            const float* vp = a.val[0];
+            for (uint32_t cc = 1; cc < C; ++cc) {
+                const uint32_t bc = lane_value(base, (int)cc);
+                if (e >= bc) {
+                    c = cc;
+                    first = bc;
+                    at = lane_value(r0, (int)cc);
+                    ip = a.idx[cc];
+                    vp = a.val[cc];
                 }
             }
+            cl[k] = kNoKey;
+            off[k] = kNoKey;
+            val[k] = 0.0f;
+            if (e < total) {
+                const uint32_t pos = at + (e - first);
+                const uint32_t i = ip[pos];
+                cl[k] = c;
+                off[k] = i - i_lo;  // outside the tile (a list out of order): skipped below
+                val[k] = a.qkind == 0 ? vp[pos] : push_val_lanes(a, c, pos, i);
+            }
         }
-        __syncthreads();  // 3
-        // This thread's entries (entry e = lt + kListThreads k), read at once.
-        uint32_t eo[kStreamPer], mw[kStreamPer];
-        float ev[kStreamPer];
-#pragma unroll
-        for (int k = 0; k < kStreamPer; ++k) {
-            const uint32_t e = lt + (uint32_t)k * kListThreads;
-            eo[k] = e < total ? L.sofs[e] : kStreamNoOff;
-            ev[k] = e < total ? L.sval[e] : 0.0f;
-        }
-#pragma unroll
-        for (int k = 0; k < kStreamPer; ++k)
-            mw[k] = eo[k] != kStreamNoOff ? more[stream_word(eo[k])] & stream_bit(eo[k]) : 0u;
-        __syncthreads();  // 4: the loading waves have copied the touched vectors and left
-        // A parameter pushed once: p - lr * (0 + value), in comp.
-#pragma unroll
-        for (int k = 0; k < kStreamPer; ++k) {
-            if (eo[k] == kStreamNoOff || mw[k] != 0) continue;
-            const uint32_t off = eo[k];
-            const uint32_t pos = min((uint32_t)L.vecpos[off >> 2], (uint32_t)kStreamCap - 1u);
-            const float sum = 0.0f + ev[k];
-            const float step = a.lr * sum;
-            L.comp[pos][off & 3u] = L.comp[pos][off & 3u] - step;
-        }
-        // Pushed by several clients: the sum in client turns.  The first
-        // client's entry starts it from +0 in its own value and is named in
-        // cfirst; each later client's entry adds its value there.
-        uint32_t first = 0;  // bit k: this thread's entry k started a sum
-        for (uint32_t t = 0; t < a.C; ++t) {
+        __syncthreads();  // sums cleared (first round), or the previous round's turns done
+        for (uint32_t t = 0; t < C; ++t) {
             if (t > 0) __syncthreads();  // the previous client's turn done
-            const uint32_t b0 = L.base[t], b1 = L.base[t + 1];
 #pragma unroll
-            for (int k = 0; k < kStreamPer; ++k) {
-                const uint32_t e = lt + (uint32_t)k * kListThreads, off = eo[k];
-                if (mw[k] == 0 || e < b0 || e >= b1) continue;
-                const uint32_t wd = stream_word(off), bit = stream_bit(off);
-                const uint32_t cp = 4u * min((uint32_t)L.vecpos[off >> 2], (uint32_t)kStreamCap - 1u) + (off & 3u);
-                if (!(atomicOr(&started[wd], bit) & bit)) {
-                    L.sval[e] = 0.0f + ev[k];
-                    L.cfirst[cp] = (uint16_t)e;
-                    first |= 1u << k;
-                } else {
-                    // (a first entry not yet named can only come from a list
-                    // holding an index twice; it is kept inside the staged entries)
-                    const uint32_t o = min((uint32_t)L.cfirst[cp], (uint32_t)kStreamCap - 1u);
-                    L.sval[o] = L.sval[o] + ev[k];
-                }
+            for (int k = 0; k < kApplyTileEntries; ++k) {
+                if (cl[k] != t || off[k] >= len) continue;
+                sum[off[k]] = sum[off[k]] + val[k];
+                atomicOr(&touched[off[k] >> 5], 1u << (off[k] & 31u));
             }
         }
-        __syncthreads();  // every sum complete
-#pragma unroll
-        for (int k = 0; k < kStreamPer; ++k) {
-            if (!((first >> k) & 1u)) continue;
-            const uint32_t e = lt + (uint32_t)k * kListThreads, off = eo[k];
-            const uint32_t pos = min((uint32_t)L.vecpos[off >> 2], (uint32_t)kStreamCap - 1u);
-            const float step = a.lr * L.sval[e];
-            L.comp[pos][off & 3u] = L.comp[pos][off & 3u] - step;
-        }
-        __syncthreads();  // comp final
-        const uint32_t ncomp = min(L.ncomp, (uint32_t)kStreamCap);
-        for (uint32_t pos = lt; pos < ncomp; pos += kListThreads) {
-            const uint32_t o = 4u * (uint32_t)L.compvec[pos];
-            const f4 v = L.comp[pos];
-            if (whole) {
-                *reinterpret_cast<f4*>(a.p + i_lo + o) = v;
-            } else {
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (o + q < len) a.p[i_lo + o + q] = v[q];
-            }
-        }
-        return;
     }
-    // More entries than LDS holds: entry by entry from the lists, as the
-    // scattered form's unstaged path (the loading waves have left).
-    for (uint32_t e = lt; e < total; e += kListThreads) {
-        uint32_t c = 0;
-        while (L.base[c + 1] <= e) ++c;  // client of entry e
-        const uint32_t q = e - L.base[c];
-        const uint32_t i = a.idx[c][L.rng[c][0] + q];
-        if (i - i_lo >= len) continue;  // outside the chunk: a list out of order
-        bool owner = true;
-        for (uint32_t cc = 0; cc < c && owner; ++cc) {
-            const uint32_t end = L.rng[cc][0] + (L.base[cc + 1] - L.base[cc]);
-            owner = find_u32(a.idx[cc], L.rng[cc][0], end, i) == end;
+    __syncthreads();  // every sum complete
+#pragma unroll
+    for (int r = 0; r < kApplyTileVecs; ++r) {
+        const uint32_t v = (uint32_t)tid + (uint32_t)r * kApplyTileThreads;
+        const uint32_t nib = (touched[v >> 3] >> ((v & 7u) * 4u)) & 0xFu;  // parameters 4v .. 4v + 3
+        if (nib == 0) continue;
+        const f4 s = reinterpret_cast<const f4*>(sum)[v];
+        f4 x = pv[r];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if ((nib >> q) & 1u) {
+                const float step = a.lr * s[q];
+                x[q] = x[q] - step;
+            }
         }
-        if (!owner) continue;
-        float s = 0.0f + push_val(a, c, L.rng[c][0] + q, i);
-        for (uint32_t cc = c + 1; cc < a.C; ++cc) {
-            const uint32_t end = L.rng[cc][0] + (L.base[cc + 1] - L.base[cc]);
-            const uint32_t hit = find_u32(a.idx[cc], L.rng[cc][0], end, i);
-            if (hit != end) s = s + push_val(a, cc, hit, i);
+        if (whole) {
+            *reinterpret_cast<f4*>(a.p + i_lo + 4u * v) = x;
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (4u * v + q < len) a.p[i_lo + 4u * v + q] = x[q];
         }
-        const float step = a.lr * s;
-        a.p[i] = a.p[i] - step;
     }
 }
 
@@ -531,28 +412,46 @@ __global__ __launch_bounds__(kStreamThreads) __attribute__((amdgpu_waves_per_eu(
 // streaming wherever the parameters are 16-byte aligned.
 static std::atomic<int> g_apply_form{0};
 
-// The streaming form's bounds table is allocated in stream order from a
-// memory pool the library keeps per device (created on first use, keeping
-// what it has reserved, so that later calls allocate without the driver).
-constexpr int kMaxDevices = 64;
-static std::mutex g_pool_mu;
-static hipMemPool_t g_pool[kMaxDevices] = {};
-
-static hipMemPool_t apply_pool(int dev) {
-    std::lock_guard<std::mutex> lk(g_pool_mu);
-    if (dev < 0 || dev >= kMaxDevices) return nullptr;
-    if (!g_pool[dev]) {
-        hipMemPoolProps props{};
-        props.allocType = hipMemAllocationTypePinned;
-        props.location.type = hipMemLocationTypeDevice;
-        props.location.id = dev;
-        hipMemPool_t p = nullptr;
-        if (hipMemPoolCreate(&p, &props) != hipSuccess) return nullptr;
-        uint64_t keep = ~0ull;
-        (void)hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep);
-        g_pool[dev] = p;
+// The streaming form's bounds table is kept per device and stream, and reused
+// by later calls on the same stream: work on one stream runs in order, so a
+// call's bounds pass cannot overwrite the table while an earlier call on that
+// stream still reads it, and calls on different streams use different tables.
+// (A per-call allocation in stream order from a memory pool, or an event
+// ordering the calls of all streams on one table, each cost about 5-6 us per
+// call.)  The per-thread default stream is one stream per host thread, so
+// its tables are kept per thread.  The mutex also keeps the two launches of
+// one call together when host threads share a stream.  A table grows when a
+// call needs more (hipFree of the old one waits for the device) and is kept
+// until the process ends.
+struct TableKey {
+    int dev;
+    uintptr_t stream;
+    std::thread::id thread;
+    bool operator<(const TableKey& o) const {
+        if (dev != o.dev) return dev < o.dev;
+        if (stream != o.stream) return stream < o.stream;
+        return thread < o.thread;
     }
-    return g_pool[dev];
+};
+static std::mutex g_tab_mu;
+static std::map<TableKey, std::pair<void*, size_t>> g_tables;
+
+// The table of the current device and stream st, at least `bytes` long, or
+// null if it cannot be allocated.  Called with g_tab_mu held.
+static uint32_t* stream_table(hipStream_t st, size_t bytes) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+    const TableKey key{dev, reinterpret_cast<uintptr_t>(st), st == hipStreamPerThread ? std::this_thread::get_id() : std::thread::id()};
+    auto& slot = g_tables[key];
+    if (slot.second < bytes) {
+        if (slot.first) (void)hipFree(slot.first);
+        slot = {nullptr, 0};
+        const size_t want = (bytes + 65535u) & ~(size_t)65535u;
+        void* q = nullptr;
+        if (hipMalloc(&q, want) != hipSuccess) return nullptr;
+        slot = {q, want};
+    }
+    return static_cast<uint32_t*>(slot.first);
 }
 
 void set_apply_form(int form) { g_apply_form.store(form); }
@@ -562,33 +461,28 @@ hipError_t launch_apply(const ApplyArgs& a, uint32_t max_nnz, hipStream_t st) {
     uint64_t total = 0;
     for (uint32_t c = 0; c < a.C; ++c) total += a.nnz[c];
     // Streaming reads every line of the shard: it pays once the entries touch
-    // most lines (one entry per 64 parameters touches about 40% of them), and
-    // while a chunk's entries usually fit its LDS (at most three quarters of
-    // kStreamCap on average; a fuller chunk is applied entry by entry).  Each
-    // list wave stages its clients one after another, so many clients stay
-    // with the scattered form.
+    // most lines (one entry per 64 parameters touches about 40% of them).
+    // Each client adds a turn of barriers to every tile and a comparison to
+    // every entry's client lookup, so many clients stay with the scattered
+    // form unless the form is forced.
     const int form = g_apply_form.load();
     const bool aligned = (reinterpret_cast<uintptr_t>(a.p) & 15u) == 0;
-    const bool dense = total * 64u >= a.n && total * kStreamLen <= (uint64_t)a.n * (kStreamCap * 3 / 4);
-    const bool stream = aligned && form != 1 && (form == 2 || (dense && a.C <= 2u * kStreamListWaves));
+    const bool dense = total * 64u >= a.n;
+    const bool stream = aligned && form != 1 && (form == 2 || (dense && a.C <= 8u));
     if (stream) {
-        const uint32_t chunks = (uint32_t)(((uint64_t)a.n + kStreamLen - 1) >> kStreamShift);
-        int dev = -1;
-        hipMemPool_t pool = hipGetDevice(&dev) == hipSuccess ? apply_pool(dev) : nullptr;
-        void* tab = nullptr;
-        const size_t bytes = (size_t)a.C * (chunks + 1u) * sizeof(uint32_t);
-        if (pool && hipMallocFromPoolAsync(&tab, bytes, pool, st) == hipSuccess) {
+        const uint32_t tiles = (uint32_t)(((uint64_t)a.n + kApplyTileLen - 1) >> kApplyTileShift);
+        std::lock_guard<std::mutex> lk(g_tab_mu);
+        uint32_t* tab = stream_table(st, (size_t)a.C * (tiles + 1u) * sizeof(uint32_t));
+        if (tab) {
             ApplyArgs b = a;
-            b.tab = static_cast<const uint32_t*>(tab);
-            b.tstride = chunks + 1u;
+            b.tab = tab;
+            b.tstride = tiles + 1u;
             uint64_t items = 0;  // head and tail, then the entries after the first
-            for (uint32_t c = 0; c < a.C; ++c) items = std::max<uint64_t>(items, chunks + 1u + (a.nnz[c] ? a.nnz[c] - 1u : 0u));
+            for (uint32_t c = 0; c < a.C; ++c) items = std::max<uint64_t>(items, tiles + 1u + (a.nnz[c] ? a.nnz[c] - 1u : 0u));
             hipLaunchKernelGGL(k_apply_bounds, dim3((uint32_t)((items + kBlock - 1) / kBlock), a.C), dim3(kBlock), 0, st, b,
-                               chunks);
-            hipLaunchKernelGGL(k_apply_stream, dim3(chunks), dim3(kStreamThreads), 0, st, b);
-            const hipError_t launched = hipGetLastError();
-            const hipError_t freed = hipFreeAsync(tab, st);
-            return launched != hipSuccess ? launched : freed;
+                               tiles);
+            hipLaunchKernelGGL(k_apply_tile, dim3(tiles), dim3(kApplyTileThreads), 0, st, b);
+            return hipGetLastError();
         }
         (void)hipGetLastError();  // no table: the scattered form below
     }

@@ -179,7 +179,7 @@ struct ApplyArgs {
     uint32_t T;
     const uint32_t* columns;     // [T]
     const uint32_t* colbase;     // [T + 1]
-    // streaming form: first position in each client's list of every chunk
+    // streaming form: first position in each client's list of every tile
     // boundary (row c at tab + c * tstride)
     const uint32_t* tab;
     uint32_t tstride;

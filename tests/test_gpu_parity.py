@@ -415,3 +415,29 @@ def test_apply_unaligned_parameters(apply_form):
         bad = torch.from_numpy(s.idx[0][::-1].copy().view(np.int32)).cuda()
         gd.apply_sparse(p, [bad], [torch.from_numpy(s.val[0]).cuda()], 1.0, validate=True)
     assert e.value.status == 1
+
+
+def test_apply_streams_keep_their_own_tables(apply_form):
+    """Applies on two streams, interleaved: each stream reuses the streaming form's bounds table of its
+    own stream, so calls in flight on the other stream cannot disturb it; every result equals the
+    oracle's bit for bit."""
+    shards = [wl.server_shard(n=300_001 + 4096 * j, clients=2 + j, nnz=9_000, dup_frac=0.2, seed=60 + j)
+              for j in range(2)]
+    want = [oracle.apply_sparse(s.params, s.idx, s.val, 1.0) for s in shards]
+    streams = [torch.cuda.Stream() for _ in shards]
+    dev = []
+    for s, st in zip(shards, streams):
+        with torch.cuda.stream(st):
+            dev.append((torch.from_numpy(s.params).cuda(), [torch.from_numpy(a.view(np.int32)).cuda() for a in s.idx],
+                        [torch.from_numpy(a).cuda() for a in s.val]))
+    torch.cuda.synchronize()
+    for rep in range(4):
+        ps = []
+        for (p0, ii, vv), st in zip(dev, streams):
+            with torch.cuda.stream(st):
+                p = p0.clone()
+                gd.apply_sparse(p, ii, vv, 1.0, stream=st)
+                ps.append(p)
+        torch.cuda.synchronize()
+        for p, w in zip(ps, want):
+            assert np.array_equal(p.cpu().numpy().view(np.uint32), w.view(np.uint32)), f"repeat {rep}"
