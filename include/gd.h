@@ -330,10 +330,10 @@ gd_status gd_debug_force_bracket(gd_ctx* ctx, int mode);
  * in this process, so that tests can run both forms at any density.  The
  * results do not change; only the work done does.  form 0: chosen per call
  * (streaming, which reads the whole shard in order, when params is 16-byte
- * aligned, the pushes hold between one entry per 64 parameters and 768 per
- * 16,384, and there are at most 8 of them; else scattered, which reads only
- * the pushed parameters); 1: scattered; 2: streaming wherever params is
- * 16-byte aligned.  A process-wide setting: it applies to every device and thread.
+ * aligned, the pushes hold at least one entry per 64 parameters, and there
+ * are at most 8 of them; else scattered, which reads only the pushed
+ * parameters); 1: scattered; 2: streaming wherever params is 16-byte
+ * aligned.  A process-wide setting: it applies to every device and thread.
  * GD_ERR_ARG for other forms.
  */
 gd_status gd_debug_apply_form(int form);
