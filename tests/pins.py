@@ -179,16 +179,18 @@ def pin_golden_apply(lib):
 
 
 def pin_brute_exhaustive(lib):
-    """Every vector of length <= 4 over {0, -0, +-1, +-2} and every k."""
-    alphabet = [0.0, -0.0, 1.0, -1.0, 2.0, -2.0]
-    for n in range(1, 5):
-        for vec in itertools.product(alphabet, repeat=n):
-            g = f32(vec)
+    """Every vector of length <= 4 over {0, -0, +-1, +-2}, and every vector of
+    length 5 to 7 over {0, -0, +1, -1} (ties and signed zeros everywhere), with
+    every k."""
+    for alphabet, sizes in (([0.0, -0.0, 1.0, -1.0, 2.0, -2.0], range(1, 5)), ([0.0, -0.0, 1.0, -1.0], range(5, 8))):
+        for n in sizes:
             z = np.zeros(n, np.float32)
-            for k in range(n + 1):
-                # smallest ppm giving exactly k of n
-                ppm = -(-k * 1_000_000 // n)
-                check_against_brute(lib, g, z, [0, n], ppm, False)
+            for vec in itertools.product(alphabet, repeat=n):
+                g = f32(vec)
+                for k in range(n + 1):
+                    # smallest ppm giving exactly k of n
+                    ppm = -(-k * 1_000_000 // n)
+                    check_against_brute(lib, g, z, [0, n], ppm, False)
 
 
 def pin_brute_random_ties(lib):
@@ -735,7 +737,6 @@ ALL_PINS = [
     pin_keep_count,
     pin_golden_compress,
     pin_golden_apply,
-    pin_brute_exhaustive,
     pin_brute_random_ties,
     pin_invariants_large,
     pin_special_cases,
@@ -754,4 +755,5 @@ ALL_PINS = [
     pin_sampled_statistics,
     pin_sampled_quant_full_sample_is_exact,
     pin_sampled_quant_sent_entries,
+    pin_brute_exhaustive,  # last: the slowest pin (about 10 s)
 ]
