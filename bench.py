@@ -67,6 +67,9 @@ def parse():
     ap.add_argument("--with-global-signmean", type=int, default=1,
                     help="on nmt_85k_per_tensor, also time the global threshold with sign-mean centres on the "
                          "same gradients (1, the default) or not (0)")
+    ap.add_argument("--with-shard", type=int, default=1,
+                    help="with the default NMT-shaped workload, also time the server step on the 37M shard "
+                         "(apply of four pushes, then the pull delta) and add it to the line")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB five times (the known-size "
                          "kernel that scales the HBM byte counters), then exit")
@@ -279,10 +282,11 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes": 4 * n, "launches": 5}), flush=True)
 
 
-def main_shard(args, torch, np, gd, wl):
+def main_shard(args, torch, np, gd, wl, emit=True):
     """The server side at one GPU's shard (37M parameters, 4 clients x 370,000 pushes,
     about 5% shared): per step, apply the four pushes (gd_apply_sparse), then compress the
-    pull delta p - p_last with a global threshold and a carried pull residual."""
+    pull delta p - p_last with a global threshold and a carried pull residual (or, with
+    --pull copy, from the last pulled copy).  Prints the JSON line (emit) and returns it."""
     sh = wl.server_shard(**wl.SHARD_FULL)
     N = sh.params.size
     print(f"[bench] shard of {N} parameters, {len(sh.idx)} pushes", file=sys.stderr, flush=True)
@@ -422,7 +426,9 @@ def main_shard(args, torch, np, gd, wl):
         line["parity_step0"] = bool(np.array_equal(p1.view(np.uint32), first_p.view(np.uint32)) and
                                     np.array_equal(o.idx, first_idx) and
                                     np.array_equal(want_state.view(np.uint32), first_res.view(np.uint32)))
-    print(json.dumps(line), flush=True)
+    if emit:
+        print(json.dumps(line), flush=True)
+    return line
 
 
 def oracle_quant_step_ok(np, o, idx, val, res, sign_bits, means, offsets, quant, columns=None):
@@ -620,6 +626,11 @@ def main():
     if w.name == "nmt_85k_per_tensor" and not sampled and args.quant == "workload" and args.with_global_signmean:
         extra = bench_global_signmean(args, torch, np, gd, wl, comp, grads, scrub)
         line["nmt_85k_global_signmean"] = extra["line"]
+    if w.name == "nmt_85k_per_tensor" and not sampled and args.quant == "workload" and args.with_shard:
+        # the server step (a7, a8) under the same protocol: its own JSON record, nested
+        sl = main_shard(args, torch, np, gd, wl, emit=False)
+        line["shard_37m_apply_pull"] = {key: sl[key] for key in ("value", "unit", "ms_per_step", "hbm_model_frac",
+                                                                  "timing", "config", "parity_step0") if key in sl}
     if args.cpu_baseline_seconds > 0:
         cb, first = cpu_baseline(w, grads_host, args.cpu_baseline_seconds, args.sample_ppm if sampled else 0, quant)
         line["cpu_baseline"] = cb
