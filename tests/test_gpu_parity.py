@@ -441,3 +441,56 @@ def test_apply_streams_keep_their_own_tables(apply_form):
         torch.cuda.synchronize()
         for p, w in zip(ps, want):
             assert np.array_equal(p.cpu().numpy().view(np.uint32), w.view(np.uint32)), f"repeat {rep}"
+
+
+def test_apply_per_thread_default_streams(apply_form):
+    """Applies from two host threads on the per-thread default stream (one HIP stream per thread behind
+    one handle): the streaming form keeps a bounds table per thread for it, and every result equals the
+    oracle's bit for bit."""
+    import ctypes
+    import threading
+
+    per_thread_stream = ctypes.c_void_p(2)  # hipStreamPerThread
+    shards = [wl.server_shard(n=250_003 + 8192 * j, clients=3, nnz=8_000, dup_frac=0.3, seed=70 + j)
+              for j in range(2)]
+    want = [oracle.apply_sparse(s.params, s.idx, s.val, 1.0) for s in shards]
+    dev = [(torch.from_numpy(s.params).cuda(), [torch.from_numpy(a.view(np.int32)).cuda() for a in s.idx],
+            [torch.from_numpy(a).cuda() for a in s.val]) for s in shards]
+    outs = [[None] * 4 for _ in shards]
+    torch.cuda.synchronize()
+    lib = gd.load()
+
+    errors = []
+
+    def run(j):
+        try:
+            apply_all(j)
+        except BaseException as e:  # reported by the main thread
+            errors.append((j, e))
+
+    def apply_all(j):
+        p0, ii, vv = dev[j]
+        ptr_i = (ctypes.c_void_p * len(ii))(*[a.data_ptr() for a in ii])
+        ptr_v = (ctypes.c_void_p * len(vv))(*[b.data_ptr() for b in vv])
+        nnz = (ctypes.c_uint64 * len(ii))(*[a.numel() for a in ii])
+        for rep in range(4):
+            p = outs[j][rep]
+            st = lib.gd_apply_sparse(p.data_ptr(), p.numel(), len(ii), ctypes.cast(ptr_i, ctypes.c_void_p),
+                                     ctypes.cast(ptr_v, ctypes.c_void_p), ctypes.cast(nnz, ctypes.c_void_p),
+                                     1.0, per_thread_stream)
+            assert st == 0
+
+    for j in range(len(shards)):
+        for rep in range(4):
+            outs[j][rep] = dev[j][0].clone()
+    torch.cuda.synchronize()
+    threads = [threading.Thread(target=run, args=(j,)) for j in range(len(shards))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for j, w in enumerate(want):
+        for rep in range(4):
+            assert np.array_equal(outs[j][rep].cpu().numpy().view(np.uint32), w.view(np.uint32)), (j, rep)
