@@ -206,6 +206,8 @@ def server_shard(
         n_dup = min(n_dup, union.size)
         dup = rng.choice(union, size=n_dup, replace=False) if n_dup else np.zeros(0, np.int64)
         need = nnz - n_dup
+        if need > n - union.size:
+            raise ValueError(f"client {c} needs {need} fresh indices but only {n - union.size} of {n} are left")
         fresh = np.zeros(0, dtype=np.int64)
         while fresh.size < need:
             cand = rng.integers(0, n, size=2 * (need - fresh.size) + 16, dtype=np.int64)
