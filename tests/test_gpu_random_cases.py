@@ -12,7 +12,8 @@ from parity import check_case
 
 pytestmark = pytest.mark.gpu
 
-CASES = 200
+CASES = 600
+BLOCKS = 12
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -58,9 +59,9 @@ def _case(case):
     return offsets, g, r, drop, per, quant, debug, columns
 
 
-@pytest.mark.parametrize("block", range(4))
+@pytest.mark.parametrize("block", range(BLOCKS))
 def test_random_cases(block):
-    for case in range(block * CASES // 4, (block + 1) * CASES // 4):
+    for case in range(block * CASES // BLOCKS, (block + 1) * CASES // BLOCKS):
         offsets, g, r, drop, per, quant, debug, columns = _case(case)
         comp = gd.Compressor(offsets)
         if columns is not None:
